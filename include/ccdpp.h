@@ -1,0 +1,159 @@
+/*
+ * ccdpp.h -- C ABI of the MI355X (gfx950) CCD++ library.
+ *
+ * CCD++ is the feature-wise cyclic coordinate descent for matrix
+ * factorization of Rodrigues, Jorge and Dutra, "Accelerating Recommender
+ * Systems using GPUs" (SAC'15), Section 3.2.2 (eq. 11-18, Algorithm 3), with
+ * the row/column data parallelism of Section 6 (eq. 19-23) and the device
+ * residency of Section 7 (Algorithm 7).
+ *
+ * Problem (Section 3, eq. 1): a sparse m x n rating matrix A is given as
+ * triplets (i, j, a_ij) on the observed set Omega.  The library finds
+ * W (m x k) and H (n x k) that minimise
+ *     sum_{(i,j) in Omega} (A_ij - w_i^T h_j)^2 + lambda (||W||_F^2 + ||H||_F^2)
+ * by sweeping the k features in order; for feature t it builds
+ * R-hat = R + wbar_t hbar_t^T on Omega (eq. 13), alternates the closed-form
+ * updates u_i = sum_j R-hat_ij v_j / (lambda + sum_j v_j^2) (eq. 15) and
+ * v_j = sum_i R-hat_ij u_i / (lambda + sum_i u_i^2) (eq. 16) inner_iters
+ * times, commits (wbar_t, hbar_t) = (u, v) (eq. 17) and updates the residual
+ * R = R-hat - u v^T (eq. 18).
+ *
+ * Conventions for every call:
+ *  - Indices are 0-based int32; m and n must be below 2^30 and nnz at most
+ *    2^31 - 1.
+ *  - Every array argument is HOST memory owned by the caller.  The library
+ *    copies what it needs during the call and keeps no pointer to it.
+ *  - Factor matrices at the boundary are row-major float32: W is m x k
+ *    (row i = w_i), H is n x k (row j = h_j).
+ *  - The handle owns all device memory (on the device that was current at
+ *    ccdpp_create) and is not thread-safe.
+ *  - Calls return CCDPP_OK (0) or a negative status.  Out-parameters are left
+ *    untouched on error.  After a device error the handle answers every
+ *    later call with CCDPP_ESTATE until it is destroyed.
+ *  - Calls that compute are blocking: they synchronise the handle's stream
+ *    before returning.
+ */
+#ifndef CCDPP_H
+#define CCDPP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ccdpp ccdpp_t;
+
+enum ccdpp_status {
+    CCDPP_OK = 0,
+    CCDPP_EINVAL = -1,   /* bad argument: size, range, NULL pointer, non-finite value */
+    CCDPP_EDUP = -2,     /* a position (i, j) occurs twice; Omega is a set (Section 3) */
+    CCDPP_ENOMEM = -3,   /* device or host allocation failed */
+    CCDPP_EDEVICE = -4,  /* HIP runtime error, or no usable gfx950 device */
+    CCDPP_ESTATE = -5    /* handle poisoned by an earlier device error, or NULL handle */
+};
+
+/*
+ * Create a factorization problem from training triplets (Section 3: A as
+ * triplets i, j, a_ij; Algorithms 3 and 7: W = 0, R = A).
+ *   m, n    : rows (users) and columns (items), 1 <= m, n < 2^30
+ *   k       : number of features, >= 1
+ *   lambda  : regularisation of eq. 1, finite and >= 0
+ *   nnz     : number of observed entries, 0 <= nnz <= 2^31 - 1
+ *   row,col : int32[nnz] positions (may be NULL when nnz == 0)
+ *   val     : float32[nnz] ratings, finite
+ *   seed    : seed of the initial H, drawn N(0, 0.01) (standard deviation
+ *             0.1) from a counter-based generator; ccdpp_set_factors
+ *             replaces it with caller-supplied values
+ *   out     : receives the handle
+ * Validation of sizes, ranges and values happens on the host before any HIP
+ * call.  Returns EDUP if a position repeats, ENOMEM or EDEVICE on device
+ * failure.  The device layout (row and column compressed copies of the
+ * residual, the map between them and the degree-binned schedule) is built on
+ * the device during this call.
+ */
+int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
+                 const int32_t *row, const int32_t *col, const float *val,
+                 uint64_t seed, ccdpp_t **out);
+
+/*
+ * Run outer_iters iterations of Algorithm 3 (each sweeps features t = 0..k-1
+ * in order), each feature with inner_iters alternations of eq. 15 then
+ * eq. 16.  outer_iters >= 0, inner_iters >= 1.  State (W, H, residual)
+ * persists across calls: two calls of 1 outer iteration give bitwise the
+ * same result as one call of 2.  Blocking.
+ */
+int ccdpp_run(ccdpp_t *h, int32_t outer_iters, int32_t inner_iters);
+
+/* Copy the factors out: W as m x k, H as n x k, row-major float32.  Either
+ * pointer may be NULL to skip it.  Blocking. */
+int ccdpp_get_factors(ccdpp_t *h, float *W, float *H);
+
+/* Replace the factors (row-major m x k and n x k, finite; either may be NULL
+ * to keep the current one) and rebuild the residual R = A - W H^T on Omega
+ * (Section 3.2) on the device.  Blocking. */
+int ccdpp_set_factors(ccdpp_t *h, const float *W, const float *H);
+
+/* Root mean squared error of the predictions w_i^T h_j against held-out
+ * triplets (Section 8: RMSE on the probe set; predictions are not clipped):
+ * sqrt(sum (a - w_i^T h_j)^2 / nnz), accumulated in float64 on the device in
+ * a fixed order.  nnz >= 1; indices must be in range.  Blocking. */
+int ccdpp_rmse(ccdpp_t *h, int64_t nnz, const int32_t *row, const int32_t *col,
+               const float *val, double *rmse_out);
+
+/* Training RMSE sqrt(sum_{Omega} R_ij^2 / nnz) of the current residual
+ * (float64 accumulation).  nnz must be >= 1.  Blocking. */
+int ccdpp_train_rmse(ccdpp_t *h, double *rmse_out);
+
+/* Residual R in the order of the triplets given to ccdpp_create
+ * (float32[nnz]).  Diagnostic.  Blocking. */
+int ccdpp_get_residual(ccdpp_t *h, float *R);
+
+/* Count the observed entries whose residual differs, bit for bit, between
+ * the row-compressed and the column-compressed device copies (0 when the two
+ * copies are consistent).  Diagnostic.  Blocking. */
+int ccdpp_check_consistency(ccdpp_t *h, int64_t *mismatches);
+
+/* Use this HIP stream (a hipStream_t, e.g. PyTorch's current stream) for all
+ * later work; NULL selects the handle's own stream.  The stream must belong
+ * to the handle's device and outlive its use. */
+int ccdpp_set_stream(ccdpp_t *h, void *hip_stream);
+
+/* Kernel timing.  When enabled, every kernel launch of ccdpp_run is bracketed
+ * by HIP events on the handle's stream and accumulated per kernel kind
+ * (CCDPP_K_*): launch count, summed device time in milliseconds, and the
+ * algorithmic bytes those launches had to move (index and value arrays,
+ * residual writes, row pointers, per-row scalars and outputs, and one read of
+ * each gathered vector).  Enabling clears the counters. */
+enum ccdpp_kernel_kind {
+    CCDPP_K_PASS_FUSED = 0,  /* first u- or v-pass of a feature: eq. 18 of the previous
+                                feature, eq. 13, then eq. 15 or eq. 16 */
+    CCDPP_K_PASS = 1,        /* later u- or v-passes: eq. 15 or eq. 16 on R-hat */
+    CCDPP_K_COMBINE = 2,     /* fixed-order combine of split heavy rows */
+    CCDPP_K_COMMIT = 3,      /* eq. 17 when inner_iters == 1 */
+    CCDPP_K_FLUSH = 4,       /* final eq. 18 and the training sum of squares */
+    CCDPP_K_COUNT = 5
+};
+int ccdpp_profile(ccdpp_t *h, int32_t enable);
+int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int64_t *launches, double *total_ms,
+                       double *algo_bytes);
+
+/* Sizes and schedule of the handle: fills up to `len` int64 values of
+ *   [0] m, [1] n, [2] nnz, [3] k, [4] device build time in microseconds,
+ *   [5] row-layout rows handled by whole workgroups, [6] of those split
+ *   over several workgroups, [7] row-layout workgroups per pass,
+ *   [8..10] the same three for the column layout, [11] device bytes held.
+ * Returns the number of values written. */
+int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
+
+/* Human-readable message of the last failure on this handle; with h == NULL,
+ * of the last failed ccdpp_create on this thread.  Never NULL. */
+const char *ccdpp_last_error(const ccdpp_t *h);
+
+/* Free the handle and all its device memory.  NULL is accepted. */
+void ccdpp_destroy(ccdpp_t *h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

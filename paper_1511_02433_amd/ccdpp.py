@@ -1,0 +1,241 @@
+"""Python binding of the C ABI in include/ccdpp.h (argument marshalling only).
+
+Every computation happens in libccdpp.so on the GPU.  The module-level
+functions carry the C names; the ``CCDPP`` class wraps a handle.  If the
+library has not been built, importing works but every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libccdpp.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "ccdpp.h")
+
+CCDPP_OK, CCDPP_EINVAL, CCDPP_EDUP, CCDPP_ENOMEM, CCDPP_EDEVICE, CCDPP_ESTATE = 0, -1, -2, -3, -4, -5
+STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "EDUP", -3: "ENOMEM", -4: "EDEVICE", -5: "ESTATE"}
+K_PASS_FUSED, K_PASS, K_COMBINE, K_COMMIT, K_FLUSH = range(5)
+KERNEL_KINDS = {K_PASS_FUSED: "ccd_pass_fused*", K_PASS: "ccd_pass", K_COMBINE: "ccd_combine",
+                K_COMMIT: "ccd_copy", K_FLUSH: "ccd_flush"}
+
+
+class CCDPPError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {message}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libccdpp.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1511_02433_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i64, i32, u64, dbl = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64,
+                                 ctypes.c_double)
+        sig = {
+            "ccdpp_create": ([i64, i64, i32, dbl, i64, P, P, P, u64, ctypes.POINTER(P)], ctypes.c_int),
+            "ccdpp_run": ([P, i32, i32], ctypes.c_int),
+            "ccdpp_get_factors": ([P, P, P], ctypes.c_int),
+            "ccdpp_set_factors": ([P, P, P], ctypes.c_int),
+            "ccdpp_rmse": ([P, i64, P, P, P, ctypes.POINTER(dbl)], ctypes.c_int),
+            "ccdpp_train_rmse": ([P, ctypes.POINTER(dbl)], ctypes.c_int),
+            "ccdpp_get_residual": ([P, P], ctypes.c_int),
+            "ccdpp_check_consistency": ([P, ctypes.POINTER(i64)], ctypes.c_int),
+            "ccdpp_set_stream": ([P, P], ctypes.c_int),
+            "ccdpp_profile": ([P, i32], ctypes.c_int),
+            "ccdpp_profile_read": ([P, i32, ctypes.POINTER(i64), ctypes.POINTER(dbl),
+                                    ctypes.POINTER(dbl)], ctypes.c_int),
+            "ccdpp_info": ([P, ctypes.POINTER(i64), i32], ctypes.c_int),
+            "ccdpp_last_error": ([P], ctypes.c_char_p),
+            "ccdpp_destroy": ([P], None),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def declared_symbols() -> list[str]:
+    """Function names declared in include/ccdpp.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(ccdpp_[a-z_]+)\s*\(", text)))
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(h, rc):
+    if rc < 0:
+        msg = lib().ccdpp_last_error(h)
+        raise CCDPPError(rc, msg.decode() if msg else "")
+    return rc
+
+
+# ---- C-named functions ---------------------------------------------------------------
+def ccdpp_create(m, n, k, lam, row, col, val, seed=0):
+    row = np.ascontiguousarray(row, dtype=np.int32)
+    col = np.ascontiguousarray(col, dtype=np.int32)
+    val = np.ascontiguousarray(val, dtype=np.float32)
+    if not (row.size == col.size == val.size):
+        raise ValueError("row, col and val must have the same length")
+    h = ctypes.c_void_p()
+    rc = lib().ccdpp_create(int(m), int(n), int(k), float(lam), int(row.size), _p(row), _p(col),
+                            _p(val), int(seed) & (2**64 - 1), ctypes.byref(h))
+    _check(None, rc)
+    return h
+
+
+def ccdpp_run(h, outer_iters, inner_iters):
+    _check(h, lib().ccdpp_run(h, int(outer_iters), int(inner_iters)))
+
+
+def ccdpp_get_factors(h, m, n, k):
+    W = np.empty((m, k), dtype=np.float32)
+    H = np.empty((n, k), dtype=np.float32)
+    _check(h, lib().ccdpp_get_factors(h, _p(W), _p(H)))
+    return W, H
+
+
+def ccdpp_set_factors(h, W=None, H=None):
+    W = None if W is None else np.ascontiguousarray(W, dtype=np.float32)
+    H = None if H is None else np.ascontiguousarray(H, dtype=np.float32)
+    _check(h, lib().ccdpp_set_factors(h, _p(W), _p(H)))
+
+
+def ccdpp_rmse(h, row, col, val):
+    row = np.ascontiguousarray(row, dtype=np.int32)
+    col = np.ascontiguousarray(col, dtype=np.int32)
+    val = np.ascontiguousarray(val, dtype=np.float32)
+    out = ctypes.c_double()
+    _check(h, lib().ccdpp_rmse(h, int(row.size), _p(row), _p(col), _p(val), ctypes.byref(out)))
+    return out.value
+
+
+def ccdpp_train_rmse(h):
+    out = ctypes.c_double()
+    _check(h, lib().ccdpp_train_rmse(h, ctypes.byref(out)))
+    return out.value
+
+
+def ccdpp_get_residual(h, nnz):
+    R = np.empty(nnz, dtype=np.float32)
+    _check(h, lib().ccdpp_get_residual(h, _p(R)))
+    return R
+
+
+def ccdpp_check_consistency(h):
+    out = ctypes.c_int64()
+    _check(h, lib().ccdpp_check_consistency(h, ctypes.byref(out)))
+    return out.value
+
+
+def ccdpp_set_stream(h, stream_ptr):
+    _check(h, lib().ccdpp_set_stream(h, ctypes.c_void_p(stream_ptr) if stream_ptr else None))
+
+
+def ccdpp_profile(h, enable):
+    _check(h, lib().ccdpp_profile(h, 1 if enable else 0))
+
+
+def ccdpp_profile_read(h, kind):
+    n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
+    _check(h, lib().ccdpp_profile_read(h, int(kind), ctypes.byref(n), ctypes.byref(ms),
+                                       ctypes.byref(b)))
+    return n.value, ms.value, b.value
+
+
+INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "row_block_rows", "row_split_rows", "row_grid",
+               "col_block_rows", "col_split_rows", "col_grid", "device_bytes")
+
+
+def ccdpp_info(h):
+    buf = (ctypes.c_int64 * len(INFO_FIELDS))()
+    w = _check(h, lib().ccdpp_info(h, buf, len(INFO_FIELDS)))
+    return {INFO_FIELDS[i]: int(buf[i]) for i in range(w)}
+
+
+def ccdpp_last_error(h=None):
+    msg = lib().ccdpp_last_error(h)
+    return msg.decode() if msg else ""
+
+
+def ccdpp_destroy(h):
+    lib().ccdpp_destroy(h)
+
+
+# ---- convenience wrapper ---------------------------------------------------------------
+class CCDPP:
+    """A CCD++ problem held on the current HIP device."""
+
+    def __init__(self, m, n, k, lam, row, col, val, seed=0):
+        self.m, self.n, self.k, self.lam = int(m), int(n), int(k), float(lam)
+        self.nnz = int(np.asarray(row).size)
+        self._h = ccdpp_create(m, n, k, lam, row, col, val, seed)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            ccdpp_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def run(self, outer_iters, inner_iters):
+        ccdpp_run(self._h, outer_iters, inner_iters)
+
+    def factors(self):
+        return ccdpp_get_factors(self._h, self.m, self.n, self.k)
+
+    def set_factors(self, W=None, H=None):
+        ccdpp_set_factors(self._h, W, H)
+
+    def rmse(self, row, col, val):
+        return ccdpp_rmse(self._h, row, col, val)
+
+    def train_rmse(self):
+        return ccdpp_train_rmse(self._h)
+
+    def residual(self):
+        return ccdpp_get_residual(self._h, self.nnz)
+
+    def check_consistency(self):
+        return ccdpp_check_consistency(self._h)
+
+    def set_stream(self, stream_ptr):
+        ccdpp_set_stream(self._h, stream_ptr)
+
+    def use_torch_stream(self):
+        """Run on PyTorch's current HIP stream (PyTorch is used for streams only)."""
+        import torch
+        self.set_stream(torch.cuda.current_stream().cuda_stream)
+
+    def profile(self, enable=True):
+        ccdpp_profile(self._h, enable)
+
+    def profile_read(self, kind):
+        return ccdpp_profile_read(self._h, kind)
+
+    def info(self):
+        return ccdpp_info(self._h)

@@ -1,0 +1,162 @@
+"""GPU path against the fp64 CPU oracle on identical seeded inputs.
+
+Tolerances: W and H within 1e-3 (per-feature scaled max relative error) after
+one outer iteration, and |delta RMSE| <= 1e-4 after the full run.  The GPU keeps
+the residual in fp32 (as the paper's float version does) and sums in fp64, so it
+is not bitwise equal to the oracle.
+"""
+import numpy as np
+import pytest
+
+from oracle import Oracle
+from paper_1511_02433_amd import synth
+from paper_1511_02433_amd.ccdpp import CCDPP
+from gpu_util import colscaled_max_rel_err
+
+pytestmark = pytest.mark.gpu
+
+W_TOL = 1e-3
+RMSE_TOL = 1e-4
+
+
+def _pair(m, n, k, lam, row, col, val, H0, threads=0):
+    g = CCDPP(m, n, k, lam, row, col, val)
+    g.set_factors(np.zeros((m, k), np.float32), H0)
+    o = Oracle(m, n, k, lam, row, col, val, H0, threads=threads)
+    return g, o
+
+
+def test_tiny_parity_one_outer_and_full_run():
+    ds = synth.load("tiny")
+    w = ds.workload
+    print(f"case: tiny {w.describe()}", flush=True)
+    g, o = _pair(w.m, w.n, w.k, w.lam, ds.row, ds.col, ds.val, ds.H0)
+    g.run(1, w.inner)
+    o.run(1, w.inner)
+    Wg, Hg = g.factors()
+    Wo, Ho = o.factors()
+    ew, eh = colscaled_max_rel_err(Wg, Wo), colscaled_max_rel_err(Hg, Ho)
+    print(f"tiny after 1 outer: W err {ew:.3e}  H err {eh:.3e}")
+    assert ew <= W_TOL and eh <= W_TOL
+    g.run(w.outer - 1, w.inner)
+    o.run(w.outer - 1, w.inner)
+    tr_g, tr_o = g.train_rmse(), o.train_rmse()
+    te_g = g.rmse(ds.test_row, ds.test_col, ds.test_val)
+    te_o = o.test_rmse(ds.test_row, ds.test_col, ds.test_val)
+    print(f"tiny full run: train {tr_g:.6f} vs {tr_o:.6f}; test {te_g:.6f} vs {te_o:.6f}")
+    assert abs(tr_g - tr_o) <= RMSE_TOL
+    assert abs(te_g - te_o) <= RMSE_TOL
+    assert g.check_consistency() == 0
+
+
+# Row lengths at every edge of the scheduling classes: lane groups of 1..64 lanes
+# (up to 8 or 16 entries per lane), one workgroup per row up to 32768 entries, and
+# rows split over several workgroups beyond that.
+EDGE_LENGTHS = [0, 1, 2, 7, 8, 9, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256,
+                257, 511, 512, 513, 1023, 1024, 1025, 4095, 4096, 4097, 32767, 32768, 32769,
+                70001]
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("inner", [1, 2])
+def test_every_schedule_class(transpose, inner):
+    n_other = 70_001 + 5
+    row, col, val, H0 = synth.lengths_problem(EDGE_LENGTHS * 2, n_other, 3, seed=17)
+    m, n = len(EDGE_LENGTHS) * 2, n_other
+    if transpose:
+        row, col = col, row
+        m, n = n, m
+        H0 = (np.random.default_rng(5).standard_normal((n, 3)) * 0.1).astype(np.float32)
+    print(f"case: edge lengths transpose={transpose} inner={inner} m={m} n={n} nnz={row.size}",
+          flush=True)
+    g, o = _pair(m, n, 3, 0.1, row, col, val, H0)
+    g.run(1, inner)
+    o.run(1, inner)
+    Wg, Hg = g.factors()
+    Wo, Ho = o.factors()
+    ew, eh = colscaled_max_rel_err(Wg, Wo), colscaled_max_rel_err(Hg, Ho)
+    print(f"W err {ew:.3e}  H err {eh:.3e}")
+    assert ew <= W_TOL and eh <= W_TOL
+    # Empty rows / columns get a zero coordinate.
+    assert np.all(Wg[np.bincount(row, minlength=m) == 0] == 0)
+    assert np.all(Hg[np.bincount(col, minlength=n) == 0] == 0)
+    assert g.check_consistency() == 0
+    R = g.residual().astype(np.float64)
+    np.testing.assert_allclose(R, o.residual(), rtol=0, atol=1e-4 * np.abs(val).max())
+
+
+def test_determinism_and_split_runs_bitwise():
+    ds = synth.load("tiny")
+    w = ds.workload
+    print("case: tiny determinism", flush=True)
+    a = CCDPP(w.m, w.n, w.k, w.lam, ds.row, ds.col, ds.val)
+    b = CCDPP(w.m, w.n, w.k, w.lam, ds.row, ds.col, ds.val)
+    for h in (a, b):
+        h.set_factors(np.zeros((w.m, w.k), np.float32), ds.H0)
+    a.run(2, 3)
+    b.run(1, 3)
+    b.run(1, 3)
+    Wa, Ha = a.factors()
+    Wb, Hb = b.factors()
+    assert np.array_equal(Wa, Wb) and np.array_equal(Ha, Hb)
+    assert np.array_equal(a.residual(), b.residual())
+    c = CCDPP(w.m, w.n, w.k, w.lam, ds.row, ds.col, ds.val)
+    c.set_factors(np.zeros((w.m, w.k), np.float32), ds.H0)
+    c.run(2, 3)
+    Wc, Hc = c.factors()
+    assert np.array_equal(Wa, Wc) and np.array_equal(Ha, Hc)
+
+
+def test_residual_is_a_minus_wht_and_factors_roundtrip():
+    row, col, val, H0 = synth.small_random(300, 200, 9000, 5, seed=23)
+    print("case: residual definition 300x200", flush=True)
+    g = CCDPP(300, 200, 5, 0.05, row, col, val)
+    g.run(2, 2)
+    W, H = g.factors()
+    R = g.residual().astype(np.float64)
+    ref = val.astype(np.float64) - np.einsum("ek,ek->e", W[row].astype(np.float64),
+                                             H[col].astype(np.float64))
+    assert np.abs(R - ref).max() <= 1e-5 * np.abs(val).max()
+    # set_factors / get_factors round trip is exact, and the rebuilt residual agrees.
+    g.set_factors(W, H)
+    W2, H2 = g.factors()
+    assert np.array_equal(W, W2) and np.array_equal(H, H2)
+    R2 = g.residual().astype(np.float64)
+    assert np.abs(R2 - ref).max() <= 1e-6 * np.abs(val).max()
+    assert g.check_consistency() == 0
+
+
+def test_rmse_kernels_match_their_definition():
+    row, col, val, H0 = synth.small_random(500, 400, 20000, 6, seed=29)
+    print("case: rmse 500x400", flush=True)
+    g = CCDPP(500, 400, 6, 0.1, row[:18000], col[:18000], val[:18000])
+    g.run(1, 2)
+    W, H = g.factors()
+    pred = np.einsum("ek,ek->e", W[row].astype(np.float64), H[col].astype(np.float64))
+    err = val.astype(np.float64) - pred
+    te = np.sqrt(np.mean(err[18000:] ** 2))
+    tr = np.sqrt(np.mean(err[:18000] ** 2))
+    assert abs(g.rmse(row[18000:], col[18000:], val[18000:]) - te) <= 1e-9 * te
+    assert abs(g.train_rmse() - tr) <= 1e-5 * tr
+
+
+def test_zero_lambda_and_empty_rows():
+    row = np.array([0, 0, 1, 1, 3, 4], dtype=np.int32)
+    col = np.array([0, 1, 1, 2, 0, 4], dtype=np.int32)
+    val = np.array([1.0, -2.0, 0.5, 3.0, 1.5, 2.0], dtype=np.float32)
+    H0 = np.full((6, 2), 0.1, dtype=np.float32)
+    print("case: lambda 0 and 0.1 with empty rows", flush=True)
+    # lambda = 0: rows 2, 5 and columns 3, 5 are empty, their coordinates are 0, nothing is NaN.
+    # (With lambda = 0 the second feature of a single-entry row is a ratio of two rounding
+    # residues, so values are compared with the oracle only for lambda > 0.)
+    for lam in (0.0, 0.1):
+        g, o = _pair(6, 6, 2, lam, row, col, val, H0)
+        g.run(2, 2)
+        o.run(2, 2)
+        Wg, Hg = g.factors()
+        assert np.all(np.isfinite(Wg)) and np.all(np.isfinite(Hg))
+        assert np.all(Wg[[2, 5]] == 0) and np.all(Hg[[3, 5]] == 0)
+        if lam > 0:
+            Wo, Ho = o.factors()
+            assert colscaled_max_rel_err(Wg, Wo) <= W_TOL
+            assert colscaled_max_rel_err(Hg, Ho) <= W_TOL
