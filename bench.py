@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Throughput of the CCD++ sweep on one MI355X.
+
+A step is one outer iteration of Algorithm 3 on the whole workload: all k
+features, each with inner_iters u/v alternations, the fused residual
+bookkeeping, and the final residual flush with the training sum of squares
+(one ccdpp_run(1, inner) call).  Inputs are resident in HBM before timing.
+
+  value    = 2 * inner * k * nnz / (seconds per step) / 1e9   [G nonzero visits / s]
+  roofline = algorithmic bytes of the dominant kernel per launch / its mean
+             duration (HIP events on the library's stream, inside the timed
+             region), against 8 TB/s HBM peak
+  cpu_baseline = the fp64 oracle on the host cores, on a bounded sample of
+             features of the same matrix
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+KERNEL_NAMES = {0: "ccd_pass_fused", 1: "ccd_pass", 2: "ccd_combine", 3: "ccd_copy", 4: "ccd_flush"}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("sweep.hip", "ccdpp_internal.hpp"):
+        with open(os.path.join(ROOT, "paper_1511_02433_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel source; otherwise None."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        t = json.load(f)
+    if t.get("source_digest") != source_digest():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(ds, k, inner, budget_s, threads):
+    import numpy as np
+    from oracle import Oracle
+
+    w = ds.workload
+    log(f"cpu baseline: building the oracle on {w.name} ({threads} threads)")
+    o = Oracle(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val, ds.h0(k), threads=threads)
+    done = 0
+    t0 = time.perf_counter()
+    while done < k:
+        o.rank(done, inner, debug=False)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    o.close()
+    visits = 2.0 * inner * w.nnz * done
+    log(f"cpu baseline: {done} features x {inner} inner in {dt:.2f}s")
+    return {"value": visits / dt / 1e9, "unit": "Gnnz/s", "cores": threads, "kind": "oracle",
+            "sample": f"features 0..{done - 1} of one outer iteration ({done} of {k} features, "
+                      f"inner {inner}) on the full {w.name} matrix, fp64 oracle, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="large", choices=["tiny", "medium", "large", "vlarge"])
+    ap.add_argument("--k", type=int, default=0, help="override the number of features")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1511_02433_amd import synth
+    from paper_1511_02433_amd.ccdpp import CCDPP
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    ds = synth.load(args.workload, verbose=True)
+    w = ds.workload
+    k = args.k or w.k
+    inner = w.inner
+    log(f"workload {w.describe()} (k={k})")
+
+    g = CCDPP(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val)
+    g.use_torch_stream()
+    g.set_factors(np.zeros((w.m, k), np.float32), ds.h0(k))
+    info = g.info()
+    log(f"device build {info['build_us'] / 1e3:.1f} ms; schedule {info}")
+
+    for _ in range(args.warmup):
+        g.run(1, inner)
+    torch.cuda.synchronize()
+
+    def timed(steps, prof):
+        g.profile(prof)
+        s = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s)
+        for _ in range(steps):
+            g.run(1, inner)
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    prof = not args.no_prof
+    ms = timed(args.steps, prof)
+    kinds = {}
+    per_layout = {}
+    if prof:
+        for kind, name in KERNEL_NAMES.items():
+            n, tot, b = g.profile_read(kind)
+            if n:
+                kinds[name] = {"launches": n, "mean_us": tot / n * 1e3, "total_ms": tot,
+                               "algo_bytes_per_launch": b / n, "gbs": b / (tot * 1e-3) / 1e9}
+                for lay, lname in ((0, "rows"), (1, "cols")):
+                    n2, t2, b2 = g.profile_read(kind, lay)
+                    if n2:
+                        per_layout[f"{name}/{lname}"] = {
+                            "launches": n2, "mean_us": round(t2 / n2 * 1e3, 2),
+                            "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
+    g.profile(False)
+    ms_plain = timed(max(2, args.steps // 2), False) if prof else ms
+    visits = 2.0 * inner * k * w.nnz
+    value = visits / (ms * 1e-3) / 1e9
+    log(f"{ms:.3f} ms/step with kernel events, {ms_plain:.3f} ms/step without; {value:.1f} Gnnz/s")
+
+    roofline = None
+    if kinds:
+        dom = max(kinds, key=lambda kk: kinds[kk]["total_ms"])
+        d = kinds[dom]
+        achieved = d["algo_bytes_per_launch"] / (d["mean_us"] * 1e-6) / 1e9
+        roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": stored_traffic(dom, w.name)}
+    train_rmse = g.train_rmse()
+    test_rmse = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
+    model_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / args.steps \
+        if kinds else None
+    g.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = min(16, os.cpu_count() or 1)
+        cpu = cpu_baseline(synth.load(args.workload), k, inner, args.cpu_budget, threads)
+
+    out = {
+        "metric": "CCD++ nonzeros/sec (G/s) + achieved HBM GB/s vs peak; s per outer iter",
+        "value": round(value, 3),
+        "unit": "Gnnz/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "s_per_outer_iter": round(ms * 1e-3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.m}x{w.n}, nnz={w.nnz}, k={k}, lambda={w.lam}, "
+                               f"inner={inner}; step = 1 outer iteration",
+                   "m": w.m, "n": w.n, "nnz": w.nnz, "k": k, "inner_iters": inner},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "model_bytes_per_step": model_bytes,
+        "model_gbs": round(model_bytes / (ms * 1e-3) / 1e9, 1) if model_bytes else None,
+        "ms_per_step_without_kernel_events": round(ms_plain, 4),
+        "kernels": kinds,
+        "kernels_by_layout": per_layout,
+        "train_rmse": train_rmse,
+        "test_rmse": test_rmse,
+        "device_build_ms": info["build_us"] / 1e3,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -77,6 +77,30 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
                  uint64_t seed, ccdpp_t **out);
 
 /*
+ * Tuning and testing knobs of the device layout (all zero = automatic, which
+ * is what ccdpp_create uses).  Index 0 is the user-major copy read by the
+ * u-passes of eq. 15, index 1 the item-major copy read by the v-passes of
+ * eq. 16.
+ *   gather_mode : 0 automatic; 1 gather the other side's coordinates from
+ *                 global memory; 2 stage them in LDS, cut into tiles of
+ *                 tile_width columns when they do not fit
+ *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
+ *                 163840 / (4 * v) where v = 2 for index 0 and 3 for index 1
+ *   workgroups  : persistent workgroups per pass (0: two per compute unit)
+ * Results differ between layouts only by floating-point summation order.
+ */
+typedef struct ccdpp_options {
+    int32_t gather_mode[2];
+    int32_t tile_width[2];
+    int32_t workgroups;
+} ccdpp_options_t;
+
+/* ccdpp_create with explicit layout options (opts may be NULL). */
+int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
+                    const int32_t *row, const int32_t *col, const float *val,
+                    uint64_t seed, const ccdpp_options_t *opts, ccdpp_t **out);
+
+/*
  * Run outer_iters iterations of Algorithm 3 (each sweeps features t = 0..k-1
  * in order), each feature with inner_iters alternations of eq. 15 then
  * eq. 16.  outer_iters >= 0, inner_iters >= 1.  State (W, H, residual)
@@ -121,10 +145,12 @@ int ccdpp_set_stream(ccdpp_t *h, void *hip_stream);
 
 /* Kernel timing.  When enabled, every kernel launch of ccdpp_run is bracketed
  * by HIP events on the handle's stream and accumulated per kernel kind
- * (CCDPP_K_*): launch count, summed device time in milliseconds, and the
- * algorithmic bytes those launches had to move (index and value arrays,
- * residual writes, row pointers, per-row scalars and outputs, and one read of
- * each gathered vector).  Enabling clears the counters. */
+ * (CCDPP_K_*) and per residual copy (layout 0: row-compressed, the u-passes of
+ * eq. 15; layout 1: column-compressed, the v-passes of eq. 16; -1: both):
+ * launch count, summed device time in milliseconds, and the algorithmic bytes
+ * those launches had to move (index and value arrays, residual writes, row
+ * pointers, per-row scalars and outputs, and one read of each gathered
+ * vector).  Enabling or disabling clears the counters. */
 enum ccdpp_kernel_kind {
     CCDPP_K_PASS_FUSED = 0,  /* first u- or v-pass of a feature: eq. 18 of the previous
                                 feature, eq. 13, then eq. 15 or eq. 16 */
@@ -135,14 +161,15 @@ enum ccdpp_kernel_kind {
     CCDPP_K_COUNT = 5
 };
 int ccdpp_profile(ccdpp_t *h, int32_t enable);
-int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int64_t *launches, double *total_ms,
-                       double *algo_bytes);
+int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launches,
+                       double *total_ms, double *algo_bytes);
 
 /* Sizes and schedule of the handle: fills up to `len` int64 values of
  *   [0] m, [1] n, [2] nnz, [3] k, [4] device build time in microseconds,
- *   [5] row-layout rows handled by whole workgroups, [6] of those split
- *   over several workgroups, [7] row-layout workgroups per pass,
- *   [8..10] the same three for the column layout, [11] device bytes held.
+ *   [5] user-major copy gather mode (1 global memory, 2 LDS-staged),
+ *   [6] its number of tiles P, [7] tile width T, [8] persistent workgroups per
+ *   pass, [9] row segments, [10..14] the same five for the item-major copy,
+ *   [15] device bytes held.
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

@@ -98,8 +98,13 @@ class Oracle:
             raise ValueError("oracle_run: bad arguments")
         return tr
 
-    def rank(self, t: int, inner: int):
-        """One rank update; returns (trace, rhat in input order, u history, v history)."""
+    def rank(self, t: int, inner: int, debug: bool = True):
+        """One rank update; returns (trace, rhat in input order, u history, v history),
+        or None when debug is False (no side outputs are produced)."""
+        if not debug:
+            if lib().oracle_rank(self._h, int(t), int(inner), None, None, None, None):
+                raise ValueError("oracle_rank: bad arguments")
+            return None
         tr = np.zeros(1 + 2 * inner)
         rh = np.zeros(self.nnz)
         uh = np.zeros((inner, self.m))

@@ -23,6 +23,21 @@ KERNEL_KINDS = {K_PASS_FUSED: "ccd_pass_fused*", K_PASS: "ccd_pass", K_COMBINE: 
                 K_COMMIT: "ccd_copy", K_FLUSH: "ccd_flush"}
 
 
+class Options(ctypes.Structure):
+    """ccdpp_options_t: layout knobs (0 = automatic).  Index 0 is the user-major copy,
+    1 the item-major copy.  gather_mode: 1 global memory, 2 LDS-staged."""
+    _fields_ = [("gather_mode", ctypes.c_int32 * 2), ("tile_width", ctypes.c_int32 * 2),
+                ("workgroups", ctypes.c_int32)]
+
+
+def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0) -> Options:
+    o = Options()
+    o.gather_mode[0], o.gather_mode[1] = gather_mode
+    o.tile_width[0], o.tile_width[1] = tile_width
+    o.workgroups = workgroups
+    return o
+
+
 class CCDPPError(RuntimeError):
     def __init__(self, code: int, message: str):
         super().__init__(f"{STATUS_NAMES.get(code, code)}: {message}")
@@ -43,6 +58,8 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_double)
         sig = {
             "ccdpp_create": ([i64, i64, i32, dbl, i64, P, P, P, u64, ctypes.POINTER(P)], ctypes.c_int),
+            "ccdpp_create_ex": ([i64, i64, i32, dbl, i64, P, P, P, u64, ctypes.POINTER(Options),
+                                 ctypes.POINTER(P)], ctypes.c_int),
             "ccdpp_run": ([P, i32, i32], ctypes.c_int),
             "ccdpp_get_factors": ([P, P, P], ctypes.c_int),
             "ccdpp_set_factors": ([P, P, P], ctypes.c_int),
@@ -52,7 +69,7 @@ def lib() -> ctypes.CDLL:
             "ccdpp_check_consistency": ([P, ctypes.POINTER(i64)], ctypes.c_int),
             "ccdpp_set_stream": ([P, P], ctypes.c_int),
             "ccdpp_profile": ([P, i32], ctypes.c_int),
-            "ccdpp_profile_read": ([P, i32, ctypes.POINTER(i64), ctypes.POINTER(dbl),
+            "ccdpp_profile_read": ([P, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(dbl),
                                     ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_info": ([P, ctypes.POINTER(i64), i32], ctypes.c_int),
             "ccdpp_last_error": ([P], ctypes.c_char_p),
@@ -86,14 +103,22 @@ def _check(h, rc):
 
 # ---- C-named functions ---------------------------------------------------------------
 def ccdpp_create(m, n, k, lam, row, col, val, seed=0):
+    return ccdpp_create_ex(m, n, k, lam, row, col, val, seed, None)
+
+
+def ccdpp_create_ex(m, n, k, lam, row, col, val, seed=0, opts=None):
     row = np.ascontiguousarray(row, dtype=np.int32)
     col = np.ascontiguousarray(col, dtype=np.int32)
     val = np.ascontiguousarray(val, dtype=np.float32)
     if not (row.size == col.size == val.size):
         raise ValueError("row, col and val must have the same length")
     h = ctypes.c_void_p()
-    rc = lib().ccdpp_create(int(m), int(n), int(k), float(lam), int(row.size), _p(row), _p(col),
-                            _p(val), int(seed) & (2**64 - 1), ctypes.byref(h))
+    args = (int(m), int(n), int(k), float(lam), int(row.size), _p(row), _p(col), _p(val),
+            int(seed) & (2**64 - 1))
+    if opts is None:
+        rc = lib().ccdpp_create(*args, ctypes.byref(h))
+    else:
+        rc = lib().ccdpp_create_ex(*args, ctypes.byref(opts), ctypes.byref(h))
     _check(None, rc)
     return h
 
@@ -150,15 +175,16 @@ def ccdpp_profile(h, enable):
     _check(h, lib().ccdpp_profile(h, 1 if enable else 0))
 
 
-def ccdpp_profile_read(h, kind):
+def ccdpp_profile_read(h, kind, layout=-1):
     n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
-    _check(h, lib().ccdpp_profile_read(h, int(kind), ctypes.byref(n), ctypes.byref(ms),
-                                       ctypes.byref(b)))
+    _check(h, lib().ccdpp_profile_read(h, int(kind), int(layout), ctypes.byref(n),
+                                       ctypes.byref(ms), ctypes.byref(b)))
     return n.value, ms.value, b.value
 
 
-INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "row_block_rows", "row_split_rows", "row_grid",
-               "col_block_rows", "col_split_rows", "col_grid", "device_bytes")
+INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_width",
+               "u_workgroups", "u_segments", "v_gather", "v_tiles", "v_tile_width", "v_workgroups",
+               "v_segments", "device_bytes")
 
 
 def ccdpp_info(h):
@@ -180,10 +206,10 @@ def ccdpp_destroy(h):
 class CCDPP:
     """A CCD++ problem held on the current HIP device."""
 
-    def __init__(self, m, n, k, lam, row, col, val, seed=0):
+    def __init__(self, m, n, k, lam, row, col, val, seed=0, opts=None):
         self.m, self.n, self.k, self.lam = int(m), int(n), int(k), float(lam)
         self.nnz = int(np.asarray(row).size)
-        self._h = ccdpp_create(m, n, k, lam, row, col, val, seed)
+        self._h = ccdpp_create_ex(m, n, k, lam, row, col, val, seed, opts)
 
     def close(self):
         if getattr(self, "_h", None):
@@ -234,8 +260,8 @@ class CCDPP:
     def profile(self, enable=True):
         ccdpp_profile(self._h, enable)
 
-    def profile_read(self, kind):
-        return ccdpp_profile_read(self._h, kind)
+    def profile_read(self, kind, layout=-1):
+        return ccdpp_profile_read(self._h, kind, layout)
 
     def info(self):
         return ccdpp_info(self._h)

@@ -1,12 +1,13 @@
 // Host runtime of the CCD++ library: the C ABI of include/ccdpp.h.
 //
 // The handle keeps everything on one device: the ratings A, the residual in a
-// row-compressed and a column-compressed copy, the map between the copies, W
-// and H column-major over relabelled ids (so the feature columns wbar_t and
-// hbar_t of eq. 11 are contiguous), and the scratch vectors u and v.  Unlike
-// the paper's Algorithm 7, u and v never travel to the host between features:
-// the host only enqueues kernels on one stream, and ccdpp_run synchronises
-// once at the end.
+// user-major and an item-major copy (each tiled and scheduled as described in
+// ccdpp_internal.hpp), the map between the two copies, W and H column-major
+// over relabelled ids (so the feature columns wbar_t and hbar_t of eq. 11 are
+// contiguous), and the scratch vectors u and v.  Unlike the paper's
+// Algorithm 7, u and v never travel to the host between features: the host
+// only enqueues kernels on one stream, and ccdpp_run synchronises once at the
+// end.
 #include <algorithm>
 #include <chrono>
 #include <cmath>
@@ -29,6 +30,7 @@ constexpr int32_t kReduceParts = 1024;
 
 struct ProfEvent {
     int kind;
+    int layout;
     hipEvent_t a, b;
     double bytes;
 };
@@ -40,6 +42,7 @@ struct ccdpp {
     int32_t k = 0;
     double lambda = 0.0;
     int device = 0;
+    int cus = 0;
     hipStream_t own_stream = nullptr;
     hipStream_t stream = nullptr;
     Layout L[2];                   // 0: rows are users (eq. 15), 1: rows are items (eq. 16)
@@ -47,9 +50,9 @@ struct ccdpp {
     int32_t* rold2new = nullptr;
     int32_t* cnew2old = nullptr;
     int32_t* cold2new = nullptr;
-    int32_t* csr_src = nullptr;    // row-ordered position -> input triplet index
-    int32_t* csr2csc = nullptr;    // row-ordered position -> column-ordered position
-    float* A = nullptr;            // ratings, row order
+    int32_t* perm0 = nullptr;      // user-major position -> input triplet index
+    int32_t* map01 = nullptr;      // user-major position -> item-major position
+    float* A = nullptr;            // ratings, user-major order
     float* W = nullptr;            // k x m: W[t*m + i]
     float* H = nullptr;            // k x n
     float* u = nullptr;
@@ -70,9 +73,9 @@ struct ccdpp {
     bool prof = false;
     std::vector<ProfEvent> prof_pending;
     std::vector<hipEvent_t> event_pool;
-    int64_t prof_launch[CCDPP_K_COUNT] = {};
-    double prof_ms[CCDPP_K_COUNT] = {};
-    double prof_bytes[CCDPP_K_COUNT] = {};
+    int64_t prof_launch[CCDPP_K_COUNT][2] = {};
+    double prof_ms[CCDPP_K_COUNT][2] = {};
+    double prof_bytes[CCDPP_K_COUNT][2] = {};
 };
 
 namespace {
@@ -100,6 +103,12 @@ int fail(ccdpp* h, int code, const char* fmt, ...) {
                         "%s failed: %s", #expr, hipGetErrorString(e_));                       \
     } while (0)
 
+#define RCK(expr)                      \
+    do {                               \
+        int r_ = (expr);               \
+        if (r_ != CCDPP_OK) return r_; \
+    } while (0)
+
 template <class T>
 hipError_t dalloc(ccdpp* h, T** p, int64_t count) {
     size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
@@ -112,11 +121,19 @@ hipError_t dalloc(ccdpp* h, T** p, int64_t count) {
     return hipSuccess;
 }
 
+template <class T>
+int upload(ccdpp* h, T** dst, const std::vector<T>& src) {
+    HIPCK(h, dalloc(h, dst, (int64_t)src.size()));
+    if (!src.empty())
+        HIPCK(h, hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
+    return CCDPP_OK;
+}
+
 // Temporary device buffer freed when it goes out of scope.
 struct Tmp {
     void* p = nullptr;
     ~Tmp() {
-        if (p) hipFree(p);
+        if (p) (void)hipFree(p);
     }
 };
 template <class T>
@@ -146,80 +163,10 @@ float initial_h(uint64_t seed, uint64_t e) {
     return (float)(0.1 * z);
 }
 
-// Schedule of one layout from its row lengths (already in decreasing order).
-int build_schedule(ccdpp* h, Layout& L, const std::vector<int64_t>& len) {
-    using namespace ccdk;
-    const int64_t rows = (int64_t)len.size();
-    int64_t nb = 0;
-    while (nb < rows && len[nb] > kGroupMaxLen) ++nb;
-    std::vector<int32_t> piece_row, split_row, split_first;
-    std::vector<int64_t> piece_lo;
-    int64_t pos = 0;
-    for (int64_t r = 0; r < nb; ++r) {
-        const int64_t npc = (len[r] + kPieceMax - 1) / kPieceMax;
-        const int64_t base = len[r] / npc, extra = len[r] % npc;
-        if (npc > 1) {
-            split_row.push_back((int32_t)r);
-            split_first.push_back((int32_t)piece_row.size());
-        }
-        for (int64_t c = 0; c < npc; ++c) {
-            piece_row.push_back((int32_t)r);
-            piece_lo.push_back(pos);
-            pos += base + (c < extra ? 1 : 0);
-        }
-    }
-    piece_lo.push_back(pos);
-    split_first.push_back((int32_t)piece_row.size());
-
-    L.segs.clear();
-    int64_t blocks = 0;
-    if (!piece_row.empty()) {
-        L.segs.push_back(Seg{kSegBlock, (int32_t)blocks, 0, (int32_t)piece_row.size()});
-        blocks += (int64_t)piece_row.size();
-    }
-    struct Cls {
-        int kind;
-        int64_t maxlen;
-        int g;
-    };
-    static const Cls classes[] = {{kSegG64E16, 1024, 64}, {kSegG64E8, 512, 64},
-                                  {kSegG32E8, 256, 32},   {kSegG16E8, 128, 16},
-                                  {kSegG8E8, 64, 8},      {kSegG4E8, 32, 4},
-                                  {kSegG2E8, 16, 2},      {kSegG1E8, 8, 1}};
-    int64_t r = nb;
-    for (int ci = 0; ci < 8; ++ci) {
-        const int64_t minlen = ci + 1 < 8 ? classes[ci + 1].maxlen + 1 : 0;
-        int64_t e = r;
-        while (e < rows && len[e] >= minlen) ++e;
-        if (e > r) {
-            const int64_t per = kBlock / classes[ci].g;
-            L.segs.push_back(Seg{classes[ci].kind, (int32_t)blocks, (int32_t)r, (int32_t)e});
-            blocks += (e - r + per - 1) / per;
-        }
-        r = e;
-    }
-    if (r != rows) return fail(h, CCDPP_EDEVICE, "internal: schedule does not cover all rows");
-    if ((int)L.segs.size() > kMaxSegs) return fail(h, CCDPP_EDEVICE, "internal: too many segments");
-    if (blocks > INT32_MAX) return fail(h, CCDPP_EINVAL, "too many workgroups per pass");
-    L.grid = (int32_t)blocks;
-    L.nblock_rows = (int32_t)nb;
-    L.npieces = (int32_t)piece_row.size();
-    L.nsplit = (int32_t)split_row.size();
-    HIPCK(h, dalloc(h, &L.piece_row, L.npieces));
-    HIPCK(h, dalloc(h, &L.piece_lo, L.npieces + 1));
-    HIPCK(h, dalloc(h, &L.split_row, L.nsplit));
-    HIPCK(h, dalloc(h, &L.split_first, L.nsplit + 1));
-    HIPCK(h, dalloc(h, &L.part, L.npieces));
-    if (L.npieces) {
-        HIPCK(h, hipMemcpy(L.piece_row, piece_row.data(), piece_row.size() * 4, hipMemcpyHostToDevice));
-    }
-    HIPCK(h, hipMemcpy(L.piece_lo, piece_lo.data(), piece_lo.size() * 8, hipMemcpyHostToDevice));
-    if (L.nsplit) {
-        HIPCK(h, hipMemcpy(L.split_row, split_row.data(), split_row.size() * 4, hipMemcpyHostToDevice));
-    }
-    HIPCK(h, hipMemcpy(L.split_first, split_first.data(), split_first.size() * 4,
-                       hipMemcpyHostToDevice));
-    return CCDPP_OK;
+int bits_for(uint64_t maxval) {
+    int b = 1;
+    while (b < 64 && (maxval >> b) != 0) ++b;
+    return b;
 }
 
 // Order ids by decreasing count, ties by increasing id.
@@ -234,14 +181,229 @@ void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
     for (int64_t i = 0; i < N; ++i) old2new[new2old[i]] = (int32_t)i;
 }
 
-int bits_for(uint64_t maxkey) {
-    int b = 1;
-    while (b < 64 && (maxkey >> b) != 0) ++b;
-    return b;
+// Unit kinds for lane groups: {kind, longest segment, lanes per segment}.
+struct GroupClass {
+    int kind;
+    int64_t maxlen;
+    int g;
+};
+const GroupClass kClasses[] = {{ccdk::kUG64E16, 1024, 64}, {ccdk::kUG64E8, 512, 64},
+                               {ccdk::kUG32E8, 256, 32},   {ccdk::kUG16E8, 128, 16},
+                               {ccdk::kUG8E8, 64, 8},      {ccdk::kUG4E8, 32, 4},
+                               {ccdk::kUG2E8, 16, 2},      {ccdk::kUG1E8, 8, 1}};
+
+// Build one layout.  lrow/lcol: relabelled row and gathered-column id of every
+// input triplet (device).  side 0 is the user-major copy (its first pass stages
+// q and qq, x being q), side 1 the item-major copy (first pass stages x, q, qq).
+// On return perm holds, for every layout position, the input triplet index.
+int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, const int32_t* lrow,
+                 const int32_t* lcol, const float* val_in, const ccdpp_options_t* opt,
+                 int32_t* perm, hipStream_t s) {
+    using namespace ccdk;
+    const int64_t N = h->nnz;
+    L.rows = rows;
+    L.cols = cols;
+    L.nnz = N;
+    const int nvec = side == 0 ? 2 : 3;
+    const int64_t tmax = ((int64_t)kLdsBytes / (4 * nvec)) / 64 * 64;
+    const int forced = opt ? opt->gather_mode[side] : 0;
+    const int64_t forced_T = opt ? opt->tile_width[side] : 0;
+    if (forced_T > tmax)
+        return fail(h, CCDPP_EINVAL, "tile_width must be at most %lld", (long long)tmax);
+
+    // Tile width: whole vector if it fits, else balanced tiles of at most tmax.
+    int64_t T = cols, P = 1;
+    bool lds = forced != kGatherGlobal;
+    if (forced_T > 0) {
+        T = forced_T;
+    } else if (cols > tmax) {
+        P = (cols + tmax - 1) / tmax;
+        T = ((cols + P - 1) / P + 63) / 64 * 64;
+    }
+    if (!lds) T = cols;
+    P = (cols + T - 1) / T;
+    if ((uint64_t)P * (uint64_t)rows > (uint64_t)INT32_MAX) {
+        if (forced == kGatherLds) return fail(h, CCDPP_EINVAL, "too many (tile, row) pairs");
+        lds = false;
+        T = cols;
+        P = 1;
+    }
+
+    // Entries per (tile, row).
+    std::vector<int32_t> cnt;
+    for (int attempt = 0; attempt < 2; ++attempt) {
+        int32_t* d_cnt;
+        Tmp tc;
+        HIPCK(h, talloc(tc, &d_cnt, P * rows));
+        HIPCK(h, hipMemsetAsync(d_cnt, 0, (size_t)(P * rows) * 4, s));
+        HIPCK(h, launch_seg_histogram(lrow, lcol, N, (int32_t)rows, (int32_t)T, d_cnt, s));
+        cnt.assign((size_t)(P * rows), 0);
+        HIPCK(h, hipMemcpyAsync(cnt.data(), d_cnt, (size_t)(P * rows) * 4, hipMemcpyDeviceToHost,
+                                s));
+        HIPCK(h, hipStreamSynchronize(s));
+        if (P == 1 || forced == kGatherLds) break;
+        // Tiling pays only when segments are long enough; otherwise gather through L2.
+        int64_t nonempty = 0;
+        for (int32_t c : cnt) nonempty += c > 0;
+        if (nonempty > 0 && N / nonempty >= kMinTiledSeg) break;
+        lds = false;
+        T = cols;
+        P = 1;
+    }
+    L.gather = lds ? kGatherLds : kGatherGlobal;
+    L.T = (int32_t)T;
+    L.P = (int32_t)P;
+    L.idx16 = T <= 65536;
+
+    // Segments: per tile, rows in order of decreasing count (all rows when P == 1,
+    // so every row gets its coordinate written; only non-empty rows otherwise).
+    std::vector<int32_t> segid((size_t)(P * rows), -1), seg_row, tile_seg(P + 1, 0);
+    std::vector<int64_t> seg_start;
+    std::vector<int32_t> order;
+    int64_t pos = 0;
+    for (int64_t p = 0; p < P; ++p) {
+        tile_seg[p] = (int32_t)seg_row.size();
+        order.clear();
+        const int32_t* cp = cnt.data() + p * rows;
+        for (int64_t r = 0; r < rows; ++r)
+            if (P == 1 || cp[r] > 0) order.push_back((int32_t)r);
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int32_t a, int32_t b) { return cp[a] > cp[b]; });
+        for (int32_t r : order) {
+            segid[p * rows + r] = (int32_t)seg_row.size();
+            seg_row.push_back(r);
+            seg_start.push_back(pos);
+            pos += cp[r];
+        }
+    }
+    tile_seg[P] = (int32_t)seg_row.size();
+    seg_start.push_back(pos);
+    const int64_t S = (int64_t)seg_row.size();
+    if (pos != N) return fail(h, CCDPP_EDEVICE, "internal: segment counts do not cover nnz");
+    L.nseg = S;
+
+    // Units per tile and their tile ranges.
+    std::vector<int2> units;
+    std::vector<int32_t> tile_unit(P + 1, 0);
+    int32_t nlong = 0;
+    for (int64_t p = 0; p < P; ++p) {
+        tile_unit[p] = (int32_t)units.size();
+        const int64_t sb = tile_seg[p], se = tile_seg[p + 1];
+        int64_t si = sb;
+        while (si < se && seg_start[si + 1] - seg_start[si] > kGroupMaxLen) {
+            units.push_back(make_int2((int32_t)si, kULong | (1 << 8)));
+            ++nlong;
+            ++si;
+        }
+        for (int ci = 0; ci < 8; ++ci) {
+            const int64_t minlen = ci + 1 < 8 ? kClasses[ci + 1].maxlen + 1 : 0;
+            const int per = 64 / kClasses[ci].g;
+            int64_t e = si;
+            while (e < se && seg_start[e + 1] - seg_start[e] >= minlen) ++e;
+            for (int64_t u0 = si; u0 < e; u0 += per) {
+                const int c = (int)std::min<int64_t>(per, e - u0);
+                units.push_back(make_int2((int32_t)u0, kClasses[ci].kind | (c << 8)));
+            }
+            si = e;
+        }
+        if (si != se) return fail(h, CCDPP_EDEVICE, "internal: units do not cover the tile");
+    }
+    tile_unit[P] = (int32_t)units.size();
+    L.nunits = (int32_t)units.size();
+    L.nlong = nlong;
+
+    // Persistent workgroups, given to tiles in proportion to their entries.
+    const int64_t want = opt && opt->workgroups > 0 ? opt->workgroups : 2 * (int64_t)h->cus;
+    std::vector<int32_t> wg_tile, wg_rank, tile_nwg(P, 0);
+    for (int64_t p = 0; p < P; ++p) {
+        const int64_t ent = seg_start[tile_seg[p + 1]] - seg_start[tile_seg[p]];
+        const int64_t nu = tile_unit[p + 1] - tile_unit[p];
+        int64_t w = N > 0 ? (want * ent + N / 2) / N : (p == 0 ? want : 0);
+        w = std::min<int64_t>(w, (nu + kWaves - 1) / kWaves);
+        w = std::max<int64_t>(w, nu > 0 ? 1 : 0);
+        tile_nwg[p] = (int32_t)w;
+        for (int64_t r = 0; r < w; ++r) {
+            wg_tile.push_back((int32_t)p);
+            wg_rank.push_back((int32_t)r);
+        }
+    }
+    L.grid = (int32_t)wg_tile.size();
+
+    // Segments of each row in tile order (for the combine of P > 1).
+    if (P > 1) {
+        std::vector<int32_t> rptr(rows + 1, 0), rsegs((size_t)S);
+        for (int64_t r = 0; r < rows; ++r) {
+            int32_t c = 0;
+            for (int64_t p = 0; p < P; ++p) c += segid[p * rows + r] >= 0;
+            rptr[r + 1] = rptr[r] + c;
+        }
+        std::vector<int32_t> fillp(rptr.begin(), rptr.end() - 1);
+        for (int64_t r = 0; r < rows; ++r)
+            for (int64_t p = 0; p < P; ++p)
+                if (segid[p * rows + r] >= 0) rsegs[fillp[r]++] = segid[p * rows + r];
+        RCK(upload(h, &L.row_seg_ptr, rptr));
+        RCK(upload(h, &L.row_segs, rsegs));
+        HIPCK(h, dalloc(h, &L.part, S));
+    }
+    RCK(upload(h, &L.seg_start, seg_start));
+    RCK(upload(h, &L.seg_row, seg_row));
+    RCK(upload(h, &L.tile_seg, tile_seg));
+    RCK(upload(h, &L.units, units));
+    RCK(upload(h, &L.wg_tile, wg_tile));
+    RCK(upload(h, &L.wg_rank, wg_rank));
+    RCK(upload(h, &L.tile_unit, tile_unit));
+    RCK(upload(h, &L.tile_nwg, tile_nwg));
+
+    // Sort the entries into layout order and fill index and value arrays.
+    const int cbits = bits_for((uint64_t)std::max<int64_t>(T - 1, 1));
+    const int sbits = bits_for((uint64_t)std::max<int64_t>(S - 1, 1));
+    if (cbits + sbits > 64) return fail(h, CCDPP_EDEVICE, "internal: sort key too wide");
+    HIPCK(h, dalloc(h, &L.val, N));
+    if (L.idx16) {
+        uint16_t* d;
+        HIPCK(h, dalloc(h, &d, N));
+        L.idx = d;
+    } else {
+        int32_t* d;
+        HIPCK(h, dalloc(h, &d, N));
+        L.idx = d;
+    }
+    if (N > 0) {
+        int32_t* d_segid;
+        uint64_t *k0, *k1;
+        int32_t* i0;
+        Tmp tsid, tk0, tk1, ti0, ttmp;
+        HIPCK(h, talloc(tsid, &d_segid, P * rows));
+        HIPCK(h, hipMemcpyAsync(d_segid, segid.data(), segid.size() * 4, hipMemcpyHostToDevice, s));
+        HIPCK(h, talloc(tk0, &k0, N));
+        HIPCK(h, talloc(tk1, &k1, N));
+        HIPCK(h, talloc(ti0, &i0, N));
+        HIPCK(h, launch_seg_keys(lrow, lcol, d_segid, N, (int32_t)rows, (int32_t)T, cbits, k0, i0,
+                                 s));
+        void* tmp = nullptr;
+        size_t tmp_bytes = 0;
+        hipError_t e = sort_pairs(k0, k1, i0, perm, N, cbits + sbits, s, &tmp, &tmp_bytes);
+        ttmp.p = tmp;
+        HIPCK(h, e);
+        if (side == 0) {
+            int32_t* d_flag;
+            Tmp tflag;
+            HIPCK(h, talloc(tflag, &d_flag, 1));
+            HIPCK(h, hipMemsetAsync(d_flag, 0, 4, s));
+            HIPCK(h, launch_dup_check(k1, N, d_flag, s));
+            int32_t flag = 0;
+            HIPCK(h, hipMemcpyAsync(&flag, d_flag, 4, hipMemcpyDeviceToHost, s));
+            HIPCK(h, hipStreamSynchronize(s));
+            if (flag) return fail(h, CCDPP_EDUP, "a position (i, j) occurs more than once");
+        }
+        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, L.idx16, L.idx, L.val, s));
+        HIPCK(h, hipStreamSynchronize(s));
+    }
+    return CCDPP_OK;
 }
 
 int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float* val,
-                  uint64_t seed) {
+                  uint64_t seed, const ccdpp_options_t* opt) {
     using namespace ccdk;
     const auto t0 = std::chrono::steady_clock::now();
     const int64_t m = h->m, n = h->n, N = h->nnz;
@@ -251,6 +413,11 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(h, CCDPP_EDEVICE, "device %d is %s; this library is built for gfx950",
                     h->device, prop.gcnArchName);
+    if (prop.sharedMemPerBlock < (size_t)kLdsBytes)
+        return fail(h, CCDPP_EDEVICE, "device offers %zu bytes of LDS per workgroup, need %d",
+                    prop.sharedMemPerBlock, kLdsBytes);
+    h->cus = prop.multiProcessorCount;
+    HIPCK(h, sweep_init());
     HIPCK(h, hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
     h->stream = h->own_stream;
     hipStream_t s = h->stream;
@@ -278,97 +445,54 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, hipMemcpyAsync(cnt_c.data(), d_cnt_c, n * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
 
-    // Relabel by decreasing degree.
+    // Relabel users and items by decreasing degree.
     std::vector<int32_t> rn2o, ro2n, cn2o, co2n;
     relabel(cnt_r, rn2o, ro2n);
     relabel(cnt_c, cn2o, co2n);
-    HIPCK(h, dalloc(h, &h->rnew2old, m));
-    HIPCK(h, dalloc(h, &h->rold2new, m));
-    HIPCK(h, dalloc(h, &h->cnew2old, n));
-    HIPCK(h, dalloc(h, &h->cold2new, n));
-    HIPCK(h, hipMemcpyAsync(h->rnew2old, rn2o.data(), m * 4, hipMemcpyHostToDevice, s));
-    HIPCK(h, hipMemcpyAsync(h->rold2new, ro2n.data(), m * 4, hipMemcpyHostToDevice, s));
-    HIPCK(h, hipMemcpyAsync(h->cnew2old, cn2o.data(), n * 4, hipMemcpyHostToDevice, s));
-    HIPCK(h, hipMemcpyAsync(h->cold2new, co2n.data(), n * 4, hipMemcpyHostToDevice, s));
+    RCK(upload(h, &h->rnew2old, rn2o));
+    RCK(upload(h, &h->rold2new, ro2n));
+    RCK(upload(h, &h->cnew2old, cn2o));
+    RCK(upload(h, &h->cold2new, co2n));
+    int32_t *d_ru, *d_ci;
+    Tmp t_ru, t_ci;
+    HIPCK(h, talloc(t_ru, &d_ru, N));
+    HIPCK(h, talloc(t_ci, &d_ci, N));
+    HIPCK(h, launch_map(d_row, h->rold2new, N, d_ru, s));
+    HIPCK(h, launch_map(d_col, h->cold2new, N, d_ci, s));
 
-    // Persistent arrays.
-    Layout& R = h->L[0];
-    Layout& C = h->L[1];
-    R.rows = m; R.cols = n; R.nnz = N;
-    C.rows = n; C.cols = m; C.nnz = N;
-    HIPCK(h, dalloc(h, &R.ptr, m + 1));
-    HIPCK(h, dalloc(h, &R.idx, N));
-    HIPCK(h, dalloc(h, &R.val, N));
-    HIPCK(h, dalloc(h, &C.ptr, n + 1));
-    HIPCK(h, dalloc(h, &C.idx, N));
-    HIPCK(h, dalloc(h, &C.val, N));
-    HIPCK(h, dalloc(h, &h->A, N));
-    HIPCK(h, dalloc(h, &h->csr_src, N));
-    HIPCK(h, dalloc(h, &h->csr2csc, N));
-
-    // Sort to row order, check repeats, fill the row copy; sort to column order.
+    // The two copies, the ratings in user-major order and the map between copies.
+    HIPCK(h, dalloc(h, &h->perm0, N));
+    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, s));
     {
-        uint64_t *k0, *k1;
-        int32_t *i0, *i1;
-        Tmp tk0, tk1, ti0, ti1, ttmp;
-        void* tmp = nullptr;
-        size_t tmp_bytes = 0;
-        HIPCK(h, talloc(tk0, &k0, N));
-        HIPCK(h, talloc(tk1, &k1, N));
-        HIPCK(h, talloc(ti0, &i0, N));
-        HIPCK(h, talloc(ti1, &i1, N));
-        HIPCK(h, launch_make_keys_csr(d_row, d_col, h->rold2new, h->cold2new, N, n, k0, i0, s));
-        const int bits = bits_for((uint64_t)m * (uint64_t)n - 1);
-        hipError_t e = N ? sort_pairs(k0, k1, i0, h->csr_src, N, bits, s, &tmp, &tmp_bytes)
-                         : hipSuccess;
-        ttmp.p = tmp;
-        HIPCK(h, e);
-        int32_t* d_flag;
-        Tmp tflag;
-        HIPCK(h, talloc(tflag, &d_flag, 1));
-        HIPCK(h, hipMemsetAsync(d_flag, 0, 4, s));
-        HIPCK(h, launch_dup_check(k1, N, d_flag, s));
-        int32_t flag = 0;
-        HIPCK(h, hipMemcpyAsync(&flag, d_flag, 4, hipMemcpyDeviceToHost, s));
-        HIPCK(h, hipStreamSynchronize(s));
-        if (flag) return fail(h, CCDPP_EDUP, "a position (i, j) occurs more than once");
-        HIPCK(h, launch_csr_fill(k1, h->csr_src, d_val, N, n, m, R.idx, R.val, h->A, k0, i0, s));
-        const int bits2 = bits_for((uint64_t)n * (uint64_t)m - 1);
-        tmp = ttmp.p;
-        e = N ? sort_pairs(k0, k1, i0, i1, N, bits2, s, &tmp, &tmp_bytes) : hipSuccess;
-        ttmp.p = tmp;
-        HIPCK(h, e);
-        HIPCK(h, launch_csc_fill(k1, i1, R.val, N, m, C.idx, C.val, h->csr2csc, s));
+        int32_t *perm1, *inv1;
+        Tmp tp1, tinv;
+        HIPCK(h, talloc(tp1, &perm1, N));
+        RCK(build_layout(h, 1, h->L[1], n, m, d_ci, d_ru, d_val, opt, perm1, s));
+        HIPCK(h, talloc(tinv, &inv1, N));
+        HIPCK(h, launch_invert(perm1, N, inv1, s));
+        HIPCK(h, dalloc(h, &h->map01, N));
+        HIPCK(h, launch_compose(inv1, h->perm0, N, h->map01, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
-
-    // Row pointers and schedules from the sorted degrees.
-    std::vector<int64_t> len_r(m), len_c(n), ptr_r(m + 1), ptr_c(n + 1);
-    for (int64_t i = 0; i < m; ++i) len_r[i] = cnt_r[rn2o[i]];
-    for (int64_t j = 0; j < n; ++j) len_c[j] = cnt_c[cn2o[j]];
-    ptr_r[0] = 0;
-    for (int64_t i = 0; i < m; ++i) ptr_r[i + 1] = ptr_r[i] + len_r[i];
-    ptr_c[0] = 0;
-    for (int64_t j = 0; j < n; ++j) ptr_c[j + 1] = ptr_c[j] + len_c[j];
-    HIPCK(h, hipMemcpy(R.ptr, ptr_r.data(), (m + 1) * 8, hipMemcpyHostToDevice));
-    HIPCK(h, hipMemcpy(C.ptr, ptr_c.data(), (n + 1) * 8, hipMemcpyHostToDevice));
-    int rc = build_schedule(h, R, len_r);
-    if (rc) return rc;
-    rc = build_schedule(h, C, len_c);
-    if (rc) return rc;
+    HIPCK(h, dalloc(h, &h->A, N));
+    if (N) HIPCK(h, hipMemcpyAsync(h->A, h->L[0].val, N * 4, hipMemcpyDeviceToDevice, s));
 
     // Factors: W = 0 (Algorithm 3), H from the seed; scratch.
     HIPCK(h, dalloc(h, &h->W, (int64_t)h->k * m));
     HIPCK(h, dalloc(h, &h->H, (int64_t)h->k * n));
     HIPCK(h, dalloc(h, &h->u, m));
     HIPCK(h, dalloc(h, &h->v, n));
-    h->sse_nparts = std::max<int32_t>({R.grid, C.grid, kReduceParts});
+    h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid) * kWaves, kReduceParts);
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
     HIPCK(h, dalloc(h, &h->d_count, 1));
     HIPCK(h, launch_fill(h->W, 0.0f, (int64_t)h->k * m, s));
     HIPCK(h, launch_fill(h->u, 0.0f, m, s));
     HIPCK(h, launch_fill(h->v, 0.0f, n, s));
+    for (int li = 0; li < 2; ++li)
+        if (h->L[li].part)  // partials are written before they are read: start them as NaN
+            HIPCK(h, launch_fill(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
+                                 4 * h->L[li].nseg, s));
     {
         std::vector<float> h0((size_t)n * h->k);
         for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
@@ -387,14 +511,14 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
 }
 
 void destroy_all(ccdpp* h) {
-    for (void* p : h->allocs) hipFree(p);
+    for (void* p : h->allocs) (void)hipFree(p);
     h->allocs.clear();
     for (auto& pe : h->prof_pending) {
         h->event_pool.push_back(pe.a);
         h->event_pool.push_back(pe.b);
     }
-    for (hipEvent_t e : h->event_pool) hipEventDestroy(e);
-    if (h->own_stream) hipStreamDestroy(h->own_stream);
+    for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
+    if (h->own_stream) (void)hipStreamDestroy(h->own_stream);
 }
 
 // ---- kernel timing ---------------------------------------------------------------
@@ -412,20 +536,22 @@ hipEvent_t take_event(ccdpp* h) {
 struct Timed {
     ccdpp* h;
     int kind;
+    int layout;
     double bytes;
     hipEvent_t a = nullptr;
-    Timed(ccdpp* h_, int kind_, double bytes_) : h(h_), kind(kind_), bytes(bytes_) {
+    Timed(ccdpp* h_, int kind_, int layout_, double bytes_)
+        : h(h_), kind(kind_), layout(layout_), bytes(bytes_) {
         if (h->prof) {
             a = take_event(h);
-            if (a) hipEventRecord(a, h->stream);
+            if (a) (void)hipEventRecord(a, h->stream);
         }
     }
     void done() {
         if (h->prof && a) {
             hipEvent_t b = take_event(h);
             if (b) {
-                hipEventRecord(b, h->stream);
-                h->prof_pending.push_back(ProfEvent{kind, a, b, bytes});
+                (void)hipEventRecord(b, h->stream);
+                h->prof_pending.push_back(ProfEvent{kind, layout, a, b, bytes});
             } else {
                 h->event_pool.push_back(a);
             }
@@ -437,9 +563,9 @@ void collect_profile(ccdpp* h) {
     for (auto& pe : h->prof_pending) {
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, pe.a, pe.b) == hipSuccess) {
-            h->prof_launch[pe.kind] += 1;
-            h->prof_ms[pe.kind] += ms;
-            h->prof_bytes[pe.kind] += pe.bytes;
+            h->prof_launch[pe.kind][pe.layout] += 1;
+            h->prof_ms[pe.kind][pe.layout] += ms;
+            h->prof_bytes[pe.kind][pe.layout] += pe.bytes;
         }
         h->event_pool.push_back(pe.a);
         h->event_pool.push_back(pe.b);
@@ -447,14 +573,17 @@ void collect_profile(ccdpp* h) {
     h->prof_pending.clear();
 }
 
-// Algorithmic bytes of one pass over layout L (see ccdpp_profile_read).
+// Algorithmic bytes of one pass over layout L (see ccdpp_profile_read): index and
+// value arrays, residual write-back, segment table, per-segment row scalars,
+// outputs, and every gathered vector read once.
 double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors) {
-    const double nnz = (double)L.nnz, rows = (double)L.rows, cols = (double)L.cols;
-    double b = 8.0 * nnz + 8.0 * (rows + 1);             // index + value reads, row pointers
-    if (mode != ccdk::kModePlain) b += 4.0 * nnz;      // residual write-back
-    if (mode != ccdk::kModeFlush) b += 4.0 * rows;     // output coordinates
-    if (mode == ccdk::kModeAdd || mode == ccdk::kModeSubAdd) b += 4.0 * rows;  // p
-    if (mode == ccdk::kModeSubAdd || mode == ccdk::kModeFlush) b += 4.0 * rows;  // pp
+    using namespace ccdk;
+    const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
+    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz + 12.0 * S;
+    if (mode != kModePlain) b += 4.0 * nnz;
+    if (mode != kModeFlush) b += L.P == 1 ? 4.0 * S : 16.0 * S;
+    if (mode == kModeAdd || mode == kModeSubAdd) b += 4.0 * S;
+    if (mode == kModeSubAdd || mode == kModeFlush) b += 4.0 * S;
     b += 4.0 * cols * gathered_vectors;
     return b;
 }
@@ -464,26 +593,23 @@ int pass(ccdpp* h, int li, ccdk::PassMode mode, const float* x, const float* p, 
     const Layout& L = h->L[li];
     const int kind = mode == ccdk::kModePlain ? CCDPP_K_PASS
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
-                                                 : CCDPP_K_PASS_FUSED;
+                                                : CCDPP_K_PASS_FUSED;
     {
-        Timed tm(h, kind, pass_bytes(L, mode, gathered));
+        Timed tm(h, kind, li, pass_bytes(L, mode, gathered));
         HIPCK(h, ccdk::launch_pass(L, mode, x, p, pp, q, qq, y, h->lambda, h->sse_part, h->stream));
         tm.done();
     }
-    if (mode != ccdk::kModeFlush && L.nsplit > 0) {
-        Timed tc(h, CCDPP_K_COMBINE, 16.0 * L.npieces + 12.0 * L.nsplit);
+    if (mode != ccdk::kModeFlush && L.P > 1) {
+        Timed tc(h, CCDPP_K_COMBINE, li, 20.0 * L.nseg + 8.0 * L.rows);
         HIPCK(h, ccdk::launch_combine(L, y, h->lambda, h->stream));
         tc.done();
     }
     return CCDPP_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, const int32_t* row,
-                 const int32_t* col, const float* val, uint64_t seed, ccdpp_t** out) {
+int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, const int32_t* row,
+                const int32_t* col, const float* val, uint64_t seed, const ccdpp_options_t* opts,
+                ccdpp_t** out) {
     g_create_error.clear();
     if (!out) return fail(nullptr, CCDPP_EINVAL, "out is NULL");
     if (m < 1 || m >= kMaxDim || n < 1 || n >= kMaxDim)
@@ -494,6 +620,14 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, co
     if (nnz < 0 || nnz > kMaxNnz) return fail(nullptr, CCDPP_EINVAL, "nnz must be in [0, 2^31-1]");
     if (nnz > 0 && (!row || !col || !val))
         return fail(nullptr, CCDPP_EINVAL, "row, col and val must be non-NULL when nnz > 0");
+    if (opts) {
+        for (int i = 0; i < 2; ++i) {
+            if (opts->gather_mode[i] < 0 || opts->gather_mode[i] > 2)
+                return fail(nullptr, CCDPP_EINVAL, "gather_mode must be 0, 1 or 2");
+            if (opts->tile_width[i] < 0) return fail(nullptr, CCDPP_EINVAL, "tile_width < 0");
+        }
+        if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
+    }
     for (int64_t e = 0; e < nnz; ++e) {
         if (row[e] < 0 || row[e] >= m)
             return fail(nullptr, CCDPP_EINVAL, "row[%lld] = %d out of range", (long long)e, row[e]);
@@ -509,7 +643,7 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, co
     h->k = k;
     h->lambda = lambda;
     h->nnz = nnz;
-    int rc = create_device(h, row, col, val, seed);
+    int rc = create_device(h, row, col, val, seed, opts);
     if (rc != CCDPP_OK) {
         g_create_error = h->err;
         destroy_all(h);
@@ -520,13 +654,27 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, co
     return CCDPP_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, const int32_t* row,
+                 const int32_t* col, const float* val, uint64_t seed, ccdpp_t** out) {
+    return create_impl(m, n, k, lambda, nnz, row, col, val, seed, nullptr, out);
+}
+
+int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
+                    const int32_t* row, const int32_t* col, const float* val, uint64_t seed,
+                    const ccdpp_options_t* opts, ccdpp_t** out) {
+    return create_impl(m, n, k, lambda, nnz, row, col, val, seed, opts, out);
+}
+
 int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
     using namespace ccdk;
     if (!usable(h)) return CCDPP_ESTATE;
     if (outer < 0 || inner < 1)
         return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0 and inner_iters >= 1");
     const int64_t m = h->m, n = h->n;
-    int rc;
     for (int32_t it = 0; it < outer; ++it) {
         for (int32_t t = 0; t < h->k; ++t) {
             float* Wt = h->W + (int64_t)t * m;
@@ -537,23 +685,19 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
             const PassMode first = prev ? kModeSubAdd : kModeAdd;
             const int g1 = prev ? 2 : 1;
             // First u-pass: eq. 18 of the pending feature, eq. 13, eq. 15 with v = hbar_t.
-            rc = pass(h, 0, first, Ht, Wt, Wp, Ht, Hp, h->u, g1);
-            if (rc) return rc;
-            // First v-pass: the same residual update on the column copy, eq. 16 with the new u.
+            RCK(pass(h, 0, first, Ht, Wt, Wp, Ht, Hp, h->u, g1));
+            // First v-pass: the same residual update on the item-major copy, eq. 16 with the new u.
             float* yv = inner == 1 ? Ht : h->v;
-            rc = pass(h, 1, first, h->u, Ht, Hp, Wt, Wp, yv, g1 + 1);
-            if (rc) return rc;
+            RCK(pass(h, 1, first, h->u, Ht, Hp, Wt, Wp, yv, g1 + 1));
             for (int32_t s = 2; s <= inner; ++s) {
                 const bool last = s == inner;
                 float* yu = last ? Wt : h->u;  // the last u is committed in place (eq. 17)
-                rc = pass(h, 0, kModePlain, h->v, nullptr, nullptr, nullptr, nullptr, yu, 1);
-                if (rc) return rc;
-                rc = pass(h, 1, kModePlain, yu, nullptr, nullptr, nullptr, nullptr,
-                          last ? Ht : h->v, 1);
-                if (rc) return rc;
+                RCK(pass(h, 0, kModePlain, h->v, nullptr, nullptr, nullptr, nullptr, yu, 1));
+                RCK(pass(h, 1, kModePlain, yu, nullptr, nullptr, nullptr, nullptr,
+                         last ? Ht : h->v, 1));
             }
             if (inner == 1) {
-                Timed tm(h, CCDPP_K_COMMIT, 8.0 * m);
+                Timed tm(h, CCDPP_K_COMMIT, 0, 8.0 * m);
                 HIPCK(h, launch_copy(h->u, Wt, m, h->stream));
                 tm.done();
             }
@@ -561,14 +705,12 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
         }
     }
     if (h->pending >= 0) {
-        // Final eq. 18 on both copies; the row copy also sums R^2 for the training RMSE.
+        // Final eq. 18 on both copies; the user-major one also sums R^2 for the training RMSE.
         const float* Wp = h->W + (int64_t)h->pending * m;
         const float* Hp = h->H + (int64_t)h->pending * n;
-        rc = pass(h, 0, kModeFlush, nullptr, nullptr, Wp, nullptr, Hp, nullptr, 1);
-        if (rc) return rc;
-        HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid, h->d_scalar, h->stream));
-        rc = pass(h, 1, kModeFlush, nullptr, nullptr, Hp, nullptr, Wp, nullptr, 1);
-        if (rc) return rc;
+        RCK(pass(h, 0, kModeFlush, nullptr, nullptr, Wp, nullptr, Hp, nullptr, 1));
+        HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
+        RCK(pass(h, 1, kModeFlush, nullptr, nullptr, Hp, nullptr, Wp, nullptr, 1));
         h->pending = -1;
         double sse = 0.0;
         HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
@@ -608,10 +750,12 @@ int ccdpp_set_factors(ccdpp_t* h, const float* W, const float* H) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (W)
         for (int64_t e = 0; e < h->m * h->k; ++e)
-            if (!std::isfinite(W[e])) return fail(h, CCDPP_EINVAL, "W[%lld] is not finite", (long long)e);
+            if (!std::isfinite(W[e]))
+                return fail(h, CCDPP_EINVAL, "W[%lld] is not finite", (long long)e);
     if (H)
         for (int64_t e = 0; e < h->n * h->k; ++e)
-            if (!std::isfinite(H[e])) return fail(h, CCDPP_EINVAL, "H[%lld] is not finite", (long long)e);
+            if (!std::isfinite(H[e]))
+                return fail(h, CCDPP_EINVAL, "H[%lld] is not finite", (long long)e);
     hipStream_t s = h->stream;
     if (W) {
         float* d;
@@ -629,9 +773,8 @@ int ccdpp_set_factors(ccdpp_t* h, const float* W, const float* H) {
         HIPCK(h, ccdk::launch_scatter_factor_in(d, h->cnew2old, h->n, h->k, h->H, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
-    HIPCK(h, ccdk::launch_rebuild_residual(h->L[0].ptr, h->L[0].idx, h->A, h->W, h->H, h->m,
-                                            h->n, h->k, h->nnz, h->L[0].val, s));
-    HIPCK(h, ccdk::launch_scatter_csc(h->L[0].val, h->csr2csc, h->nnz, h->L[1].val, s));
+    HIPCK(h, ccdk::launch_rebuild_residual(h->L[0], h->A, h->W, h->H, h->m, h->n, h->k, s));
+    HIPCK(h, ccdk::launch_scatter_f32(h->L[0].val, h->map01, h->nnz, h->L[1].val, s));
     HIPCK(h, hipStreamSynchronize(s));
     h->pending = -1;
     h->train_sse_valid = false;
@@ -661,7 +804,7 @@ int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, 
     HIPCK(h, hipMemcpyAsync(dc, col, nnz * 4, hipMemcpyHostToDevice, s));
     HIPCK(h, hipMemcpyAsync(dv, val, nnz * 4, hipMemcpyHostToDevice, s));
     HIPCK(h, ccdk::launch_test_err(dr, dc, dv, nnz, h->rold2new, h->cold2new, h->W, h->H, h->m,
-                                    h->n, h->k, h->sse_part, kReduceParts, s));
+                                   h->n, h->k, h->sse_part, kReduceParts, s));
     HIPCK(h, ccdk::launch_reduce_sum(h->sse_part, kReduceParts, h->d_scalar, s));
     double sum = 0.0;
     HIPCK(h, hipMemcpyAsync(&sum, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
@@ -696,7 +839,7 @@ int ccdpp_get_residual(ccdpp_t* h, float* R) {
     float* d;
     Tmp t;
     HIPCK(h, talloc(t, &d, h->nnz));
-    HIPCK(h, ccdk::launch_residual_out(h->L[0].val, h->csr_src, h->nnz, d, s));
+    HIPCK(h, ccdk::launch_scatter_f32(h->L[0].val, h->perm0, h->nnz, d, s));
     HIPCK(h, hipMemcpyAsync(R, d, h->nnz * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
     return CCDPP_OK;
@@ -707,7 +850,7 @@ int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
     if (!mismatches) return fail(h, CCDPP_EINVAL, "mismatches is NULL");
     hipStream_t s = h->stream;
     HIPCK(h, hipMemsetAsync(h->d_count, 0, 8, s));
-    HIPCK(h, ccdk::launch_consistency(h->L[0].val, h->L[1].val, h->csr2csc, h->nnz, h->d_count, s));
+    HIPCK(h, ccdk::launch_consistency(h->L[0].val, h->L[1].val, h->map01, h->nnz, h->d_count, s));
     unsigned long long c = 0;
     HIPCK(h, hipMemcpyAsync(&c, h->d_count, 8, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
@@ -727,40 +870,42 @@ int ccdpp_profile(ccdpp_t* h, int32_t enable) {
     HIPCK(h, hipStreamSynchronize(h->stream));
     collect_profile(h);
     h->prof = enable != 0;
-    for (int i = 0; i < CCDPP_K_COUNT; ++i) {
-        h->prof_launch[i] = 0;
-        h->prof_ms[i] = 0.0;
-        h->prof_bytes[i] = 0.0;
-    }
+    for (int i = 0; i < CCDPP_K_COUNT; ++i)
+        for (int l = 0; l < 2; ++l) {
+            h->prof_launch[i][l] = 0;
+            h->prof_ms[i][l] = 0.0;
+            h->prof_bytes[i][l] = 0.0;
+        }
     return CCDPP_OK;
 }
 
-int ccdpp_profile_read(ccdpp_t* h, int32_t kind, int64_t* launches, double* total_ms,
-                       double* algo_bytes) {
+int ccdpp_profile_read(ccdpp_t* h, int32_t kind, int32_t layout, int64_t* launches,
+                       double* total_ms, double* algo_bytes) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (kind < 0 || kind >= CCDPP_K_COUNT) return fail(h, CCDPP_EINVAL, "bad kernel kind");
-    if (launches) *launches = h->prof_launch[kind];
-    if (total_ms) *total_ms = h->prof_ms[kind];
-    if (algo_bytes) *algo_bytes = h->prof_bytes[kind];
+    if (layout < -1 || layout > 1) return fail(h, CCDPP_EINVAL, "bad layout");
+    int64_t cnt = 0;
+    double ms = 0.0, b = 0.0;
+    for (int l = 0; l < 2; ++l)
+        if (layout < 0 || layout == l) {
+            cnt += h->prof_launch[kind][l];
+            ms += h->prof_ms[kind][l];
+            b += h->prof_bytes[kind][l];
+        }
+    if (launches) *launches = cnt;
+    if (total_ms) *total_ms = ms;
+    if (algo_bytes) *algo_bytes = b;
     return CCDPP_OK;
 }
 
 int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     if (!h) return CCDPP_ESTATE;
     if (!out || len < 0) return fail(h, CCDPP_EINVAL, "bad output buffer");
-    const int64_t v[12] = {h->m,
-                           h->n,
-                           h->nnz,
-                           h->k,
-                           h->build_us,
-                           h->L[0].nblock_rows,
-                           h->L[0].nsplit,
-                           h->L[0].grid,
-                           h->L[1].nblock_rows,
-                           h->L[1].nsplit,
-                           h->L[1].grid,
-                           h->bytes_held};
-    int32_t w = std::min<int32_t>(len, 12);
+    const int64_t v[16] = {h->m,         h->n,         h->nnz,       h->k,
+                           h->build_us,  h->L[0].gather, h->L[0].P,  h->L[0].T,
+                           h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
+                           h->L[1].T,    h->L[1].grid, h->L[1].nseg, h->bytes_held};
+    int32_t w = std::min<int32_t>(len, 16);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }
@@ -772,7 +917,7 @@ const char* ccdpp_last_error(const ccdpp_t* h) {
 
 void ccdpp_destroy(ccdpp_t* h) {
     if (!h) return;
-    if (h->stream) hipStreamSynchronize(h->stream);
+    if (h->stream) (void)hipStreamSynchronize(h->stream);
     destroy_all(h);
     delete h;
 }

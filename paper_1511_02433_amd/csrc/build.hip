@@ -1,13 +1,12 @@
-// Device-side construction of the two compressed residual copies and the
-// utility kernels of the CCD++ library (gfx950).
+// Device-side construction of the compressed residual copies and the utility
+// kernels of the CCD++ library (gfx950).
 //
-// Construction (done once per handle): the observed set Omega of Section 3 is
-// given as triplets.  Rows and columns are relabelled by decreasing degree
-// (the per-row work of Section 6 is proportional to the row length), then
-//   key = new_row * n + new_col   -> radix sort -> row-compressed copy,
-//   key = new_col * m + new_row   -> radix sort -> column-compressed copy,
-// with the map from every row-ordered position to its column-ordered
-// position.  Adjacent equal keys after the first sort are repeated positions.
+// Construction (once per handle): the observed set Omega of Section 3 is given
+// as triplets.  For each copy, every entry gets a key (segment id, column inside
+// its tile) -- the segment order is decided on the host from per-(tile, row)
+// counts -- and a radix sort brings the entries into layout order, carrying the
+// triplet index along so values and the map between the two copies follow.
+// Adjacent equal keys after the user-major sort are repeated positions.
 #include <hipcub/hipcub.hpp>
 
 #include "ccdpp_internal.hpp"
@@ -29,13 +28,32 @@ __global__ void k_histogram(const int32_t* __restrict__ key, int64_t n, int32_t*
         atomicAdd(&count[key[e]], 1);
 }
 
-__global__ void k_make_keys(const int32_t* __restrict__ row, const int32_t* __restrict__ col,
-                            const int32_t* __restrict__ rnew, const int32_t* __restrict__ cnew,
-                            int64_t nnz, int64_t ncols, uint64_t* __restrict__ keys,
-                            int32_t* __restrict__ ids) {
+__global__ void k_map(const int32_t* __restrict__ in, const int32_t* __restrict__ table,
+                      int64_t n, int32_t* __restrict__ out) {
+    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < n; e += (int64_t)gridDim.x * kT)
+        out[e] = table[in[e]];
+}
+
+// Entries per (tile, row) segment: count[(col / T) * rows + row].
+__global__ void k_seg_histogram(const int32_t* __restrict__ lrow, const int32_t* __restrict__ lcol,
+                                int64_t nnz, int32_t rows, int32_t T, int32_t* count) {
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
          e += (int64_t)gridDim.x * kT) {
-        keys[e] = (uint64_t)rnew[row[e]] * (uint64_t)ncols + (uint64_t)cnew[col[e]];
+        const int64_t p = lcol[e] / T;
+        atomicAdd(&count[p * rows + lrow[e]], 1);
+    }
+}
+
+// Sort key of an entry: its segment id, then its column inside the tile.
+__global__ void k_seg_keys(const int32_t* __restrict__ lrow, const int32_t* __restrict__ lcol,
+                           const int32_t* __restrict__ segid, int64_t nnz, int32_t rows, int32_t T,
+                           int cbits, uint64_t* __restrict__ keys, int32_t* __restrict__ ids) {
+    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
+         e += (int64_t)gridDim.x * kT) {
+        const int64_t c = lcol[e];
+        const int64_t p = c / T;
+        const uint64_t s = (uint64_t)segid[p * rows + lrow[e]];
+        keys[e] = (s << cbits) | (uint64_t)(c - p * T);
         ids[e] = (int32_t)e;
     }
 }
@@ -46,38 +64,26 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
         if (keys[p] == keys[p + 1]) *flag = 1;
 }
 
-__global__ void k_csr_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ src,
-                           const float* __restrict__ val_in, int64_t nnz, int64_t ncols,
-                           int64_t nrows, int32_t* __restrict__ idx, float* __restrict__ val,
-                           float* __restrict__ A, uint64_t* __restrict__ keys_csc,
-                           int32_t* __restrict__ ids_csc) {
-    for (int64_t p = (int64_t)blockIdx.x * kT + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kT) {
-        const uint64_t key = keys[p];
-        const uint64_t r = key / (uint64_t)ncols;
-        const uint64_t c = key - r * (uint64_t)ncols;
-        idx[p] = (int32_t)c;
-        const float v = val_in[src[p]];
-        val[p] = v;
-        A[p] = v;
-        keys_csc[p] = c * (uint64_t)nrows + r;
-        ids_csc[p] = (int32_t)p;
+template <class I>
+__global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
+                              const float* __restrict__ val_in, int64_t nnz, uint64_t mask,
+                              I* __restrict__ idx, float* __restrict__ val) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * kT) {
+        idx[q] = (I)(keys[q] & mask);
+        val[q] = val_in[perm[q]];
     }
 }
 
-__global__ void k_csc_fill(const uint64_t* __restrict__ keys_csc, const int32_t* __restrict__ pos,
-                           const float* __restrict__ csr_val, int64_t nnz, int64_t nrows,
-                           int32_t* __restrict__ idx, float* __restrict__ val,
-                           int32_t* __restrict__ csr2csc) {
-    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
-         q += (int64_t)gridDim.x * kT) {
-        const uint64_t key = keys_csc[q];
-        const uint64_t c = key / (uint64_t)nrows;
-        idx[q] = (int32_t)(key - c * (uint64_t)nrows);
-        const int32_t p = pos[q];
-        val[q] = csr_val[p];
-        csr2csc[p] = (int32_t)q;
-    }
+__global__ void k_invert(const int32_t* __restrict__ perm, int64_t n, int32_t* __restrict__ inv) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
+        inv[perm[q]] = (int32_t)q;
+}
+
+__global__ void k_compose(const int32_t* __restrict__ a, const int32_t* __restrict__ b, int64_t n,
+                          int32_t* __restrict__ out) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
+        out[q] = a[b[q]];
 }
 
 __global__ void k_fill(float* __restrict__ dst, float value, int64_t n) {
@@ -109,49 +115,48 @@ __global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* 
     }
 }
 
-// R = A - w_i^T h_j for every row-ordered entry (prediction summed in fp64 over
-// ascending features, one rounding to fp32).
-__global__ void k_rebuild(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+// R = A - w_i^T h_j for every entry of the user-major layout (prediction summed
+// in fp64 over ascending features, one rounding to fp32).  The entry's segment,
+// and from it the row and the tile, are found by binary search.
+template <class I>
+__global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
+                          const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
+                          int32_t P, int32_t T, const I* __restrict__ idx,
                           const float* __restrict__ A, const float* __restrict__ W,
                           const float* __restrict__ H, int64_t m, int64_t n, int32_t k,
-                          int64_t nnz, float* __restrict__ csr_val) {
-    for (int64_t p = (int64_t)blockIdx.x * kT + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kT) {
-        // row of p: the last i with ptr[i] <= p
-        int64_t lo = 0, hi = m;  // invariant ptr[lo] <= p < ptr[hi]
+                          int64_t nnz, float* __restrict__ val) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * kT) {
+        int64_t lo = 0, hi = nseg;  // last s with seg_start[s] <= q
         while (hi - lo > 1) {
             const int64_t mid = (lo + hi) >> 1;
-            if (ptr[mid] <= p) lo = mid; else hi = mid;
+            if (seg_start[mid] <= q) lo = mid; else hi = mid;
         }
-        const int64_t j = idx[p];
+        int32_t plo = 0, phi = P;  // last tile p with tile_seg[p] <= s
+        while (phi - plo > 1) {
+            const int32_t mid = (plo + phi) >> 1;
+            if (tile_seg[mid] <= lo) plo = mid; else phi = mid;
+        }
+        const int64_t i = seg_row[lo];
+        const int64_t j = (int64_t)plo * T + (int64_t)idx[q];
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
-            pred = __builtin_fma((double)W[(int64_t)t * m + lo], (double)H[(int64_t)t * n + j], pred);
-        csr_val[p] = (float)((double)A[p] - pred);
+            pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
+        val[q] = (float)((double)A[q] - pred);
     }
 }
 
-__global__ void k_scatter_csc(const float* __restrict__ csr_val, const int32_t* __restrict__ map,
-                              int64_t nnz, float* __restrict__ csc_val) {
-    for (int64_t p = (int64_t)blockIdx.x * kT + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kT)
-        csc_val[map[p]] = csr_val[p];
+__global__ void k_scatter_f32(const float* __restrict__ src, const int32_t* __restrict__ map,
+                              int64_t n, float* __restrict__ dst) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
+        dst[map[q]] = src[q];
 }
 
-__global__ void k_residual_out(const float* __restrict__ csr_val, const int32_t* __restrict__ src,
-                               int64_t nnz, float* __restrict__ out) {
-    for (int64_t p = (int64_t)blockIdx.x * kT + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kT)
-        out[src[p]] = csr_val[p];
-}
-
-__global__ void k_consistency(const float* __restrict__ csr_val, const float* __restrict__ csc_val,
-                              const int32_t* __restrict__ map, int64_t nnz,
+__global__ void k_consistency(const float* __restrict__ a, const float* __restrict__ b,
+                              const int32_t* __restrict__ map, int64_t n,
                               unsigned long long* count) {
-    for (int64_t p = (int64_t)blockIdx.x * kT + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * kT)
-        if (__float_as_uint(csr_val[p]) != __float_as_uint(csc_val[map[p]]))
-            atomicAdd(count, 1ull);
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
+        if (__float_as_uint(a[q]) != __float_as_uint(b[map[q]])) atomicAdd(count, 1ull);
 }
 
 // Workgroup b sums elements b*256 + t + s*(nparts*256) in order per thread, then a
@@ -203,12 +208,27 @@ hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t* count, hipSt
     return hipGetLastError();
 }
 
-hipError_t launch_make_keys_csr(const int32_t* row, const int32_t* col, const int32_t* rnew,
-                                const int32_t* cnew, int64_t nnz, int64_t ncols, uint64_t* keys,
-                                int32_t* ids, hipStream_t s) {
+hipError_t launch_map(const int32_t* in, const int32_t* table, int64_t n, int32_t* out,
+                      hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_map, grid_for(n), dim3(kT), 0, s, in, table, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_seg_histogram(const int32_t* lrow, const int32_t* lcol, int64_t nnz,
+                                int32_t rows, int32_t T, int32_t* count, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_make_keys, grid_for(nnz), dim3(kT), 0, s, row, col, rnew, cnew, nnz,
-                       ncols, keys, ids);
+    hipLaunchKernelGGL(k_seg_histogram, grid_for(nnz, 8192), dim3(kT), 0, s, lrow, lcol, nnz, rows,
+                       T, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32_t* segid,
+                           int64_t nnz, int32_t rows, int32_t T, int cbits, uint64_t* keys,
+                           int32_t* ids, hipStream_t s) {
+    if (nnz == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_seg_keys, grid_for(nnz), dim3(kT), 0, s, lrow, lcol, segid, nnz, rows, T,
+                       cbits, keys, ids);
     return hipGetLastError();
 }
 
@@ -218,21 +238,30 @@ hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hi
     return hipGetLastError();
 }
 
-hipError_t launch_csr_fill(const uint64_t* keys, const int32_t* src, const float* val_in,
-                           int64_t nnz, int64_t ncols, int64_t nrows, int32_t* idx, float* val,
-                           float* A, uint64_t* keys_csc, int32_t* ids_csc, hipStream_t s) {
+hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
+                              int64_t nnz, int cbits, bool idx16, void* idx, float* val,
+                              hipStream_t s) {
     if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_csr_fill, grid_for(nnz), dim3(kT), 0, s, keys, src, val_in, nnz, ncols,
-                       nrows, idx, val, A, keys_csc, ids_csc);
+    const uint64_t mask = cbits >= 64 ? ~0ull : ((1ull << cbits) - 1);
+    if (idx16)
+        hipLaunchKernelGGL(k_layout_fill<uint16_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
+                           val_in, nnz, mask, static_cast<uint16_t*>(idx), val);
+    else
+        hipLaunchKernelGGL(k_layout_fill<int32_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
+                           val_in, nnz, mask, static_cast<int32_t*>(idx), val);
     return hipGetLastError();
 }
 
-hipError_t launch_csc_fill(const uint64_t* keys_csc, const int32_t* csr_pos, const float* csr_val,
-                           int64_t nnz, int64_t nrows, int32_t* idx, float* val,
-                           int32_t* csr2csc, hipStream_t s) {
-    if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_csc_fill, grid_for(nnz), dim3(kT), 0, s, keys_csc, csr_pos, csr_val, nnz,
-                       nrows, idx, val, csr2csc);
+hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_invert, grid_for(n), dim3(kT), 0, s, perm, n, inv);
+    return hipGetLastError();
+}
+
+hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t* out,
+                          hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_compose, grid_for(n), dim3(kT), 0, s, a, b, n, out);
     return hipGetLastError();
 }
 
@@ -256,35 +285,32 @@ hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2ne
     return hipGetLastError();
 }
 
-hipError_t launch_rebuild_residual(const int64_t* ptr, const int32_t* idx, const float* A,
-                                   const float* W, const float* H, int64_t m, int64_t n,
-                                   int32_t k, int64_t nnz, float* csr_val, hipStream_t s) {
-    if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_rebuild, grid_for(nnz), dim3(kT), 0, s, ptr, idx, A, W, H, m, n, k, nnz,
-                       csr_val);
+hipError_t launch_rebuild_residual(const Layout& L, const float* A, const float* W,
+                                   const float* H, int64_t m, int64_t n, int32_t k,
+                                   hipStream_t s) {
+    if (L.nnz == 0) return hipSuccess;
+    if (L.idx16)
+        hipLaunchKernelGGL(k_rebuild<uint16_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
+                           static_cast<const uint16_t*>(L.idx), A, W, H, m, n, k, L.nnz, L.val);
+    else
+        hipLaunchKernelGGL(k_rebuild<int32_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
+                           static_cast<const int32_t*>(L.idx), A, W, H, m, n, k, L.nnz, L.val);
     return hipGetLastError();
 }
 
-hipError_t launch_scatter_csc(const float* csr_val, const int32_t* csr2csc, int64_t nnz,
-                              float* csc_val, hipStream_t s) {
-    if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_scatter_csc, grid_for(nnz), dim3(kT), 0, s, csr_val, csr2csc, nnz,
-                       csc_val);
+hipError_t launch_scatter_f32(const float* src, const int32_t* map, int64_t n, float* dst,
+                              hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_scatter_f32, grid_for(n), dim3(kT), 0, s, src, map, n, dst);
     return hipGetLastError();
 }
 
-hipError_t launch_residual_out(const float* csr_val, const int32_t* csr_src, int64_t nnz,
-                               float* out, hipStream_t s) {
-    if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_residual_out, grid_for(nnz), dim3(kT), 0, s, csr_val, csr_src, nnz, out);
-    return hipGetLastError();
-}
-
-hipError_t launch_consistency(const float* csr_val, const float* csc_val, const int32_t* csr2csc,
-                              int64_t nnz, unsigned long long* count, hipStream_t s) {
-    if (nnz == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_consistency, grid_for(nnz), dim3(kT), 0, s, csr_val, csc_val, csr2csc,
-                       nnz, count);
+hipError_t launch_consistency(const float* a, const float* b, const int32_t* map, int64_t n,
+                              unsigned long long* count, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_consistency, grid_for(n), dim3(kT), 0, s, a, b, map, n, count);
     return hipGetLastError();
 }
 

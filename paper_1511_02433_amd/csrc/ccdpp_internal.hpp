@@ -12,133 +12,160 @@
 namespace ccdk {
 
 // ---------------------------------------------------------------------------
-// Scheduling.  Rows of a layout (users for the row-compressed copy, items for
-// the column-compressed copy) are relabelled in order of decreasing length, so
-// every scheduling class is a contiguous range of rows and of entries.
-//   class "block": rows longer than kGroupMaxLen; one 256-thread workgroup per
-//                  row piece of at most kPieceMax entries, LDS reduction across
-//                  the 4 waves; rows with several pieces are finished by a
-//                  fixed-order combine kernel.
-//   class G (1..64 lanes per row): rows of length <= G * E handled by groups
-//                  of G lanes (256/G rows per workgroup), each lane taking E
-//                  entries, reduced with DPP / permlane cross-lane moves.
+// Layout and schedule.
+//
+// A layout is one compressed copy of the residual: "rows" are the units whose
+// coordinate a pass computes (users for the u-pass of eq. 15, items for the
+// v-pass of eq. 16) and every entry names a "column" of the other side whose
+// coordinate the pass gathers.
+//
+// The gathered dimension is cut into P tiles of T columns.  Entries are
+// stored tile-major; inside a tile, the non-empty row segments come in order
+// of decreasing length and each segment's entries in increasing column order.
+// A pass stages the tile's slice of every gathered vector in LDS (160 KB per
+// CU on gfx950), so each random gather is an LDS read instead of a cache line
+// pulled from L2.  With P == 1 a segment is a whole row and the pass writes
+// the coordinate directly; with P > 1 every segment yields a partial
+// (numerator, denominator) and a combine kernel adds a row's partials in tile
+// order.  A layout whose tiles would hold too few entries per segment keeps
+// P == 1 and gathers from global memory instead ("global" mode).
+//
+// Work units are wave-sized: a long segment (more than kGroupMaxLen entries)
+// is one unit walked by a whole wave; shorter segments are packed 64/G to a
+// unit, G lanes per segment, E entries per lane.  Persistent workgroups of
+// kWG threads are assigned to tiles in proportion to the tile's entries and
+// their waves take the tile's units in a fixed stride, so the schedule and
+// every reduction order are deterministic.
 // ---------------------------------------------------------------------------
-constexpr int kBlock = 256;           // threads per workgroup, 4 waves of 64
-constexpr int kBlockUnroll = 16;      // entries per thread per step in the block class
-constexpr int kBlockStep = kBlock * kBlockUnroll;  // 4096 entries per workgroup step
-constexpr int kPieceMax = 8 * kBlockStep;           // 32768 entries per workgroup at most
-constexpr int kGroupMaxLen = 1024;    // longest row handled by a lane group
-constexpr int kMaxSegs = 16;
+constexpr int kWG = 1024;                 // threads per persistent workgroup
+constexpr int kWaves = kWG / 64;          // 16 waves
+constexpr int kLongE = 16;                // entries per lane per step of a long segment
+constexpr int kGroupMaxLen = 1024;        // longest segment packed into a lane group
+constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
+constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
 
-enum SegKind : int32_t {
-    kSegBlock = 0,   // workgroup per row piece
-    kSegG1E8 = 1,    // 1 lane per row, <= 8 entries
-    kSegG2E8 = 2,
-    kSegG4E8 = 3,
-    kSegG8E8 = 4,
-    kSegG16E8 = 5,
-    kSegG32E8 = 6,
-    kSegG64E8 = 7,
-    kSegG64E16 = 8,
-};
-
-struct Seg {
-    int32_t kind;
-    int32_t block_begin;   // first workgroup of the segment
-    int32_t row_begin;     // first row (block class: first piece)
-    int32_t row_end;       // one past the last row (block class: one past the last piece)
+enum UnitKind : int32_t {
+    kULong = 0,     // one segment, the whole wave, steps of 64 * kLongE entries
+    kUG64E16 = 1,   // lanes-per-segment G and entries-per-lane E
+    kUG64E8 = 2,
+    kUG32E8 = 3,
+    kUG16E8 = 4,
+    kUG8E8 = 5,
+    kUG4E8 = 6,
+    kUG2E8 = 7,
+    kUG1E8 = 8,
 };
 
 enum PassMode : int32_t {
     kModePlain = 0,     // R-hat read only: y = sum rhat x / (lambda + sum x^2)
-    kModeAdd = 1,       // rhat = fma(p, q, val); store; then as plain with x
+    kModeAdd = 1,       // rhat = fma(p, q, val); store; then as plain
     kModeSubAdd = 2,    // rhat = fma(p, q, fma(-pp, qq, val)); store; then as plain
-    kModeFlush = 3,     // r = fma(-pp, qq, val); store; sum of r^2 per workgroup
+    kModeFlush = 3,     // r = fma(-pp, qq, val); store; per-wave sum of r^2
+};
+
+enum GatherMode : int32_t {
+    kGatherAuto = 0,
+    kGatherGlobal = 1,  // P == 1, gathers from global memory
+    kGatherLds = 2,     // vectors staged in LDS (tiled when they do not fit)
 };
 
 struct PassArgs {
-    const int64_t* ptr;      // [rows + 1]
-    const int32_t* idx;      // [nnz] other-side index of each entry
-    float* val;              // [nnz] residual / R-hat
-    const float* x;          // [cols] gathered vector of the update
-    const float* p;          // [rows] self factor column of the current feature
-    const float* pp;         // [rows] self factor column of the previous feature (committed)
-    const float* q;          // [cols] other factor column of the current feature
-    const float* qq;         // [cols] other factor column of the previous feature (committed)
-    float* y;                // [rows] output coordinates
-    double2* part;           // [npieces] partial (num, den) of split rows
-    double* sse_part;        // [grid] flush: per-workgroup sum of squares
-    const int32_t* piece_row;   // [npieces] row of each block-class piece
-    const int64_t* piece_lo;    // [npieces + 1] first entry of each piece (last: end)
-    int32_t rows;
-    int32_t cols;
-    double lambda;
+    const void* idx;            // [nnz] uint16 or int32 tile-local column
+    float* val;                 // [nnz] residual / R-hat
+    const int64_t* seg_start;   // [S + 1]
+    const int32_t* seg_row;     // [S]
+    const int2* units;          // [U] {first segment, kind | count << 8}
+    const int32_t* wg_tile;     // [grid] tile of each workgroup
+    const int32_t* wg_rank;     // [grid] rank of the workgroup inside its tile
+    const int32_t* tile_unit;   // [P + 1] unit range of each tile
+    const int32_t* tile_nwg;    // [P] workgroups of each tile
+    const float* x;             // [cols] gathered vector of the update
+    const float* p;             // [rows] own factor column, current feature
+    const float* pp;            // [rows] own factor column, previous feature (committed)
+    const float* q;             // [cols] other factor column, current feature
+    const float* qq;            // [cols] other factor column, previous feature (committed)
+    float* y;                   // [rows] coordinates (P == 1)
+    double2* part;              // [S] partial (num, den) per segment (P > 1)
+    double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
+    int64_t nnz;
+    int32_t rows, cols, T, P;
     int32_t nseg;
-    Seg seg[kMaxSegs];
+    int32_t x_is_q;             // x and q are the same vector (staged once)
+    double lambda;
 };
 
 struct CombineArgs {
-    const int32_t* split_row;    // [nsplit] rows with more than one piece
-    const int32_t* split_first;  // [nsplit + 1] first piece of each such row
+    const int32_t* row_seg_ptr;  // [rows + 1]
+    const int32_t* row_segs;     // [S] segments of each row in tile order
     const double2* part;
     float* y;
+    int32_t rows;
     double lambda;
-    int32_t nsplit;
 };
 
 // One compressed copy of the residual plus its schedule.
 struct Layout {
     int64_t rows = 0, cols = 0, nnz = 0;
-    int64_t* ptr = nullptr;
-    int32_t* idx = nullptr;
+    int32_t gather = kGatherGlobal;
+    int32_t T = 0, P = 1;
+    bool idx16 = false;
+    void* idx = nullptr;
     float* val = nullptr;
-    // schedule
-    std::vector<Seg> segs;
-    int32_t grid = 0;              // workgroups per pass
-    int32_t nblock_rows = 0;       // rows in the block class
-    int32_t npieces = 0;
-    int32_t nsplit = 0;            // rows with more than one piece
-    int32_t* piece_row = nullptr;
-    int64_t* piece_lo = nullptr;
-    int32_t* split_row = nullptr;
-    int32_t* split_first = nullptr;
-    double2* part = nullptr;
+    int64_t* seg_start = nullptr;
+    int32_t* seg_row = nullptr;
+    int32_t* tile_seg = nullptr;     // [P + 1] first segment of each tile
+    int2* units = nullptr;
+    int32_t* wg_tile = nullptr;
+    int32_t* wg_rank = nullptr;
+    int32_t* tile_unit = nullptr;
+    int32_t* tile_nwg = nullptr;
+    int32_t* row_seg_ptr = nullptr;  // P > 1
+    int32_t* row_segs = nullptr;     // P > 1
+    double2* part = nullptr;         // P > 1
+    int64_t nseg = 0;
+    int32_t nunits = 0;
+    int32_t grid = 0;                // persistent workgroups per pass
+    int32_t nlong = 0;               // units of the long kind
 };
 
 // Launchers (sweep.hip).
+hipError_t sweep_init();  // raise the dynamic-LDS limit of the staged kernels
 hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const float* p,
                        const float* pp, const float* q, const float* qq, float* y, double lambda,
                        double* sse_part, hipStream_t s);
 hipError_t launch_combine(const Layout& L, float* y, double lambda, hipStream_t s);
 hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s);
 hipError_t launch_reduce_sum(const double* part, int32_t n, double* out, hipStream_t s);
+int staged_vectors(PassMode mode, bool x_is_q);
 
 // Device build and utilities (build.hip).
 hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t* count, hipStream_t s);
-hipError_t launch_make_keys_csr(const int32_t* row, const int32_t* col, const int32_t* rnew,
-                                const int32_t* cnew, int64_t nnz, int64_t ncols, uint64_t* keys,
-                                int32_t* ids, hipStream_t s);
+hipError_t launch_map(const int32_t* in, const int32_t* table, int64_t n, int32_t* out,
+                      hipStream_t s);
+hipError_t launch_seg_histogram(const int32_t* lrow, const int32_t* lcol, int64_t nnz,
+                                int32_t rows, int32_t T, int32_t* count, hipStream_t s);
+hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32_t* segid,
+                           int64_t nnz, int32_t rows, int32_t T, int cbits, uint64_t* keys,
+                           int32_t* ids, hipStream_t s);
 hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hipStream_t s);
-hipError_t launch_csr_fill(const uint64_t* keys, const int32_t* src, const float* val_in,
-                           int64_t nnz, int64_t ncols, int64_t nrows, int32_t* idx, float* val,
-                           float* A, uint64_t* keys_csc, int32_t* ids_csc, hipStream_t s);
-hipError_t launch_csc_fill(const uint64_t* keys_csc, const int32_t* csr_pos, const float* csr_val,
-                           int64_t nnz, int64_t nrows, int32_t* idx, float* val,
-                           int32_t* csr2csc, hipStream_t s);
+hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
+                              int64_t nnz, int cbits, bool idx16, void* idx, float* val,
+                              hipStream_t s);
+hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
+hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t* out,
+                          hipStream_t s);
 hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t s);
 hipError_t launch_scatter_factor_in(const float* rowmajor, const int32_t* new2old, int64_t rows,
                                     int32_t k, float* colmajor, hipStream_t s);
 hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2new, int64_t rows,
                                     int32_t k, float* rowmajor, hipStream_t s);
-hipError_t launch_rebuild_residual(const int64_t* ptr, const int32_t* idx, const float* A,
-                                   const float* W, const float* H, int64_t m, int64_t n,
-                                   int32_t k, int64_t nnz, float* csr_val, hipStream_t s);
-hipError_t launch_scatter_csc(const float* csr_val, const int32_t* csr2csc, int64_t nnz,
-                              float* csc_val, hipStream_t s);
-hipError_t launch_residual_out(const float* csr_val, const int32_t* csr_src, int64_t nnz,
-                               float* out, hipStream_t s);
-hipError_t launch_consistency(const float* csr_val, const float* csc_val, const int32_t* csr2csc,
-                              int64_t nnz, unsigned long long* count, hipStream_t s);
+hipError_t launch_rebuild_residual(const Layout& L, const float* A, const float* W,
+                                   const float* H, int64_t m, int64_t n, int32_t k,
+                                   hipStream_t s);
+hipError_t launch_scatter_f32(const float* src, const int32_t* map, int64_t n, float* dst,
+                              hipStream_t s);
+hipError_t launch_consistency(const float* a, const float* b, const int32_t* map, int64_t n,
+                              unsigned long long* count, hipStream_t s);
 hipError_t launch_sq_sum(const float* v, int64_t n, double* part, int32_t nparts,
                          hipStream_t s);
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,

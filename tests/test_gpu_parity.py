@@ -160,3 +160,68 @@ def test_zero_lambda_and_empty_rows():
             Wo, Ho = o.factors()
             assert colscaled_max_rel_err(Wg, Wo) <= W_TOL
             assert colscaled_max_rel_err(Hg, Ho) <= W_TOL
+
+
+# Every layout strategy on the same problem: automatic, global-memory gathers,
+# LDS staging with small tiles (several tiles per side, per-tile partials and the
+# combine), and very few persistent workgroups (long unit loops per wave).
+LAYOUTS = {
+    "auto": dict(),
+    "global": dict(gather_mode=(1, 1)),
+    "tiled": dict(gather_mode=(2, 2), tile_width=(192, 128)),
+    "tiled_odd": dict(gather_mode=(2, 2), tile_width=(100, 333), workgroups=3),
+    "mixed": dict(gather_mode=(1, 2), tile_width=(0, 64), workgroups=1),
+}
+
+
+@pytest.mark.parametrize("name", list(LAYOUTS))
+def test_layout_strategies_match_oracle(name):
+    from paper_1511_02433_amd.ccdpp import make_options
+    # A few heavy rows plus many short ones, so long segments and every lane-group
+    # class occur on the user side; item lengths follow from the random columns.
+    lens = [850, 700, 300, 40] + list(np.random.default_rng(31).integers(0, 80, 1496))
+    row, col, val, H0 = synth.lengths_problem(lens, 900, 4, seed=32)
+    print(f"case: layout {name} nnz={row.size}", flush=True)
+    opts = make_options(**LAYOUTS[name])
+    g = CCDPP(1500, 900, 4, 0.1, row, col, val, opts=opts)
+    info = g.info()
+    print({k: v for k, v in info.items() if k.startswith(("u_", "v_"))})
+    g.set_factors(np.zeros((1500, 4), np.float32), H0)
+    o = Oracle(1500, 900, 4, 0.1, row, col, val, H0)
+    for outer in range(2):
+        g.run(1, 2)
+        o.run(1, 2)
+        Wg, Hg = g.factors()
+        Wo, Ho = o.factors()
+        ew, eh = colscaled_max_rel_err(Wg, Wo), colscaled_max_rel_err(Hg, Ho)
+        print(f"outer {outer}: W err {ew:.3e}  H err {eh:.3e}")
+        if outer == 0:
+            assert ew <= W_TOL and eh <= W_TOL
+    assert abs(g.train_rmse() - o.train_rmse()) <= RMSE_TOL
+    assert g.check_consistency() == 0
+    if name == "tiled":
+        assert info["u_tiles"] > 1 and info["v_tiles"] > 1
+    if name == "global":
+        assert info["u_gather"] == 1 and info["v_gather"] == 1
+
+
+def test_heavy_rows_in_tiles_and_layout_equivalence():
+    # Rows far longer than kGroupMaxLen inside tiles, plus the same problem under two
+    # layouts: results agree to summation-order rounding.
+    from paper_1511_02433_amd.ccdpp import make_options
+    lens = [5000, 3000, 2049, 1025, 1024, 513, 200, 64, 9, 1, 0] * 3
+    row, col, val, H0 = synth.lengths_problem(lens, 6000, 3, seed=41)
+    m = len(lens)
+    print("case: heavy rows in tiles", flush=True)
+    res = []
+    for opts in (make_options(), make_options(gather_mode=(2, 2), tile_width=(512, 16))):
+        g = CCDPP(m, 6000, 3, 0.05, row, col, val, opts=opts)
+        g.set_factors(np.zeros((m, 3), np.float32), H0)
+        g.run(1, 3)
+        res.append(g.factors())
+        assert g.check_consistency() == 0
+    o = Oracle(m, 6000, 3, 0.05, row, col, val, H0)
+    o.run(1, 3)
+    Wo, Ho = o.factors()
+    for W, H in res:
+        assert colscaled_max_rel_err(W, Wo) <= W_TOL and colscaled_max_rel_err(H, Ho) <= W_TOL
