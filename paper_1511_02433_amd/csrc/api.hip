@@ -50,9 +50,12 @@ struct ccdpp {
     int32_t* rold2new = nullptr;
     int32_t* cnew2old = nullptr;
     int32_t* cold2new = nullptr;
-    int32_t* perm0 = nullptr;      // user-major position -> input triplet index
-    int32_t* map01 = nullptr;      // user-major position -> item-major position
-    float* A = nullptr;            // ratings, user-major order
+    // Entry e of the user-major copy in layout order, padding excluded:
+    int32_t* perm0 = nullptr;      // e -> input triplet index
+    int32_t* pos0 = nullptr;       // e -> padded position in the user-major copy
+    int32_t* map01 = nullptr;      // e -> padded position in the item-major copy
+    float* A = nullptr;            // A[e], the rating of entry e
+    float* fseg[2] = {};           // P > 1: own factor columns spread over segments (k x S)
     float* W = nullptr;            // k x m: W[t*m + i]
     float* H = nullptr;            // k x n
     float* u = nullptr;
@@ -181,31 +184,22 @@ void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
     for (int64_t i = 0; i < N; ++i) old2new[new2old[i]] = (int32_t)i;
 }
 
-// Unit kinds for lane groups: {kind, longest segment, lanes per segment}.
-struct GroupClass {
-    int kind;
-    int64_t maxlen;
-    int g;
-};
-const GroupClass kClasses[] = {{ccdk::kUG64E16, 1024, 64}, {ccdk::kUG64E8, 512, 64},
-                               {ccdk::kUG32E8, 256, 32},   {ccdk::kUG16E8, 128, 16},
-                               {ccdk::kUG8E8, 64, 8},      {ccdk::kUG4E8, 32, 4},
-                               {ccdk::kUG2E8, 16, 2},      {ccdk::kUG1E8, 8, 1}};
-
 // Build one layout.  lrow/lcol: relabelled row and gathered-column id of every
 // input triplet (device).  side 0 is the user-major copy (its first pass stages
 // q and qq, x being q), side 1 the item-major copy (first pass stages x, q, qq).
-// On return perm holds, for every layout position, the input triplet index.
+// On return, for every entry e in layout order (padding excluded), perm[e] holds
+// its input triplet index and epos[e] its padded position.
 int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, const int32_t* lrow,
                  const int32_t* lcol, const float* val_in, const ccdpp_options_t* opt,
-                 int32_t* perm, hipStream_t s) {
+                 int32_t* perm, int32_t* epos, hipStream_t s) {
     using namespace ccdk;
     const int64_t N = h->nnz;
     L.rows = rows;
     L.cols = cols;
     L.nnz = N;
     const int nvec = side == 0 ? 2 : 3;
-    const int64_t tmax = ((int64_t)kLdsBytes / (4 * nvec)) / 64 * 64;
+    // Each staged slice holds T floats plus a trailing zero (the padding entries' target).
+    const int64_t tmax = ((int64_t)kLdsVecBytes / (4 * nvec) - 1) / 64 * 64;
     const int forced = opt ? opt->gather_mode[side] : 0;
     const int64_t forced_T = opt ? opt->tile_width[side] : 0;
     if (forced_T > tmax)
@@ -253,25 +247,23 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     L.gather = lds ? kGatherLds : kGatherGlobal;
     L.T = (int32_t)T;
     L.P = (int32_t)P;
-    L.idx16 = T <= 65536;
+    L.idx16 = T < 65536;  // tile-local indices 0..T-1 and the padding index T fit 16 bits
 
-    // Segments: per tile, rows in order of decreasing count (all rows when P == 1,
-    // so every row gets its coordinate written; only non-empty rows otherwise).
+    // Segments.  P == 1: segment r is row r (rows are relabelled by decreasing
+    // length, so the empty ones come last).  P > 1: the non-empty rows of each
+    // tile in increasing row order.
     std::vector<int32_t> segid((size_t)(P * rows), -1), seg_row, tile_seg(P + 1, 0);
     std::vector<int64_t> seg_start;
-    std::vector<int32_t> order;
     int64_t pos = 0;
     for (int64_t p = 0; p < P; ++p) {
         tile_seg[p] = (int32_t)seg_row.size();
-        order.clear();
         const int32_t* cp = cnt.data() + p * rows;
-        for (int64_t r = 0; r < rows; ++r)
-            if (P == 1 || cp[r] > 0) order.push_back((int32_t)r);
-        std::stable_sort(order.begin(), order.end(),
-                         [&](int32_t a, int32_t b) { return cp[a] > cp[b]; });
-        for (int32_t r : order) {
+        for (int64_t r = 0; r < rows; ++r) {
+            if (P > 1 && cp[r] == 0) continue;
+            if (P == 1 && r > 0 && cp[r] > cp[r - 1])
+                return fail(h, CCDPP_EDEVICE, "internal: rows are not in decreasing length");
             segid[p * rows + r] = (int32_t)seg_row.size();
-            seg_row.push_back(r);
+            seg_row.push_back((int32_t)r);
             seg_start.push_back(pos);
             pos += cp[r];
         }
@@ -281,53 +273,69 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     const int64_t S = (int64_t)seg_row.size();
     if (pos != N) return fail(h, CCDPP_EDEVICE, "internal: segment counts do not cover nnz");
     L.nseg = S;
+    int64_t S_ne = S;
+    while (S_ne > 0 && seg_start[S_ne] == seg_start[S_ne - 1]) --S_ne;
+    L.nseg_ne = S_ne;
 
-    // Units per tile and their tile ranges.
-    std::vector<int2> units;
-    std::vector<int32_t> tile_unit(P + 1, 0);
-    int32_t nlong = 0;
-    for (int64_t p = 0; p < P; ++p) {
-        tile_unit[p] = (int32_t)units.size();
-        const int64_t sb = tile_seg[p], se = tile_seg[p + 1];
-        int64_t si = sb;
-        while (si < se && seg_start[si + 1] - seg_start[si] > kGroupMaxLen) {
-            units.push_back(make_int2((int32_t)si, kULong | (1 << 8)));
-            ++nlong;
-            ++si;
-        }
-        for (int ci = 0; ci < 8; ++ci) {
-            const int64_t minlen = ci + 1 < 8 ? kClasses[ci + 1].maxlen + 1 : 0;
-            const int per = 64 / kClasses[ci].g;
-            int64_t e = si;
-            while (e < se && seg_start[e + 1] - seg_start[e] >= minlen) ++e;
-            for (int64_t u0 = si; u0 < e; u0 += per) {
-                const int c = (int)std::min<int64_t>(per, e - u0);
-                units.push_back(make_int2((int32_t)u0, kClasses[ci].kind | (c << 8)));
+    // Persistent workgroups.  Workgroup g owns the entries from the first segment
+    // start at or after g * N / G up to the same point for g + 1, so every share is
+    // within one segment of N / G.  A share is processed as one piece per tile it
+    // touches; inside a piece the 16 waves own chunks cut the same way.  Chunk
+    // bounds are kept as segment indices here and turned into padded positions below.
+    int64_t G = opt && opt->workgroups > 0 ? opt->workgroups : (int64_t)h->cus;
+    if (!(opt && opt->workgroups > 0))
+        G = std::max<int64_t>(1, std::min<int64_t>(G, (N + kWaves * kWin - 1) / (kWaves * kWin)));
+    const int64_t S_work = P == 1 ? S_ne : S;  // segments that hold entries
+    auto seg_at = [&](int64_t s_lo, int64_t s_hi, int64_t target) -> int64_t {
+        // first segment in [s_lo, s_hi] whose start is >= target (s_hi if none)
+        return std::lower_bound(seg_start.begin() + s_lo, seg_start.begin() + s_hi, target) -
+               seg_start.begin();
+    };
+    std::vector<int32_t> wg_piece(1, 0), piece_tile, piece_seg;
+    std::vector<int64_t> chunk_segs;  // [npieces * (kWaves + 1)] segment index of each bound
+    std::vector<char> chunk_start((size_t)S + 1, 0);
+    int64_t g_seg = 0;
+    for (int64_t g = 0; g < G; ++g) {
+        const int64_t g_end = g + 1 == G ? S_work : seg_at(g_seg, S_work, N * (g + 1) / G);
+        for (int64_t p = 0; p < P && g_seg < g_end; ++p) {
+            const int64_t a0 = std::max<int64_t>(g_seg, tile_seg[p]);
+            const int64_t a1 = std::min<int64_t>(g_end, tile_seg[p + 1]);
+            if (a0 >= a1 || seg_start[a0] == seg_start[a1]) continue;
+            const int64_t lo = seg_start[a0], hi = seg_start[a1];
+            piece_tile.push_back((int32_t)p);
+            int64_t sw = a0;
+            for (int w = 0; w < kWaves; ++w) {
+                chunk_segs.push_back(sw);
+                piece_seg.push_back((int32_t)sw);
+                chunk_start[sw] = 1;
+                sw = w + 1 == kWaves ? a1 : seg_at(sw, a1, lo + (hi - lo) * (w + 1) / kWaves);
             }
-            si = e;
+            chunk_segs.push_back(a1);
         }
-        if (si != se) return fail(h, CCDPP_EDEVICE, "internal: units do not cover the tile");
+        wg_piece.push_back((int32_t)piece_tile.size());
+        g_seg = g_end;
     }
-    tile_unit[P] = (int32_t)units.size();
-    L.nunits = (int32_t)units.size();
-    L.nlong = nlong;
+    L.grid = (int32_t)G;
+    L.npieces = (int32_t)piece_tile.size();
 
-    // Persistent workgroups, given to tiles in proportion to their entries.
-    const int64_t want = opt && opt->workgroups > 0 ? opt->workgroups : 2 * (int64_t)h->cus;
-    std::vector<int32_t> wg_tile, wg_rank, tile_nwg(P, 0);
-    for (int64_t p = 0; p < P; ++p) {
-        const int64_t ent = seg_start[tile_seg[p + 1]] - seg_start[tile_seg[p]];
-        const int64_t nu = tile_unit[p + 1] - tile_unit[p];
-        int64_t w = N > 0 ? (want * ent + N / 2) / N : (p == 0 ? want : 0);
-        w = std::min<int64_t>(w, (nu + kWaves - 1) / kWaves);
-        w = std::max<int64_t>(w, nu > 0 ? 1 : 0);
-        tile_nwg[p] = (int32_t)w;
-        for (int64_t r = 0; r < w; ++r) {
-            wg_tile.push_back((int32_t)p);
-            wg_rank.push_back((int32_t)r);
-        }
+    // Alignment padding: every chunk start moves up to the next multiple of kE; the
+    // entries skipped over are padding at the end of the segment before it.
+    std::vector<int32_t> seg_off((size_t)S, 0);
+    std::vector<int64_t> pstart((size_t)S + 1);
+    int64_t off = 0;
+    for (int64_t sg = 0; sg < S_work; ++sg) {
+        if (chunk_start[sg]) off += (kE - (seg_start[sg] + off) % kE) % kE;
+        seg_off[sg] = (int32_t)off;
+        pstart[sg] = seg_start[sg] + off;
     }
-    L.grid = (int32_t)wg_tile.size();
+    const int64_t NP = (N + off + kE - 1) / kE * kE;
+    if (NP > (int64_t)INT32_MAX - kEntryPad)
+        return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
+    for (int64_t sg = S_work; sg <= S; ++sg) pstart[sg] = NP;
+    L.npad = NP;
+    std::vector<int64_t> piece_chunk(chunk_segs.size());
+    for (size_t i = 0; i < chunk_segs.size(); ++i) piece_chunk[i] = pstart[chunk_segs[i]];
+    seg_start.swap(pstart);
 
     // Segments of each row in tile order (for the combine of P > 1).
     if (P > 1) {
@@ -348,33 +356,38 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     RCK(upload(h, &L.seg_start, seg_start));
     RCK(upload(h, &L.seg_row, seg_row));
     RCK(upload(h, &L.tile_seg, tile_seg));
-    RCK(upload(h, &L.units, units));
-    RCK(upload(h, &L.wg_tile, wg_tile));
-    RCK(upload(h, &L.wg_rank, wg_rank));
-    RCK(upload(h, &L.tile_unit, tile_unit));
-    RCK(upload(h, &L.tile_nwg, tile_nwg));
+    RCK(upload(h, &L.wg_piece, wg_piece));
+    RCK(upload(h, &L.piece_tile, piece_tile));
+    RCK(upload(h, &L.piece_chunk, piece_chunk));
+    RCK(upload(h, &L.piece_seg, piece_seg));
 
     // Sort the entries into layout order and fill index and value arrays.
     const int cbits = bits_for((uint64_t)std::max<int64_t>(T - 1, 1));
     const int sbits = bits_for((uint64_t)std::max<int64_t>(S - 1, 1));
     if (cbits + sbits > 64) return fail(h, CCDPP_EDEVICE, "internal: sort key too wide");
-    HIPCK(h, dalloc(h, &L.val, N));
+    // Padding entries (and kEntryPad more after the end, for whole-lane vector loads)
+    // hold value 0 and the padding index T.
+    HIPCK(h, dalloc(h, &L.val, NP + kEntryPad));
+    HIPCK(h, launch_fill(L.val, 0.0f, NP + kEntryPad, s));
     if (L.idx16) {
         uint16_t* d;
-        HIPCK(h, dalloc(h, &d, N));
+        HIPCK(h, dalloc(h, &d, NP + kEntryPad));
         L.idx = d;
     } else {
         int32_t* d;
-        HIPCK(h, dalloc(h, &d, N));
+        HIPCK(h, dalloc(h, &d, NP + kEntryPad));
         L.idx = d;
     }
+    HIPCK(h, launch_fill_idx(L.idx, L.idx16, (int32_t)T, NP + kEntryPad, s));
     if (N > 0) {
-        int32_t* d_segid;
+        int32_t *d_segid, *d_off;
         uint64_t *k0, *k1;
         int32_t* i0;
-        Tmp tsid, tk0, tk1, ti0, ttmp;
+        Tmp tsid, toff, tk0, tk1, ti0, ttmp;
         HIPCK(h, talloc(tsid, &d_segid, P * rows));
         HIPCK(h, hipMemcpyAsync(d_segid, segid.data(), segid.size() * 4, hipMemcpyHostToDevice, s));
+        HIPCK(h, talloc(toff, &d_off, S));
+        HIPCK(h, hipMemcpyAsync(d_off, seg_off.data(), seg_off.size() * 4, hipMemcpyHostToDevice, s));
         HIPCK(h, talloc(tk0, &k0, N));
         HIPCK(h, talloc(tk1, &k1, N));
         HIPCK(h, talloc(ti0, &i0, N));
@@ -396,9 +409,21 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             HIPCK(h, hipStreamSynchronize(s));
             if (flag) return fail(h, CCDPP_EDUP, "a position (i, j) occurs more than once");
         }
-        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, L.idx16, L.idx, L.val, s));
+        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, d_off, L.idx16, L.idx, L.val, epos,
+                                    s));
         HIPCK(h, hipStreamSynchronize(s));
     }
+    return CCDPP_OK;
+}
+
+// Refresh the per-segment copies of W (user-major copy) and H (item-major copy).
+int spread_factors(ccdpp* h) {
+    for (int li = 0; li < 2; ++li)
+        if (h->fseg[li]) {
+            const Layout& L = h->L[li];
+            HIPCK(h, ccdk::launch_seg_spread(li == 0 ? h->W : h->H, L.rows, L.seg_row, L.nseg,
+                                             h->k, h->fseg[li], h->stream));
+        }
     return CCDPP_OK;
 }
 
@@ -462,20 +487,24 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
 
     // The two copies, the ratings in user-major order and the map between copies.
     HIPCK(h, dalloc(h, &h->perm0, N));
-    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, s));
+    HIPCK(h, dalloc(h, &h->pos0, N));
+    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s));
     {
-        int32_t *perm1, *inv1;
-        Tmp tp1, tinv;
+        int32_t *perm1, *pos1, *inv1, *e01;
+        Tmp tp1, tq1, tinv, te;
         HIPCK(h, talloc(tp1, &perm1, N));
-        RCK(build_layout(h, 1, h->L[1], n, m, d_ci, d_ru, d_val, opt, perm1, s));
+        HIPCK(h, talloc(tq1, &pos1, N));
+        RCK(build_layout(h, 1, h->L[1], n, m, d_ci, d_ru, d_val, opt, perm1, pos1, s));
         HIPCK(h, talloc(tinv, &inv1, N));
         HIPCK(h, launch_invert(perm1, N, inv1, s));
+        HIPCK(h, talloc(te, &e01, N));
+        HIPCK(h, launch_compose(inv1, h->perm0, N, e01, s));  // item-major entry index
         HIPCK(h, dalloc(h, &h->map01, N));
-        HIPCK(h, launch_compose(inv1, h->perm0, N, h->map01, s));
+        HIPCK(h, launch_compose(pos1, e01, N, h->map01, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
     HIPCK(h, dalloc(h, &h->A, N));
-    if (N) HIPCK(h, hipMemcpyAsync(h->A, h->L[0].val, N * 4, hipMemcpyDeviceToDevice, s));
+    HIPCK(h, launch_copy_mapped(h->L[0].val, h->pos0, h->A, nullptr, N, s));
 
     // Factors: W = 0 (Algorithm 3), H from the seed; scratch.
     HIPCK(h, dalloc(h, &h->W, (int64_t)h->k * m));
@@ -490,9 +519,11 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, launch_fill(h->u, 0.0f, m, s));
     HIPCK(h, launch_fill(h->v, 0.0f, n, s));
     for (int li = 0; li < 2; ++li)
-        if (h->L[li].part)  // partials are written before they are read: start them as NaN
+        if (h->L[li].part) {  // partials are written before they are read: start them as NaN
             HIPCK(h, launch_fill(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
                                  4 * h->L[li].nseg, s));
+            HIPCK(h, dalloc(h, &h->fseg[li], (int64_t)h->k * h->L[li].nseg));
+        }
     {
         std::vector<float> h0((size_t)n * h->k);
         for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
@@ -501,6 +532,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, talloc(th0, &d_h0, n * h->k));
         HIPCK(h, hipMemcpyAsync(d_h0, h0.data(), h0.size() * 4, hipMemcpyHostToDevice, s));
         HIPCK(h, launch_scatter_factor_in(d_h0, h->cnew2old, n, h->k, h->H, s));
+        RCK(spread_factors(h));
         HIPCK(h, hipStreamSynchronize(s));
     }
     h->pending = -1;
@@ -579,7 +611,7 @@ void collect_profile(ccdpp* h) {
 double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors) {
     using namespace ccdk;
     const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
-    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz + 12.0 * S;
+    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz + 8.0 * S;
     if (mode != kModePlain) b += 4.0 * nnz;
     if (mode != kModeFlush) b += L.P == 1 ? 4.0 * S : 16.0 * S;
     if (mode == kModeAdd || mode == kModeSubAdd) b += 4.0 * S;
@@ -588,20 +620,33 @@ double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors) {
     return b;
 }
 
-int pass(ccdpp* h, int li, ccdk::PassMode mode, const float* x, const float* p, const float* pp,
-         const float* q, const float* qq, float* y, int gathered) {
+// Own factor column t of layout li as the pass reads it: by segment, which with
+// P == 1 is the column itself.
+float* seg_col(ccdpp* h, int li, int32_t t) {
+    const Layout& L = h->L[li];
+    if (t < 0) return nullptr;
+    if (L.P == 1) return (li == 0 ? h->W : h->H) + (int64_t)t * L.rows;
+    return h->fseg[li] + (int64_t)t * L.nseg;
+}
+
+// One pass over layout li, then (P > 1) the combine, which also refreshes the
+// per-segment copy of column `commit` when the pass produces a committed column.
+int pass(ccdpp* h, int li, ccdk::PassMode mode, const float* x, int32_t pcol, int32_t ppcol,
+         const float* q, const float* qq, float* y, int32_t commit, int gathered) {
     const Layout& L = h->L[li];
     const int kind = mode == ccdk::kModePlain ? CCDPP_K_PASS
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
                                                 : CCDPP_K_PASS_FUSED;
     {
         Timed tm(h, kind, li, pass_bytes(L, mode, gathered));
-        HIPCK(h, ccdk::launch_pass(L, mode, x, p, pp, q, qq, y, h->lambda, h->sse_part, h->stream));
+        HIPCK(h, ccdk::launch_pass(L, mode, x, seg_col(h, li, pcol), seg_col(h, li, ppcol), q, qq,
+                                   y, h->lambda, h->sse_part, h->stream));
         tm.done();
     }
     if (mode != ccdk::kModeFlush && L.P > 1) {
-        Timed tc(h, CCDPP_K_COMBINE, li, 20.0 * L.nseg + 8.0 * L.rows);
-        HIPCK(h, ccdk::launch_combine(L, y, h->lambda, h->stream));
+        float* yseg = commit >= 0 ? seg_col(h, li, commit) : nullptr;
+        Timed tc(h, CCDPP_K_COMBINE, li, 20.0 * L.nseg + 8.0 * L.rows + (yseg ? 4.0 * L.nseg : 0.0));
+        HIPCK(h, ccdk::launch_combine(L, y, yseg, h->lambda, h->stream));
         tc.done();
     }
     return CCDPP_OK;
@@ -683,18 +728,20 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
             const float* Wp = prev ? h->W + (int64_t)h->pending * m : nullptr;
             const float* Hp = prev ? h->H + (int64_t)h->pending * n : nullptr;
             const PassMode first = prev ? kModeSubAdd : kModeAdd;
+            const int32_t pend = prev ? h->pending : -1;
             const int g1 = prev ? 2 : 1;
+            const int32_t c1 = inner == 1 ? t : -1;  // with one inner pass, u and v are committed
             // First u-pass: eq. 18 of the pending feature, eq. 13, eq. 15 with v = hbar_t.
-            RCK(pass(h, 0, first, Ht, Wt, Wp, Ht, Hp, h->u, g1));
+            RCK(pass(h, 0, first, Ht, t, pend, Ht, Hp, h->u, c1, g1));
             // First v-pass: the same residual update on the item-major copy, eq. 16 with the new u.
             float* yv = inner == 1 ? Ht : h->v;
-            RCK(pass(h, 1, first, h->u, Ht, Hp, Wt, Wp, yv, g1 + 1));
+            RCK(pass(h, 1, first, h->u, t, pend, Wt, Wp, yv, c1, g1 + 1));
             for (int32_t s = 2; s <= inner; ++s) {
                 const bool last = s == inner;
                 float* yu = last ? Wt : h->u;  // the last u is committed in place (eq. 17)
-                RCK(pass(h, 0, kModePlain, h->v, nullptr, nullptr, nullptr, nullptr, yu, 1));
-                RCK(pass(h, 1, kModePlain, yu, nullptr, nullptr, nullptr, nullptr,
-                         last ? Ht : h->v, 1));
+                RCK(pass(h, 0, kModePlain, h->v, -1, -1, nullptr, nullptr, yu, last ? t : -1, 1));
+                RCK(pass(h, 1, kModePlain, yu, -1, -1, nullptr, nullptr, last ? Ht : h->v,
+                         last ? t : -1, 1));
             }
             if (inner == 1) {
                 Timed tm(h, CCDPP_K_COMMIT, 0, 8.0 * m);
@@ -708,9 +755,9 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
         // Final eq. 18 on both copies; the user-major one also sums R^2 for the training RMSE.
         const float* Wp = h->W + (int64_t)h->pending * m;
         const float* Hp = h->H + (int64_t)h->pending * n;
-        RCK(pass(h, 0, kModeFlush, nullptr, nullptr, Wp, nullptr, Hp, nullptr, 1));
+        RCK(pass(h, 0, kModeFlush, nullptr, -1, h->pending, nullptr, Hp, nullptr, -1, 1));
         HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
-        RCK(pass(h, 1, kModeFlush, nullptr, nullptr, Hp, nullptr, Wp, nullptr, 1));
+        RCK(pass(h, 1, kModeFlush, nullptr, -1, h->pending, nullptr, Wp, nullptr, -1, 1));
         h->pending = -1;
         double sse = 0.0;
         HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
@@ -773,8 +820,10 @@ int ccdpp_set_factors(ccdpp_t* h, const float* W, const float* H) {
         HIPCK(h, ccdk::launch_scatter_factor_in(d, h->cnew2old, h->n, h->k, h->H, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
-    HIPCK(h, ccdk::launch_rebuild_residual(h->L[0], h->A, h->W, h->H, h->m, h->n, h->k, s));
-    HIPCK(h, ccdk::launch_scatter_f32(h->L[0].val, h->map01, h->nnz, h->L[1].val, s));
+    RCK(spread_factors(h));
+    HIPCK(h, ccdk::launch_rebuild_residual(h->L[0], h->pos0, h->A, h->W, h->H, h->m, h->n, h->k,
+                                           s));
+    HIPCK(h, ccdk::launch_copy_mapped(h->L[0].val, h->pos0, h->L[1].val, h->map01, h->nnz, s));
     HIPCK(h, hipStreamSynchronize(s));
     h->pending = -1;
     h->train_sse_valid = false;
@@ -819,7 +868,7 @@ int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
     if (h->nnz < 1) return fail(h, CCDPP_EINVAL, "no observed entries");
     if (!h->train_sse_valid) {
         hipStream_t s = h->stream;
-        HIPCK(h, ccdk::launch_sq_sum(h->L[0].val, h->nnz, h->sse_part, kReduceParts, s));
+        HIPCK(h, ccdk::launch_sq_sum(h->L[0].val, h->L[0].npad, h->sse_part, kReduceParts, s));
         HIPCK(h, ccdk::launch_reduce_sum(h->sse_part, kReduceParts, h->d_scalar, s));
         double sum = 0.0;
         HIPCK(h, hipMemcpyAsync(&sum, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
@@ -839,7 +888,7 @@ int ccdpp_get_residual(ccdpp_t* h, float* R) {
     float* d;
     Tmp t;
     HIPCK(h, talloc(t, &d, h->nnz));
-    HIPCK(h, ccdk::launch_scatter_f32(h->L[0].val, h->perm0, h->nnz, d, s));
+    HIPCK(h, ccdk::launch_copy_mapped(h->L[0].val, h->pos0, d, h->perm0, h->nnz, s));
     HIPCK(h, hipMemcpyAsync(R, d, h->nnz * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
     return CCDPP_OK;
@@ -850,7 +899,8 @@ int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
     if (!mismatches) return fail(h, CCDPP_EINVAL, "mismatches is NULL");
     hipStream_t s = h->stream;
     HIPCK(h, hipMemsetAsync(h->d_count, 0, 8, s));
-    HIPCK(h, ccdk::launch_consistency(h->L[0].val, h->L[1].val, h->map01, h->nnz, h->d_count, s));
+    HIPCK(h, ccdk::launch_consistency(h->L[0].val, h->pos0, h->L[1].val, h->map01, h->nnz,
+                                      h->d_count, s));
     unsigned long long c = 0;
     HIPCK(h, hipMemcpyAsync(&c, h->d_count, 8, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));

@@ -64,15 +64,27 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
         if (keys[p] == keys[p + 1]) *flag = 1;
 }
 
+// Entry q of the sorted order goes to padded position q + seg_off[segment].
 template <class I>
 __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
-                              const float* __restrict__ val_in, int64_t nnz, uint64_t mask,
-                              I* __restrict__ idx, float* __restrict__ val) {
+                              const float* __restrict__ val_in, int64_t nnz, int cbits,
+                              uint64_t mask, const int32_t* __restrict__ seg_off,
+                              I* __restrict__ idx, float* __restrict__ val,
+                              int32_t* __restrict__ pos) {
     for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * kT) {
-        idx[q] = (I)(keys[q] & mask);
-        val[q] = val_in[perm[q]];
+        const uint64_t key = keys[q];
+        const int64_t p = q + seg_off[key >> cbits];
+        idx[p] = (I)(key & mask);
+        val[p] = val_in[perm[q]];
+        pos[q] = (int32_t)p;
     }
+}
+
+template <class I>
+__global__ void k_fill_idx(I* __restrict__ idx, I value, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
+        idx[i] = value;
 }
 
 __global__ void k_invert(const int32_t* __restrict__ perm, int64_t n, int32_t* __restrict__ inv) {
@@ -116,17 +128,19 @@ __global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* 
 }
 
 // R = A - w_i^T h_j for every entry of the user-major layout (prediction summed
-// in fp64 over ascending features, one rounding to fp32).  The entry's segment,
-// and from it the row and the tile, are found by binary search.
+// in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
+// unpadded layout order) sits at position pos[e]; its segment, and from it the
+// row and the tile, are found by binary search.
 template <class I>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
                           int32_t P, int32_t T, const I* __restrict__ idx,
-                          const float* __restrict__ A, const float* __restrict__ W,
-                          const float* __restrict__ H, int64_t m, int64_t n, int32_t k,
-                          int64_t nnz, float* __restrict__ val) {
-    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
-         q += (int64_t)gridDim.x * kT) {
+                          const int32_t* __restrict__ pos, const float* __restrict__ A,
+                          const float* __restrict__ W, const float* __restrict__ H, int64_t m,
+                          int64_t n, int32_t k, int64_t nnz, float* __restrict__ val) {
+    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
+         e += (int64_t)gridDim.x * kT) {
+        const int64_t q = pos[e];
         int64_t lo = 0, hi = nseg;  // last s with seg_start[s] <= q
         while (hi - lo > 1) {
             const int64_t mid = (lo + hi) >> 1;
@@ -142,21 +156,34 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
-        val[q] = (float)((double)A[q] - pred);
+        val[q] = (float)((double)A[e] - pred);
     }
 }
 
-__global__ void k_scatter_f32(const float* __restrict__ src, const int32_t* __restrict__ map,
-                              int64_t n, float* __restrict__ dst) {
-    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
-        dst[map[q]] = src[q];
+__global__ void k_copy_mapped(const float* __restrict__ src, const int32_t* __restrict__ smap,
+                              float* __restrict__ dst, const int32_t* __restrict__ dmap,
+                              int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
+        dst[dmap ? dmap[i] : i] = src[smap ? smap[i] : i];
 }
 
-__global__ void k_consistency(const float* __restrict__ a, const float* __restrict__ b,
-                              const int32_t* __restrict__ map, int64_t n,
-                              unsigned long long* count) {
-    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
-        if (__float_as_uint(a[q]) != __float_as_uint(b[map[q]])) atomicAdd(count, 1ull);
+__global__ void k_consistency(const float* __restrict__ a, const int32_t* __restrict__ amap,
+                              const float* __restrict__ b, const int32_t* __restrict__ bmap,
+                              int64_t n, unsigned long long* count) {
+    for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
+        if (__float_as_uint(a[amap[i]]) != __float_as_uint(b[bmap[i]])) atomicAdd(count, 1ull);
+}
+
+__global__ void k_seg_spread(const float* __restrict__ F, int64_t rows,
+                             const int32_t* __restrict__ seg_row, int64_t S, int32_t k,
+                             float* __restrict__ out) {
+    const int64_t total = S * k;
+    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * kT) {
+        const int64_t t = e / S;
+        const int64_t sg = e - t * S;
+        out[e] = F[t * rows + seg_row[sg]];
+    }
 }
 
 // Workgroup b sums elements b*256 + t + s*(nparts*256) in order per thread, then a
@@ -239,16 +266,29 @@ hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hi
 }
 
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, bool idx16, void* idx, float* val,
-                              hipStream_t s) {
+                              int64_t nnz, int cbits, const int32_t* seg_off, bool idx16,
+                              void* idx, float* val, int32_t* pos, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
     const uint64_t mask = cbits >= 64 ? ~0ull : ((1ull << cbits) - 1);
     if (idx16)
         hipLaunchKernelGGL(k_layout_fill<uint16_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, mask, static_cast<uint16_t*>(idx), val);
+                           val_in, nnz, cbits, mask, seg_off, static_cast<uint16_t*>(idx), val,
+                           pos);
     else
         hipLaunchKernelGGL(k_layout_fill<int32_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, mask, static_cast<int32_t*>(idx), val);
+                           val_in, nnz, cbits, mask, seg_off, static_cast<int32_t*>(idx), val,
+                           pos);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    if (idx16)
+        hipLaunchKernelGGL(k_fill_idx<uint16_t>, grid_for(n), dim3(kT), 0, s,
+                           static_cast<uint16_t*>(idx), (uint16_t)value, n);
+    else
+        hipLaunchKernelGGL(k_fill_idx<int32_t>, grid_for(n), dim3(kT), 0, s,
+                           static_cast<int32_t*>(idx), value, n);
     return hipGetLastError();
 }
 
@@ -285,32 +325,42 @@ hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2ne
     return hipGetLastError();
 }
 
-hipError_t launch_rebuild_residual(const Layout& L, const float* A, const float* W,
-                                   const float* H, int64_t m, int64_t n, int32_t k,
-                                   hipStream_t s) {
+hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const float* A,
+                                   const float* W, const float* H, int64_t m, int64_t n,
+                                   int32_t k, hipStream_t s) {
     if (L.nnz == 0) return hipSuccess;
     if (L.idx16)
         hipLaunchKernelGGL(k_rebuild<uint16_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
-                           static_cast<const uint16_t*>(L.idx), A, W, H, m, n, k, L.nnz, L.val);
+                           static_cast<const uint16_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
+                           L.val);
     else
         hipLaunchKernelGGL(k_rebuild<int32_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
-                           static_cast<const int32_t*>(L.idx), A, W, H, m, n, k, L.nnz, L.val);
+                           static_cast<const int32_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
+                           L.val);
     return hipGetLastError();
 }
 
-hipError_t launch_scatter_f32(const float* src, const int32_t* map, int64_t n, float* dst,
+hipError_t launch_copy_mapped(const float* src, const int32_t* smap, float* dst,
+                              const int32_t* dmap, int64_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_copy_mapped, grid_for(n), dim3(kT), 0, s, src, smap, dst, dmap, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_consistency(const float* a, const int32_t* amap, const float* b,
+                              const int32_t* bmap, int64_t n, unsigned long long* count,
                               hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_scatter_f32, grid_for(n), dim3(kT), 0, s, src, map, n, dst);
+    hipLaunchKernelGGL(k_consistency, grid_for(n), dim3(kT), 0, s, a, amap, b, bmap, n, count);
     return hipGetLastError();
 }
 
-hipError_t launch_consistency(const float* a, const float* b, const int32_t* map, int64_t n,
-                              unsigned long long* count, hipStream_t s) {
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_consistency, grid_for(n), dim3(kT), 0, s, a, b, map, n, count);
+hipError_t launch_seg_spread(const float* F, int64_t rows, const int32_t* seg_row, int64_t S,
+                             int32_t k, float* out, hipStream_t s) {
+    if (S == 0 || k == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_seg_spread, grid_for(S * k), dim3(kT), 0, s, F, rows, seg_row, S, k, out);
     return hipGetLastError();
 }
 

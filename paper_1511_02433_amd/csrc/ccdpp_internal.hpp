@@ -20,41 +20,46 @@ namespace ccdk {
 // coordinate the pass gathers.
 //
 // The gathered dimension is cut into P tiles of T columns.  Entries are
-// stored tile-major; inside a tile, the non-empty row segments come in order
-// of decreasing length and each segment's entries in increasing column order.
-// A pass stages the tile's slice of every gathered vector in LDS (160 KB per
-// CU on gfx950), so each random gather is an LDS read instead of a cache line
-// pulled from L2.  With P == 1 a segment is a whole row and the pass writes
-// the coordinate directly; with P > 1 every segment yields a partial
+// stored tile-major; inside a tile, row segments (a row's entries in the tile)
+// follow each other and each segment's entries come in increasing column
+// order.  A pass stages the tile's slice of every gathered vector in LDS
+// (160 KB per CU on gfx950), so each random gather is an LDS read instead of
+// a cache line pulled from L2.  With P == 1 segment s is row s (rows are
+// relabelled by decreasing length, so the empty ones come last) and the pass
+// writes the coordinate directly; with P > 1 every segment yields a partial
 // (numerator, denominator) and a combine kernel adds a row's partials in tile
 // order.  A layout whose tiles would hold too few entries per segment keeps
 // P == 1 and gathers from global memory instead ("global" mode).
 //
-// Work units are wave-sized: a long segment (more than kGroupMaxLen entries)
-// is one unit walked by a whole wave; shorter segments are packed 64/G to a
-// unit, G lanes per segment, E entries per lane.  Persistent workgroups of
-// kWG threads are assigned to tiles in proportion to the tile's entries and
-// their waves take the tile's units in a fixed stride, so the schedule and
-// every reduction order are deterministic.
-// ---------------------------------------------------------------------------
+// Persistent workgroups of kWG threads each own an equal, contiguous share of
+// the layout's (tile-major) entries, cut on segment boundaries.  A share that
+// crosses tile boundaries is processed as one "piece" per tile, restaging LDS
+// between pieces; inside a piece each of the 16 waves owns one contiguous
+// chunk, again cut on segment boundaries.  Shares, pieces and chunks, and with
+// them every reduction order, are fixed at build time, so results are
+// identical run to run.
+//
+// Every chunk starts at a multiple of kE entries: the build inserts up to
+// kE - 1 padding entries at the end of the segment before each chunk start.  A
+// padding entry holds value 0 and the tile-local index T, which addresses a
+// zero kept after each staged vector slice in LDS (or lies past the vector in
+// global mode, where the bounded buffer load returns 0), so it adds exactly 0
+// to every sum and stays 0 under every residual update.
+//
+// The per-row scalars a pass reads (the own factor column of the current and
+// the previous feature) are addressed by segment: with P == 1 segment s is row
+// s and the factor column itself serves; with P > 1 the library keeps a copy of
+// every own factor column spread over the segments (written by the combine
+// kernel when the column is committed), so no pass reads through seg_row.
 constexpr int kWG = 1024;                 // threads per persistent workgroup
 constexpr int kWaves = kWG / 64;          // 16 waves
-constexpr int kLongE = 16;                // entries per lane per step of a long segment
-constexpr int kGroupMaxLen = 1024;        // longest segment packed into a lane group
+constexpr int kE = 8;                     // entries per lane per window
+constexpr int kWin = 64 * kE;             // entries per window
+constexpr int kScratch = 160;             // LDS words of per-wave scratch
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
+constexpr int kLdsVecBytes = kLdsBytes - kWaves * kScratch * 4;  // for staged vectors
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
-
-enum UnitKind : int32_t {
-    kULong = 0,     // one segment, the whole wave, steps of 64 * kLongE entries
-    kUG64E16 = 1,   // lanes-per-segment G and entries-per-lane E
-    kUG64E8 = 2,
-    kUG32E8 = 3,
-    kUG16E8 = 4,
-    kUG8E8 = 5,
-    kUG4E8 = 6,
-    kUG2E8 = 7,
-    kUG1E8 = 8,
-};
+constexpr int kEntryPad = 64;             // entries of padding after idx and val (loads past the end)
 
 enum PassMode : int32_t {
     kModePlain = 0,     // R-hat read only: y = sum rhat x / (lambda + sum x^2)
@@ -70,26 +75,26 @@ enum GatherMode : int32_t {
 };
 
 struct PassArgs {
-    const void* idx;            // [nnz] uint16 or int32 tile-local column
-    float* val;                 // [nnz] residual / R-hat
+    const void* idx;            // [npad] uint16 or int32 tile-local column
+    float* val;                 // [npad] residual / R-hat
     const int64_t* seg_start;   // [S + 1]
-    const int32_t* seg_row;     // [S]
-    const int2* units;          // [U] {first segment, kind | count << 8}
-    const int32_t* wg_tile;     // [grid] tile of each workgroup
-    const int32_t* wg_rank;     // [grid] rank of the workgroup inside its tile
-    const int32_t* tile_unit;   // [P + 1] unit range of each tile
-    const int32_t* tile_nwg;    // [P] workgroups of each tile
+    const int32_t* wg_piece;    // [grid + 1] pieces of each workgroup
+    const int32_t* piece_tile;  // [npieces] tile of each piece
+    const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
+    const int32_t* piece_seg;   // [npieces * kWaves] segment starting each chunk
     const float* x;             // [cols] gathered vector of the update
-    const float* p;             // [rows] own factor column, current feature
-    const float* pp;            // [rows] own factor column, previous feature (committed)
+    const float* p;             // [S] own factor column, current feature, per segment
+    const float* pp;            // [S] own factor column, previous feature (committed), per segment
     const float* q;             // [cols] other factor column, current feature
     const float* qq;            // [cols] other factor column, previous feature (committed)
     float* y;                   // [rows] coordinates (P == 1)
     double2* part;              // [S] partial (num, den) per segment (P > 1)
     double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
-    int64_t nnz;
     int32_t rows, cols, T, P;
-    int32_t nseg;
+    int32_t Ts;                 // LDS floats per staged vector slice (T + 1: a trailing zero)
+    int32_t nseg;               // S
+    int32_t nseg_ne;            // segments with entries (P == 1: rows before the empty ones)
+    int32_t vec_floats;         // LDS floats taken by staged vectors (scratch follows)
     int32_t x_is_q;             // x and q are the same vector (staged once)
     double lambda;
 };
@@ -99,6 +104,7 @@ struct CombineArgs {
     const int32_t* row_segs;     // [S] segments of each row in tile order
     const double2* part;
     float* y;
+    float* yseg;                 // optional [S]: y spread over the row's segments
     int32_t rows;
     double lambda;
 };
@@ -106,26 +112,26 @@ struct CombineArgs {
 // One compressed copy of the residual plus its schedule.
 struct Layout {
     int64_t rows = 0, cols = 0, nnz = 0;
+    int64_t npad = 0;                // entries including alignment padding
     int32_t gather = kGatherGlobal;
     int32_t T = 0, P = 1;
     bool idx16 = false;
-    void* idx = nullptr;
-    float* val = nullptr;
-    int64_t* seg_start = nullptr;
+    void* idx = nullptr;             // [npad + kEntryPad]
+    float* val = nullptr;            // [npad + kEntryPad]
+    int64_t* seg_start = nullptr;    // [S + 1], in padded positions
     int32_t* seg_row = nullptr;
     int32_t* tile_seg = nullptr;     // [P + 1] first segment of each tile
-    int2* units = nullptr;
-    int32_t* wg_tile = nullptr;
-    int32_t* wg_rank = nullptr;
-    int32_t* tile_unit = nullptr;
-    int32_t* tile_nwg = nullptr;
+    int32_t* wg_piece = nullptr;
+    int32_t* piece_tile = nullptr;
+    int64_t* piece_chunk = nullptr;
+    int32_t* piece_seg = nullptr;
+    int32_t npieces = 0;
     int32_t* row_seg_ptr = nullptr;  // P > 1
     int32_t* row_segs = nullptr;     // P > 1
     double2* part = nullptr;         // P > 1
     int64_t nseg = 0;
-    int32_t nunits = 0;
+    int64_t nseg_ne = 0;
     int32_t grid = 0;                // persistent workgroups per pass
-    int32_t nlong = 0;               // units of the long kind
 };
 
 // Launchers (sweep.hip).
@@ -133,7 +139,7 @@ hipError_t sweep_init();  // raise the dynamic-LDS limit of the staged kernels
 hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const float* p,
                        const float* pp, const float* q, const float* qq, float* y, double lambda,
                        double* sse_part, hipStream_t s);
-hipError_t launch_combine(const Layout& L, float* y, double lambda, hipStream_t s);
+hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda, hipStream_t s);
 hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s);
 hipError_t launch_reduce_sum(const double* part, int32_t n, double* out, hipStream_t s);
 int staged_vectors(PassMode mode, bool x_is_q);
@@ -149,8 +155,9 @@ hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32
                            int32_t* ids, hipStream_t s);
 hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hipStream_t s);
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, bool idx16, void* idx, float* val,
-                              hipStream_t s);
+                              int64_t nnz, int cbits, const int32_t* seg_off, bool idx16,
+                              void* idx, float* val, int32_t* pos, hipStream_t s);
+hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t* out,
                           hipStream_t s);
@@ -159,13 +166,18 @@ hipError_t launch_scatter_factor_in(const float* rowmajor, const int32_t* new2ol
                                     int32_t k, float* colmajor, hipStream_t s);
 hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2new, int64_t rows,
                                     int32_t k, float* rowmajor, hipStream_t s);
-hipError_t launch_rebuild_residual(const Layout& L, const float* A, const float* W,
-                                   const float* H, int64_t m, int64_t n, int32_t k,
-                                   hipStream_t s);
-hipError_t launch_scatter_f32(const float* src, const int32_t* map, int64_t n, float* dst,
+hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const float* A,
+                                   const float* W, const float* H, int64_t m, int64_t n,
+                                   int32_t k, hipStream_t s);
+// dst[dmap ? dmap[i] : i] = src[smap ? smap[i] : i] for i < n
+hipError_t launch_copy_mapped(const float* src, const int32_t* smap, float* dst,
+                              const int32_t* dmap, int64_t n, hipStream_t s);
+hipError_t launch_consistency(const float* a, const int32_t* amap, const float* b,
+                              const int32_t* bmap, int64_t n, unsigned long long* count,
                               hipStream_t s);
-hipError_t launch_consistency(const float* a, const float* b, const int32_t* map, int64_t n,
-                              unsigned long long* count, hipStream_t s);
+// out[t * S + s] = F[t * rows + seg_row[s]] for t < k
+hipError_t launch_seg_spread(const float* F, int64_t rows, const int32_t* seg_row, int64_t S,
+                             int32_t k, float* out, hipStream_t s);
 hipError_t launch_sq_sum(const float* v, int64_t n, double* part, int32_t nparts,
                          hipStream_t s);
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,

@@ -11,19 +11,19 @@
 // evaluated as fma(p, q, fma(-pp, qq, val)).  Both copies evaluate that same
 // expression on the same operands, so they stay bitwise identical.
 //
-// Memory: index and value arrays are streamed with non-temporal buffer loads
-// (each entry is touched once per pass).  The vectors a pass gathers from are
+// Memory: index and value arrays are streamed with non-temporal 128-bit loads
+// (each entry is touched once per pass), the next window's loads in flight
+// while the current window is reduced.  The vectors a pass gathers from are
 // staged tile by tile in LDS by persistent workgroups (see ccdpp_internal.hpp),
 // so a random gather costs an LDS read; layouts too sparse for tiling gather
-// through L2 instead.  Buffer descriptors are rebased to each wave's own entry
-// range with an exact byte limit, and masked lanes use an out-of-range offset,
-// which the hardware turns into a zero load or a dropped store.
+// through L2 with bounded buffer loads instead.
 //
-// Arithmetic: R-hat in fp32 FMA; sums of R-hat*x and x^2 in fp64 with a fixed
-// reduction tree, so results are identical run to run; the coordinate
-// num / (lambda + den) is an IEEE fp64 division rounded once to fp32.  A
-// coordinate whose denominator is exactly zero (lambda = 0 and an empty row)
-// is set to zero.
+// Arithmetic: R-hat in fp32 FMA.  Inside a window (at most 512 entries) the
+// sums of R-hat*x and x^2 are fp32 segmented scans; a segment's window sums are
+// added in fp64, across windows too, in a fixed order, so results are
+// identical run to run.  The coordinate num / (lambda + den) is an IEEE fp64
+// division rounded once to fp32; a coordinate whose denominator is exactly zero
+// (lambda = 0 and an empty row) is set to zero.
 #include "ccdpp_internal.hpp"
 
 namespace ccdk {
@@ -31,33 +31,74 @@ namespace {
 
 using rsrc_t = __amdgpu_buffer_rsrc_t;
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, gfx9 family
-constexpr uint32_t kOOB = 0xFFFFFFFFu;  // offset past any limit: load 0 / drop store
-constexpr int kNT = 2;                  // non-temporal cache policy (streamed once)
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
     uint32_t lim = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)lim,
                                             kRsrcWord3);
 }
-template <int AUX>
+// Bounded load: offsets past the descriptor's limit read 0.
 __device__ __forceinline__ float ld_f32(rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, AUX));
-}
-template <bool IDX16>
-__device__ __forceinline__ uint32_t ld_idx(rsrc_t r, uint32_t off) {
-    if constexpr (IDX16)
-        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kNT);
-    else
-        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNT);
-}
-template <int AUX>
-__device__ __forceinline__ void st_f32(float v, rsrc_t r, uint32_t off) {
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int32_t, v), r, off, 0, AUX);
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
-// ---- cross-lane sums -------------------------------------------------------
+// ---- cross-lane operations ---------------------------------------------------
+// DPP controls of the gfx9 family.
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kBcast15 = 0x142;   // lane 15 of each row to the next row
+constexpr int kBcast31 = 0x143;   // lane 31 to rows 2 and 3
+constexpr int kWaveShr1 = 0x138;  // lane l reads lane l - 1
+constexpr int kWaveShl1 = 0x130;  // lane l reads lane l + 1
+
+// Lanes whose source is out of range, or whose row is masked off, get `old`
+// (with BC, out-of-range sources read 0 instead).
+template <int CTRL, int ROWS = 0xF, bool BC = false>
+__device__ __forceinline__ int dpp_i(int old, int v) {
+    return __builtin_amdgcn_update_dpp(old, v, CTRL, ROWS, 0xF, BC);
+}
+template <int CTRL, int ROWS = 0xF, bool BC = false>
+__device__ __forceinline__ float dpp_f(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                                 __builtin_bit_cast(int, v), CTRL,
+                                                                 ROWS, 0xF, BC));
+}
+
+// Inclusive prefix sum over the 64 lanes.
+__device__ __forceinline__ int scan_i(int v) {
+    v += dpp_i<kRowShr1, 0xF, true>(0, v);
+    v += dpp_i<kRowShr2, 0xF, true>(0, v);
+    v += dpp_i<kRowShr4, 0xF, true>(0, v);
+    v += dpp_i<kRowShr8, 0xF, true>(0, v);
+    v += dpp_i<kBcast15, 0xA>(0, v);
+    v += dpp_i<kBcast31, 0xC>(0, v);
+    return v;
+}
+
+// One step of an inclusive segmented scan keyed by segment: add the values of
+// the lane CTRL reads when it holds the same key.  Keys are segment id + 1 on
+// lanes that carry data and 0 elsewhere; they never decrease over the lanes
+// that carry data, so equal keys are contiguous and the steps below compose to
+// the full segmented scan.  A source out of range or masked off contributes 0.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ void seg_step(int key, float& n, float& d) {
+    const int pk = dpp_i<CTRL, ROWS, true>(0, key);
+    const float f = pk == key ? 1.0f : 0.0f;
+    n = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, n), f, n);
+    d = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, d), f, d);
+}
+__device__ __forceinline__ void seg_scan(int key, float& n, float& d) {
+    seg_step<kRowShr1>(key, n, d);
+    seg_step<kRowShr2>(key, n, d);
+    seg_step<kRowShr4>(key, n, d);
+    seg_step<kRowShr8>(key, n, d);
+    seg_step<kBcast15, 0xA>(key, n, d);
+    seg_step<kBcast31, 0xC>(key, n, d);
+}
+
 template <int CTRL>
-__device__ __forceinline__ double dpp_d(double x) {
+__device__ __forceinline__ double dppq_d(double x) {
     int2 v = __builtin_bit_cast(int2, x);
     v.x = __builtin_amdgcn_update_dpp(0, v.x, CTRL, 0xF, 0xF, false);
     v.y = __builtin_amdgcn_update_dpp(0, v.y, CTRL, 0xF, 0xF, false);
@@ -85,16 +126,29 @@ __device__ __forceinline__ double xor32_sum(double x) {
     hi.x = (int)a[1]; hi.y = (int)b[1];
     return __builtin_bit_cast(double, lo) + __builtin_bit_cast(double, hi);
 }
-// Sum over aligned groups of G lanes; every lane of a group gets the same bits.
-template <int G>
-__device__ __forceinline__ double group_sum(double x) {
-    if constexpr (G >= 2) x += dpp_d<0xB1>(x);    // quad_perm [1,0,3,2]: lane ^ 1
-    if constexpr (G >= 4) x += dpp_d<0x4E>(x);    // quad_perm [2,3,0,1]: lane ^ 2
-    if constexpr (G >= 8) x += dpp_d<0x141>(x);   // row_half_mirror: the other quad of 8
-    if constexpr (G >= 16) x += dpp_d<0x140>(x);  // row_mirror: the other half of 16
-    if constexpr (G >= 32) x = xor16_sum(x);
-    if constexpr (G >= 64) x = xor32_sum(x);
-    return x;
+// Sum over the 64 lanes; every lane gets the same bits.
+__device__ __forceinline__ double wave_sum(double x) {
+    x += dppq_d<0xB1>(x);   // quad_perm [1,0,3,2]: lane ^ 1
+    x += dppq_d<0x4E>(x);   // quad_perm [2,3,0,1]: lane ^ 2
+    x += dppq_d<0x141>(x);  // row_half_mirror: the other quad of 8
+    x += dppq_d<0x140>(x);  // row_mirror: the other half of 16
+    x = xor16_sum(x);
+    return xor32_sum(x);
+}
+
+__device__ __forceinline__ int64_t lane_i64(int64_t v, int src) {
+    const int2 p = __builtin_bit_cast(int2, v);
+    int2 r;
+    r.x = __builtin_amdgcn_readlane(p.x, src);
+    r.y = __builtin_amdgcn_readlane(p.y, src);
+    return __builtin_bit_cast(int64_t, r);
+}
+__device__ __forceinline__ double lane_f64(double v, int src) {
+    const int2 p = __builtin_bit_cast(int2, v);
+    int2 r;
+    r.x = __builtin_amdgcn_readlane(p.x, src);
+    r.y = __builtin_amdgcn_readlane(p.y, src);
+    return __builtin_bit_cast(double, r);
 }
 
 __device__ __forceinline__ float coordinate(double num, double den, double lambda) {
@@ -108,6 +162,7 @@ template <int MODE> struct Needs {
     static constexpr bool qq = MODE == kModeSubAdd || MODE == kModeFlush;
     static constexpr bool p = MODE == kModeAdd || MODE == kModeSubAdd;
     static constexpr bool pp = MODE == kModeSubAdd || MODE == kModeFlush;
+    static constexpr bool store = MODE != kModePlain;
 };
 
 // Where a pass reads its gathered vectors: LDS slices of the tile, or global.
@@ -123,195 +178,353 @@ __device__ __forceinline__ float gat(const float* lds, rsrc_t g, uint32_t c) {
     if constexpr (STAGED)
         return lds[c];
     else
-        return ld_f32<0>(g, c * 4u);
+        return ld_f32(g, c * 4u);
 }
 
-// One entry: apply the residual bookkeeping of the mode, store it, accumulate.
+// Residual bookkeeping of a mode applied to one stored value.
 template <int MODE>
-__device__ __forceinline__ void entry(bool ok, float rv, float xv, float qv, float qqv, float pr,
-                                      float ppr, rsrc_t rval, uint32_t voff, double& num,
-                                      double& den) {
-    float r = rv;
-    if constexpr (MODE == kModeAdd) r = __builtin_fmaf(pr, qv, rv);
-    if constexpr (MODE == kModeSubAdd) r = __builtin_fmaf(pr, qv, __builtin_fmaf(-ppr, qqv, rv));
-    if constexpr (MODE == kModeFlush) r = __builtin_fmaf(-ppr, qqv, rv);
-    if constexpr (MODE != kModePlain) st_f32<kNT>(r, rval, voff);  // masked lanes: kOOB, dropped
-    if constexpr (MODE == kModeFlush) {
-        double d = ok ? (double)r : 0.0;
-        num = __builtin_fma(d, d, num);
-    } else {
-        double dx = ok ? (double)xv : 0.0;
-        num = __builtin_fma((double)r, dx, num);
-        den = __builtin_fma(dx, dx, den);
-    }
+__device__ __forceinline__ float rhat(float v, float qv, float qqv, float pr, float ppr) {
+    if constexpr (MODE == kModeAdd) return __builtin_fmaf(pr, qv, v);
+    if constexpr (MODE == kModeSubAdd) return __builtin_fmaf(pr, qv, __builtin_fmaf(-ppr, qqv, v));
+    if constexpr (MODE == kModeFlush) return __builtin_fmaf(-ppr, qqv, v);
+    return v;
 }
 
-// E entries per lane at positions first + e * STRIDE (relative to the wave's
-// rebased descriptors, valid below `end`); every load is issued before any use.
-template <int MODE, bool STAGED, bool IDX16, int E, int STRIDE>
-__device__ __forceinline__ void run_entries(rsrc_t ridx, rsrc_t rval, const Gather& gx,
-                                            uint32_t first, uint32_t end, float pr, float ppr,
-                                            double& num, double& den) {
-    using N = Needs<MODE>;
-    constexpr uint32_t kIB = IDX16 ? 2u : 4u;
-    bool ok[E];
-    uint32_t voff[E];
-    uint32_t c[E];
-    float rv[E], xv[E], qv[E], qqv[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const uint32_t pos = first + (uint32_t)(e * STRIDE);
-        ok[e] = pos < end;
-        voff[e] = ok[e] ? pos * 4u : kOOB;
-        c[e] = ld_idx<IDX16>(ridx, ok[e] ? pos * kIB : kOOB);
-    }
-#pragma unroll
-    for (int e = 0; e < E; ++e) rv[e] = ld_f32<kNT>(rval, voff[e]);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        xv[e] = N::x ? gat<STAGED>(gx.lx, gx.gx, c[e]) : 0.0f;
-        qv[e] = N::q ? gat<STAGED>(gx.lq, gx.gq, c[e]) : 0.0f;
-        qqv[e] = N::qq ? gat<STAGED>(gx.lqq, gx.gqq, c[e]) : 0.0f;
-    }
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-        entry<MODE>(ok[e], rv[e], xv[e], qv[e], qqv[e], pr, ppr, rval, voff[e], num, den);
-}
-
-template <int MODE>
-__device__ __forceinline__ void emit(const PassArgs& a, int s, int row, double num, double den) {
-    if (a.P == 1)
-        a.y[row] = coordinate(num, den, a.lambda);
+template <bool P1>
+__device__ __forceinline__ void emit(const PassArgs& a, int s, double num, double den) {
+    if constexpr (P1)
+        a.y[s] = coordinate(num, den, a.lambda);  // P == 1: segment s is row s
     else
         a.part[s] = make_double2(num, den);
 }
 
-// A unit of up to 64/G short segments, G lanes each, E entries per lane.
-template <int MODE, bool STAGED, bool IDX16, int G, int E>
-__device__ __forceinline__ void unit_groups(const PassArgs& a, const Gather& gx, int s0, int cnt,
-                                            int lane, double& sse) {
+// Copy the tile's slice of every gathered vector into LDS, each followed by a
+// zero (the target of padding entries).  Slots come in the order x, q, qq; x
+// shares q's slot when they are the same vector.
+template <int MODE>
+__device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* lds, Gather& gx) {
     using N = Needs<MODE>;
-    constexpr uint32_t kIB = IDX16 ? 2u : 4u;
-    const int g = lane / G;
-    const int l = lane % G;
-    const bool valid = g < cnt;
-    const int s = s0 + (valid ? g : cnt - 1);
-    const int64_t wlo = a.seg_start[s0];
-    const int64_t whi = a.seg_start[s0 + cnt];
-    const uint64_t wlen = (uint64_t)(whi - wlo);
-    const rsrc_t ridx = make_rsrc(static_cast<const char*>(a.idx) + wlo * kIB, wlen * kIB);
-    const rsrc_t rval = make_rsrc(a.val + wlo, wlen * 4u);
-    const int64_t lo = a.seg_start[s];
-    const int64_t hi = a.seg_start[s + 1];
-    const uint32_t first = valid ? (uint32_t)(lo - wlo) + (uint32_t)l : 0u;
-    const uint32_t end = valid ? (uint32_t)(hi - wlo) : 0u;
-    const int row = a.seg_row[s];
-    float pr = 0.0f, ppr = 0.0f;
-    if constexpr (N::p) pr = a.p[row];
-    if constexpr (N::pp) ppr = a.pp[row];
-    double num = 0.0, den = 0.0;
-    run_entries<MODE, STAGED, IDX16, E, G>(ridx, rval, gx, first, end, pr, ppr, num, den);
-    if constexpr (MODE == kModeFlush) {
-        sse += num;
-    } else {
-        num = group_sum<G>(num);
-        den = group_sum<G>(den);
-        if (valid && l == 0) emit<MODE>(a, s, row, num, den);
+    const int T = a.T, Ts = a.Ts;
+    const int c0 = tile * T;
+    const int len = min(T, a.cols - c0);
+    const bool alias = N::x && N::q && a.x_is_q;
+    int slot = 0;
+    float* sx = nullptr;
+    float* sq = nullptr;
+    float* sqq = nullptr;
+    if (N::x && !alias) sx = lds + (slot++) * Ts;
+    if (N::q) sq = lds + (slot++) * Ts;
+    if (alias) sx = sq;
+    if (N::qq) sqq = lds + (slot++) * Ts;
+    // Four strided elements per thread per step, loads first, so that a step costs
+    // one memory latency rather than four.
+    constexpr int kU = 4;
+    for (int i0 = (int)threadIdx.x; i0 < len; i0 += kU * kWG) {
+        float vx[kU], vq[kU], vqq[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int i = min(i0 + u * kWG, len - 1);
+            if (N::x && !alias) vx[u] = a.x[c0 + i];
+            if (N::q) vq[u] = a.q[c0 + i];
+            if (N::qq) vqq[u] = a.qq[c0 + i];
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int i = i0 + u * kWG;
+            if (i < len) {
+                if (N::x && !alias) sx[i] = vx[u];
+                if (N::q) sq[i] = vq[u];
+                if (N::qq) sqq[i] = vqq[u];
+            }
+        }
     }
+    if (threadIdx.x == 0) {
+        if (N::x && !alias) sx[T] = 0.0f;
+        if (N::q) sq[T] = 0.0f;
+        if (N::qq) sqq[T] = 0.0f;
+    }
+    gx.lx = sx;
+    gx.lq = sq;
+    gx.lqq = sqq;
 }
 
-// One long segment walked by the whole wave.
-template <int MODE, bool STAGED, bool IDX16>
-__device__ __forceinline__ void unit_long(const PassArgs& a, const Gather& gx, int s, int lane,
-                                          double& sse) {
+// What a window needs from memory before its arithmetic: the lane's kE values
+// and indices, the start of segment scur + 1 + lane and the row scalars of
+// segment scur + lane.
+struct Win {
+    f32x4 v0, v1;
+    u32x4 c0, c1;  // IDX16: c0 holds the 8 indices packed in pairs
+    int64_t st;
+    float pr, ppr;
+};
+
+// Loads of the window at b (a multiple of kE).  Lanes at or past `lim` all read
+// entry b instead, so every address stays inside the arrays (whose padding
+// covers the last window) and a window past the chunk costs one cache line.
+template <int MODE, bool IDX16>
+__device__ __forceinline__ void load_window(const PassArgs& a, int64_t b, int64_t lim, uint32_t le,
+                                            int scur, int lane, Win& w) {
     using N = Needs<MODE>;
-    constexpr uint32_t kIB = IDX16 ? 2u : 4u;
-    constexpr int E = (MODE == kModeAdd || MODE == kModeSubAdd) ? kLongE / 2 : kLongE;
-    const int64_t lo = a.seg_start[s];
-    const int64_t hi = a.seg_start[s + 1];
-    const uint32_t len = (uint32_t)(hi - lo);
-    const rsrc_t ridx = make_rsrc(static_cast<const char*>(a.idx) + lo * kIB, (uint64_t)len * kIB);
-    const rsrc_t rval = make_rsrc(a.val + lo, (uint64_t)len * 4u);
-    const int row = a.seg_row[s];
-    float pr = 0.0f, ppr = 0.0f;
-    if constexpr (N::p) pr = a.p[row];
-    if constexpr (N::pp) ppr = a.pp[row];
-    double num = 0.0, den = 0.0;
-    for (uint32_t base = 0; base < len; base += 64u * E)
-        run_entries<MODE, STAGED, IDX16, E, 64>(ridx, rval, gx, base + (uint32_t)lane, len, pr, ppr,
-                                                num, den);
-    if constexpr (MODE == kModeFlush) {
-        sse += num;
+    const int64_t eb = b + (b + (int64_t)le < lim ? (int64_t)le : 0);
+    const f32x4* vp = reinterpret_cast<const f32x4*>(a.val + eb);
+    w.v0 = __builtin_nontemporal_load(vp);
+    w.v1 = __builtin_nontemporal_load(vp + 1);
+    if constexpr (IDX16) {
+        w.c0 = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + eb));
     } else {
-        num = group_sum<64>(num);
-        den = group_sum<64>(den);
-        if (lane == 0) emit<MODE>(a, s, row, num, den);
+        const u32x4* ip = reinterpret_cast<const u32x4*>(static_cast<const int32_t*>(a.idx) + eb);
+        w.c0 = __builtin_nontemporal_load(ip);
+        w.c1 = __builtin_nontemporal_load(ip + 1);
     }
+    w.st = a.seg_start[min(scur + 1 + lane, a.nseg)];
+    const int sj = min(scur + lane, a.nseg - 1);
+    if constexpr (N::p) w.pr = a.p[sj];
+    if constexpr (N::pp) w.ppr = a.pp[sj];
 }
 
-template <int MODE, bool STAGED, bool IDX16>
+template <bool IDX16>
+__device__ __forceinline__ uint32_t col_of(const Win& w, int k) {
+    if constexpr (IDX16) {
+        const uint32_t d = w.c0[k >> 1];
+        return (k & 1) ? (d >> 16) : (d & 0xFFFFu);
+    } else {
+        return k < 4 ? w.c0[k] : w.c1[k - 4];
+    }
+}
+__device__ __forceinline__ float val_of(const Win& w, int k) { return k < 4 ? w.v0[k] : w.v1[k - 4]; }
+
+// State a wave carries from window to window of its chunk.
+struct Walk {
+    int64_t elo;  // first entry of the next window (a multiple of kE)
+    int64_t c1;   // end of the chunk (a multiple of kE)
+    int scur;     // segment holding entry elo
+    int cid;      // segment left open by the previous window (-1: none), and its sums
+    double cn, cd;
+    double sse;
+};
+
+// One window [elo, we) of a wave's chunk.  Lane l holds entries elo + l*kE ..
+// elo + l*kE + kE - 1; every window starts and ends on a multiple of kE, so a
+// lane's entries are either all inside the window or all outside.  The window
+// ends at the chunk end, after 64 lanes, or at the last multiple of kE not past
+// the start of segment scur + 64, so it meets at most 64 segments and their row
+// scalars fit one LDS slot per lane.  The segment of each entry comes from a
+// bitmap of the segment starts inside the window (built in the wave's LDS
+// scratch from one coalesced read of the segment table) and a prefix count over
+// lanes.  The loads of the next window are issued before the arithmetic.
+template <int MODE, bool STAGED, bool IDX16, bool P1>
+__device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk& wk,
+                                       const Win& cur, Win& nxt, int lane, uint32_t le, float* spr,
+                                       float* sppr, uint32_t* bm) {
+    using N = Needs<MODE>;
+    const int64_t b = wk.elo;
+    const int64_t st = cur.st;
+    int64_t we = min(b + (int64_t)kWin, wk.c1);
+    const int64_t st63 = lane_i64(st, 63);
+    if (st63 < we) we = st63 & ~(int64_t)(kE - 1);
+    const int adv = __builtin_popcountll(__ballot(st <= we));
+    // Row scalars of the window's segments, one LDS slot per lane.
+    if constexpr (N::p) spr[lane] = cur.pr;
+    if constexpr (N::pp) sppr[lane] = cur.ppr;
+    // Bitmap of the segment starts inside (b, we); this lane's kE bits.
+    if (lane < kWin / 32) bm[lane] = 0u;
+    __builtin_amdgcn_wave_barrier();
+    if (st < we) {
+        const uint32_t off = (uint32_t)(st - b);
+        atomicOr(&bm[off >> 5], 1u << (off & 31u));
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t bits = (bm[le >> 5] >> (le & 31u)) & ((1u << kE) - 1u);
+
+    // Next window's loads (a harmless reload of b when this window is the last).
+    const int scur_n = wk.scur + adv;
+    {
+        const bool more = we < wk.c1;
+        load_window<MODE, IDX16>(a, more ? we : b, more ? wk.c1 : b, le, scur_n, lane, nxt);
+    }
+
+    const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
+    const bool lv = lane < nl;
+    const int nb = __builtin_popcount(bits);
+    const int idb = wk.scur + scan_i(nb) - nb;  // segment of this lane's first entry
+
+    // Gathers, residual bookkeeping, and running sums restarted at segment starts.
+    float r[kE], sn[kE], sd[kE];
+    float an = 0.0f, ad = 0.0f;
+    int slot = idb - wk.scur;
+#pragma unroll
+    for (int k = 0; k < kE; ++k) {
+        const bool fk = (bits >> k) & 1u;
+        if constexpr (N::p || N::pp) slot += fk ? 1 : 0;
+        const uint32_t c = col_of<IDX16>(cur, k);
+        const float pr = N::p ? spr[slot] : 0.0f;
+        const float ppr = N::pp ? sppr[slot] : 0.0f;
+        const float qv = N::q ? gat<STAGED>(gx.lq, gx.gq, c) : 0.0f;
+        const float qqv = N::qq ? gat<STAGED>(gx.lqq, gx.gqq, c) : 0.0f;
+        r[k] = rhat<MODE>(val_of(cur, k), qv, qqv, pr, ppr);
+        if constexpr (N::x) {
+            const float xv = gat<STAGED>(gx.lx, gx.gx, c);
+            an = __builtin_fmaf(r[k], xv, fk ? 0.0f : an);
+            ad = __builtin_fmaf(xv, xv, fk ? 0.0f : ad);
+            sn[k] = an;
+            sd[k] = ad;
+        }
+    }
+    if constexpr (N::store) {
+        if (lv) {
+            f32x4 w0, w1;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                w0[k] = r[k];
+                w1[k] = r[4 + k];
+            }
+            f32x4* wp = reinterpret_cast<f32x4*>(a.val + b + le);
+            __builtin_nontemporal_store(w0, wp);
+            __builtin_nontemporal_store(w1, wp + 1);
+        }
+    }
+    if constexpr (MODE == kModeFlush) {
+        float s2 = 0.0f;
+#pragma unroll
+        for (int k = 0; k < kE; ++k) s2 = __builtin_fmaf(r[k], r[k], s2);
+        if (lv) wk.sse += (double)s2;
+    } else {
+        // A segment left open by the previous window that ended where this one starts.
+        if (wk.cid >= 0 && wk.cid != wk.scur) {
+            if (lane == 0) emit<P1>(a, wk.cid, wk.cn, wk.cd);
+            wk.cid = -1;
+        }
+        // Scan keys: segment + 1 of the lane's first (hk) and last (tk) entry, 0 on
+        // lanes without entries.
+        const int hk = lv ? idb + (int)(bits & 1u) + 1 : 0;
+        const int tk = lv ? idb + nb + 1 : 0;
+        float scn = an, scd = ad;
+        seg_scan(tk, scn, scd);
+        // Sums of this lane's first segment over earlier lanes, and from earlier windows.
+        const int pk1 = dpp_i<kWaveShr1, 0xF, true>(0, tk);
+        const float pn1 = dpp_f<kWaveShr1, 0xF, true>(0.0f, scn);
+        const float pd1 = dpp_f<kWaveShr1, 0xF, true>(0.0f, scd);
+        double hn = 0.0, hd = 0.0;
+        if (pk1 == hk) {
+            hn = (double)pn1;
+            hd = (double)pd1;
+        }
+        if (hk == wk.cid + 1) {
+            hn += wk.cn;
+            hd += wk.cd;
+        }
+        // Entry k ends a segment when entry k + 1 starts one; the lane's last entry
+        // when the next lane's first does.  The window's last entry stays open.
+        const uint32_t nb0 = (uint32_t)dpp_i<kWaveShl1, 0xF, true>(0, (int)(bits & 1u));
+        uint32_t ends = (bits >> 1) | ((lane + 1 < nl ? nb0 : 0u) << (kE - 1));
+        if (!lv) ends = 0u;
+        const uint32_t ff = bits ? (uint32_t)__builtin_ctz(bits) : (uint32_t)kE;  // head: k < ff
+        // Emit one end per lane per round; most windows need one round.
+        uint32_t rem = ends;
+        while (__ballot(rem != 0u)) {
+            if (rem != 0u) {
+                const uint32_t k = (uint32_t)__builtin_ctz(rem);
+                float vn = sn[0], vd = sd[0];
+#pragma unroll
+                for (int j = 1; j < kE; ++j)
+                    if (k == (uint32_t)j) {
+                        vn = sn[j];
+                        vd = sd[j];
+                    }
+                double en = (double)vn, ed = (double)vd;
+                if (k < ff) {
+                    en += hn;
+                    ed += hd;
+                }
+                const int s = idb + __builtin_popcount(bits & ((2u << k) - 1u));
+                emit<P1>(a, s, en, ed);
+                rem &= rem - 1u;
+            }
+        }
+        // The segment of the window's last entry stays open; one that started in that
+        // lane has no earlier sums.
+        const int ll = nl - 1;
+        const double ln = (double)an + (bits == 0u ? hn : 0.0);
+        const double ld = (double)ad + (bits == 0u ? hd : 0.0);
+        wk.cid = __builtin_amdgcn_readlane(tk, ll) - 1;
+        wk.cn = lane_f64(ln, ll);
+        wk.cd = lane_f64(ld, ll);
+    }
+    wk.scur = scur_n;
+    wk.elo = we;
+}
+
+// One wave's chunk [c0, c1) (whole segments, the first one scur), two windows per
+// loop turn so the current and next window alternate between two register sets.
+template <int MODE, bool STAGED, bool IDX16, bool P1>
+__device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, int64_t c0,
+                                          int64_t c1, int scur, int lane, float* spr,
+                                          float* sppr, uint32_t* bm, double& sse) {
+    const uint32_t le = (uint32_t)lane * kE;
+    Walk wk{c0, c1, scur, -1, 0.0, 0.0, sse};
+    Win wa, wb;
+    load_window<MODE, IDX16>(a, c0, c1, le, scur, lane, wa);
+    while (true) {
+        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wa, wb, lane, le, spr, sppr, bm);
+        if (wk.elo >= c1) break;
+        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wb, wa, lane, le, spr, sppr, bm);
+        if (wk.elo >= c1) break;
+    }
+    if constexpr (MODE != kModeFlush) {
+        if (wk.cid >= 0 && lane == 0) emit<P1>(a, wk.cid, wk.cn, wk.cd);
+    }
+    sse = wk.sse;
+}
+
+// One pass: the workgroup's pieces in order, each staging its tile (when it
+// differs from the one staged) and then giving every wave its chunk.
+template <int MODE, bool STAGED, bool IDX16, bool P1>
 __device__ __forceinline__ void pass_main(const PassArgs& a) {
     using N = Needs<MODE>;
     extern __shared__ float lds[];
     const int wg = blockIdx.x;
-    const int tile = a.wg_tile[wg];
-    const int rank = a.wg_rank[wg];
-    const int nwg = a.tile_nwg[tile];
-    const int ub = a.tile_unit[tile];
-    const int ue = a.tile_unit[tile + 1];
 
     Gather gx{};
-    if constexpr (STAGED) {
-        // Slots in the order x, q, qq; x shares q's slot when they are the same vector.
-        const int T = a.T;
-        const int c0 = tile * T;
-        const int len = min(T, a.cols - c0);
-        const bool alias = N::x && N::q && a.x_is_q;
-        int slot = 0;
-        float* sx = nullptr;
-        float* sq = nullptr;
-        float* sqq = nullptr;
-        if (N::x && !alias) sx = lds + (slot++) * T;
-        if (N::q) sq = lds + (slot++) * T;
-        if (alias) sx = sq;
-        if (N::qq) sqq = lds + (slot++) * T;
-        for (int i = threadIdx.x; i < len; i += kWG) {
-            if (N::x && !alias) sx[i] = a.x[c0 + i];
-            if (N::q) sq[i] = a.q[c0 + i];
-            if (N::qq) sqq[i] = a.qq[c0 + i];
-        }
-        __syncthreads();
-        gx.lx = sx;
-        gx.lq = sq;
-        gx.lqq = sqq;
-    } else {
+    if constexpr (!STAGED) {
         const uint64_t vb = (uint64_t)a.cols * 4u;
         if (N::x) gx.gx = make_rsrc(a.x, vb);
         if (N::q) gx.gq = make_rsrc(a.q, vb);
         if (N::qq) gx.gqq = make_rsrc(a.qq, vb);
     }
-
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = (int)(threadIdx.x & 63u);
+    uint32_t* scr = reinterpret_cast<uint32_t*>(lds + a.vec_floats) + wave * kScratch;
+    uint32_t* bm = scr;                                             // kWin / 32 words
+    float* spr = reinterpret_cast<float*>(scr + kWin / 32);        // 64 row scalars p
+    float* sppr = reinterpret_cast<float*>(scr + kWin / 32 + 64);  // 64 row scalars pp
+
+    if constexpr (MODE != kModeFlush && P1) {
+        // The rows after the last non-empty one have no entries: coordinate 0.
+        for (int i = wg * kWG + (int)threadIdx.x; i < a.rows - a.nseg_ne; i += gridDim.x * kWG)
+            a.y[a.nseg_ne + i] = coordinate(0.0, 0.0, a.lambda);
+    }
+
     double sse = 0.0;
-    for (int u = ub + rank * kWaves + wave; u < ue; u += nwg * kWaves) {
-        const int2 ud = a.units[u];
-        const int kind = ud.y & 0xFF;
-        const int cnt = ud.y >> 8;
-        switch (kind) {
-            case kULong: unit_long<MODE, STAGED, IDX16>(a, gx, ud.x, lane, sse); break;
-            case kUG64E16: unit_groups<MODE, STAGED, IDX16, 64, 16>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG64E8: unit_groups<MODE, STAGED, IDX16, 64, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG32E8: unit_groups<MODE, STAGED, IDX16, 32, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG16E8: unit_groups<MODE, STAGED, IDX16, 16, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG8E8: unit_groups<MODE, STAGED, IDX16, 8, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG4E8: unit_groups<MODE, STAGED, IDX16, 4, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            case kUG2E8: unit_groups<MODE, STAGED, IDX16, 2, 8>(a, gx, ud.x, cnt, lane, sse); break;
-            default: unit_groups<MODE, STAGED, IDX16, 1, 8>(a, gx, ud.x, cnt, lane, sse); break;
+    int staged = -1;
+    for (int pc = a.wg_piece[wg]; pc < a.wg_piece[wg + 1]; ++pc) {
+        if constexpr (STAGED) {
+            const int tile = a.piece_tile[pc];
+            if (tile != staged) {
+                if (staged >= 0) __syncthreads();  // every wave is done with the old slice
+                stage_tile<MODE>(a, tile, lds, gx);
+                __syncthreads();
+                staged = tile;
+            }
         }
+        const int64_t c0 = a.piece_chunk[pc * (kWaves + 1) + wave];
+        const int64_t c1 = a.piece_chunk[pc * (kWaves + 1) + wave + 1];
+        if (c0 < c1)
+            run_chunk<MODE, STAGED, IDX16, P1>(a, gx, c0, c1, a.piece_seg[pc * kWaves + wave],
+                                               lane, spr, sppr, bm, sse);
     }
     if constexpr (MODE == kModeFlush) {
-        const double t = group_sum<64>(sse);
+        const double t = wave_sum(sse);
         if (lane == 0) a.sse_part[wg * kWaves + wave] = t;
     }
 }
@@ -319,26 +532,28 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
 }  // namespace
 
 // Distinct kernel names per pass kind, so that profiles separate them.  The
-// template arguments select LDS staging and the index width.
-template <bool STAGED, bool IDX16>
+// template arguments select LDS staging, the index width and whether segments
+// are rows (P == 1).
+template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass(PassArgs a) {
-    pass_main<kModePlain, STAGED, IDX16>(a);
+    pass_main<kModePlain, STAGED, IDX16, P1>(a);
 }
-template <bool STAGED, bool IDX16>
+template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused_first(PassArgs a) {
-    pass_main<kModeAdd, STAGED, IDX16>(a);
+    pass_main<kModeAdd, STAGED, IDX16, P1>(a);
 }
-template <bool STAGED, bool IDX16>
+template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused(PassArgs a) {
-    pass_main<kModeSubAdd, STAGED, IDX16>(a);
+    pass_main<kModeSubAdd, STAGED, IDX16, P1>(a);
 }
-template <bool STAGED, bool IDX16>
+template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_flush(PassArgs a) {
-    pass_main<kModeFlush, STAGED, IDX16>(a);
+    pass_main<kModeFlush, STAGED, IDX16, P1>(a);
 }
 
 // Fixed-order combine of the per-tile partials of each row: one wave per row,
-// lane k takes the row's segments k, k + 64, ... in tile order, then a fixed tree.
+// lane k takes the row's segments k, k + 64, ... in tile order, then a fixed
+// tree.  With yseg, the coordinate is also written to every segment of the row.
 __global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
     const int wave = (int)(threadIdx.x >> 6);
     const int lane = (int)(threadIdx.x & 63u);
@@ -352,9 +567,12 @@ __global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
         num += pv.x;
         den += pv.y;
     }
-    num = group_sum<64>(num);
-    den = group_sum<64>(den);
-    if (lane == 0) c.y[r] = coordinate(num, den, c.lambda);
+    num = wave_sum(num);
+    den = wave_sum(den);
+    const float yr = coordinate(num, den, c.lambda);
+    if (lane == 0) c.y[r] = yr;
+    if (c.yseg)
+        for (int k = b + lane; k < e; k += 64) c.yseg[c.row_segs[k]] = yr;
 }
 
 __global__ __launch_bounds__(256) void ccd_copy(const float* __restrict__ src,
@@ -390,10 +608,10 @@ int staged_vectors(PassMode mode, bool x_is_q) {
 }
 
 namespace {
-template <bool S, bool I>
+template <bool S, bool I, bool P1>
 hipError_t raise_lds() {
-    const void* ks[] = {(const void*)ccd_pass<S, I>, (const void*)ccd_pass_fused_first<S, I>,
-                        (const void*)ccd_pass_fused<S, I>, (const void*)ccd_flush<S, I>};
+    const void* ks[] = {(const void*)ccd_pass<S, I, P1>, (const void*)ccd_pass_fused_first<S, I, P1>,
+                        (const void*)ccd_pass_fused<S, I, P1>, (const void*)ccd_flush<S, I, P1>};
     for (const void* k : ks) {
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
         if (e != hipSuccess) return e;
@@ -401,39 +619,48 @@ hipError_t raise_lds() {
     return hipSuccess;
 }
 
-template <bool S, bool I>
+template <bool S, bool I, bool P1>
 void launch_mode(PassMode mode, dim3 grid, size_t lds, hipStream_t s, const PassArgs& a) {
     switch (mode) {
-        case kModePlain: hipLaunchKernelGGL((ccd_pass<S, I>), grid, dim3(kWG), lds, s, a); break;
-        case kModeAdd: hipLaunchKernelGGL((ccd_pass_fused_first<S, I>), grid, dim3(kWG), lds, s, a); break;
-        case kModeSubAdd: hipLaunchKernelGGL((ccd_pass_fused<S, I>), grid, dim3(kWG), lds, s, a); break;
-        case kModeFlush: hipLaunchKernelGGL((ccd_flush<S, I>), grid, dim3(kWG), lds, s, a); break;
+        case kModePlain:
+            hipLaunchKernelGGL((ccd_pass<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            break;
+        case kModeAdd:
+            hipLaunchKernelGGL((ccd_pass_fused_first<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            break;
+        case kModeSubAdd:
+            hipLaunchKernelGGL((ccd_pass_fused<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            break;
+        case kModeFlush:
+            hipLaunchKernelGGL((ccd_flush<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            break;
     }
 }
 }  // namespace
 
 hipError_t sweep_init() {
-    hipError_t e = raise_lds<true, true>();
-    if (e != hipSuccess) return e;
-    e = raise_lds<false, true>();
-    if (e != hipSuccess) return e;
-    return raise_lds<false, false>();
+    hipError_t e = raise_lds<true, true, true>();
+    if (e == hipSuccess) e = raise_lds<true, true, false>();
+    if (e == hipSuccess) e = raise_lds<false, true, true>();
+    if (e == hipSuccess) e = raise_lds<false, false, true>();
+    return e;
 }
 
 hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const float* p,
                        const float* pp, const float* q, const float* qq, float* y, double lambda,
                        double* sse_part, hipStream_t s) {
     if (L.grid == 0) return hipSuccess;
+    const bool staged = L.gather == kGatherLds;
+    // Kernel variants: LDS staging uses 16-bit indices; global gathers have P == 1.
+    if (staged ? !L.idx16 : L.P != 1) return hipErrorInvalidValue;
     PassArgs a{};
     a.idx = L.idx;
     a.val = L.val;
     a.seg_start = L.seg_start;
-    a.seg_row = L.seg_row;
-    a.units = L.units;
-    a.wg_tile = L.wg_tile;
-    a.wg_rank = L.wg_rank;
-    a.tile_unit = L.tile_unit;
-    a.tile_nwg = L.tile_nwg;
+    a.wg_piece = L.wg_piece;
+    a.piece_tile = L.piece_tile;
+    a.piece_chunk = L.piece_chunk;
+    a.piece_seg = L.piece_seg;
     a.x = x;
     a.p = p;
     a.pp = pp;
@@ -442,34 +669,40 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.y = y;
     a.part = L.part;
     a.sse_part = sse_part;
-    a.nnz = L.nnz;
     a.rows = (int32_t)L.rows;
     a.cols = (int32_t)L.cols;
     a.T = L.T;
     a.P = L.P;
+    a.Ts = L.T + 1;
     a.nseg = (int32_t)L.nseg;
+    a.nseg_ne = (int32_t)L.nseg_ne;
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
     a.lambda = lambda;
+    a.vec_floats = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
+    const size_t lds = (size_t)a.vec_floats * sizeof(float) + (size_t)kWaves * kScratch * 4;
+    if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     const dim3 grid(L.grid);
-    if (L.gather == kGatherLds) {
-        const size_t lds = (size_t)staged_vectors(mode, a.x_is_q) * L.T * sizeof(float);
-        if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
-        launch_mode<true, true>(mode, grid, lds, s, a);
+    if (staged) {
+        if (L.P == 1)
+            launch_mode<true, true, true>(mode, grid, lds, s, a);
+        else
+            launch_mode<true, true, false>(mode, grid, lds, s, a);
     } else if (L.idx16) {
-        launch_mode<false, true>(mode, grid, 0, s, a);
+        launch_mode<false, true, true>(mode, grid, lds, s, a);
     } else {
-        launch_mode<false, false>(mode, grid, 0, s, a);
+        launch_mode<false, false, true>(mode, grid, lds, s, a);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_combine(const Layout& L, float* y, double lambda, hipStream_t s) {
+hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda, hipStream_t s) {
     if (L.P <= 1 || L.rows == 0) return hipSuccess;
     CombineArgs c{};
     c.row_seg_ptr = L.row_seg_ptr;
     c.row_segs = L.row_segs;
     c.part = L.part;
     c.y = y;
+    c.yseg = yseg;
     c.rows = (int32_t)L.rows;
     c.lambda = lambda;
     hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.rows + 3) / 4)), dim3(256), 0, s, c);
