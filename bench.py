@@ -29,6 +29,23 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 KERNEL_NAMES = {0: "ccd_pass_fused", 1: "ccd_pass", 2: "ccd_combine", 3: "ccd_copy", 4: "ccd_flush"}
+LAYOUT_NAMES = {0: "rows", 1: "cols"}
+
+
+def kernel_symbol(kind: int, info: dict, layout: int) -> str:
+    """The kernel's name as a trace shows it (the sweep kernels are templated on
+    LDS staging, 16-bit indices and P == 1)."""
+    if kind == 2:
+        return "ccdk::ccd_combine(ccdk::CombineArgs)"
+    if kind == 3:
+        return "ccdk::ccd_copy(float const*, float*, long)"
+    pre = "u" if layout == 0 else "v"
+    staged = info[f"{pre}_gather"] == 2
+    idx16 = staged or info[f"{pre}_tile_width"] < 65536
+    p1 = info[f"{pre}_tiles"] == 1
+    name = KERNEL_NAMES[kind]
+    b = lambda x: "true" if x else "false"
+    return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}>(ccdk::PassArgs)"
 
 
 def log(msg):
@@ -37,7 +54,7 @@ def log(msg):
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("sweep.hip", "ccdpp_internal.hpp"):
+    for f in ("sweep.hip", "ccdpp_internal.hpp", "api.hip"):
         with open(os.path.join(ROOT, "paper_1511_02433_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -89,6 +106,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-MiB device buffer 3 times (a kernel of known HBM "
+                         "traffic, to scale hardware byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -103,6 +123,15 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        nel = args.copy_calibration * (1 << 20) // 4
+        x = torch.ones(nel, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        log(f"copied {args.copy_calibration} MiB three times")
+        return
     ds = synth.load(args.workload, verbose=True)
     w = ds.workload
     k = args.k or w.k
@@ -121,16 +150,14 @@ def main():
 
     def timed(steps, prof):
         g.profile(prof)
-        s = torch.cuda.current_stream()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        e0.record(s)
+        t0 = time.perf_counter()
         for _ in range(steps):
             g.run(1, inner)
-        e1.record(s)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / steps
+        return (time.perf_counter() - t0) * 1e3 / steps
 
+    # The timed region: exactly `steps` steps, kernel events on the library's stream.
     prof = not args.no_prof
     ms = timed(args.steps, prof)
     kinds = {}
@@ -141,26 +168,32 @@ def main():
             if n:
                 kinds[name] = {"launches": n, "mean_us": tot / n * 1e3, "total_ms": tot,
                                "algo_bytes_per_launch": b / n, "gbs": b / (tot * 1e-3) / 1e9}
-                for lay, lname in ((0, "rows"), (1, "cols")):
-                    n2, t2, b2 = g.profile_read(kind, lay)
-                    if n2:
-                        per_layout[f"{name}/{lname}"] = {
-                            "launches": n2, "mean_us": round(t2 / n2 * 1e3, 2),
-                            "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
+            for lay, lname in LAYOUT_NAMES.items():
+                n2, t2, b2 = g.profile_read(kind, lay)
+                if n2:
+                    per_layout[f"{name}/{lname}"] = {
+                        "kernel": kernel_symbol(kind, info, lay), "launches": n2,
+                        "mean_us": round(t2 / n2 * 1e3, 3), "total_ms": round(t2, 4),
+                        "algo_bytes_per_launch": b2 / n2,
+                        "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
     g.profile(False)
     ms_plain = timed(max(2, args.steps // 2), False) if prof else ms
     visits = 2.0 * inner * k * w.nnz
     value = visits / (ms * 1e-3) / 1e9
     log(f"{ms:.3f} ms/step with kernel events, {ms_plain:.3f} ms/step without; {value:.1f} Gnnz/s")
 
+    # Roofline of the dominant kernel: the (kernel, residual copy) pair with the most
+    # device time per step.
     roofline = None
-    if kinds:
-        dom = max(kinds, key=lambda kk: kinds[kk]["total_ms"])
-        d = kinds[dom]
+    if per_layout:
+        dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"])
+        d = per_layout[dom]
         achieved = d["algo_bytes_per_launch"] / (d["mean_us"] * 1e-6) / 1e9
-        roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": stored_traffic(dom, w.name)}
+        roofline = {"kernel": d["kernel"], "layout": dom.split("/")[1], "bound": "hbm",
+                    "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": stored_traffic(dom.replace("/", "_"), w.name),
+                    "mean_us": d["mean_us"], "algo_bytes_per_launch": d["algo_bytes_per_launch"]}
     train_rmse = g.train_rmse()
     test_rmse = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
     model_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / args.steps \

@@ -86,13 +86,17 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 tile_width columns when they do not fit
  *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
  *                 163840 / (4 * v) where v = 2 for index 0 and 3 for index 1
- *   workgroups  : persistent workgroups per pass (0: two per compute unit)
+ *   workgroups  : persistent workgroups per pass (0: one per compute unit)
+ *   seg_weight  : work of one row segment, in entries, when the entries are
+ *                 shared out among workgroups and waves (0: the default, 12;
+ *                 -1: shares by entries alone)
  * Results differ between layouts only by floating-point summation order.
  */
 typedef struct ccdpp_options {
     int32_t gather_mode[2];
     int32_t tile_width[2];
     int32_t workgroups;
+    int32_t seg_weight;
 } ccdpp_options_t;
 
 /* ccdpp_create with explicit layout options (opts may be NULL). */

@@ -27,14 +27,15 @@ class Options(ctypes.Structure):
     """ccdpp_options_t: layout knobs (0 = automatic).  Index 0 is the user-major copy,
     1 the item-major copy.  gather_mode: 1 global memory, 2 LDS-staged."""
     _fields_ = [("gather_mode", ctypes.c_int32 * 2), ("tile_width", ctypes.c_int32 * 2),
-                ("workgroups", ctypes.c_int32)]
+                ("workgroups", ctypes.c_int32), ("seg_weight", ctypes.c_int32)]
 
 
-def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0) -> Options:
+def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight=0) -> Options:
     o = Options()
     o.gather_mode[0], o.gather_mode[1] = gather_mode
     o.tile_width[0], o.tile_width[1] = tile_width
     o.workgroups = workgroups
+    o.seg_weight = seg_weight
     return o
 
 

@@ -198,8 +198,9 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     L.cols = cols;
     L.nnz = N;
     const int nvec = side == 0 ? 2 : 3;
-    // Each staged slice holds T floats plus a trailing zero (the padding entries' target).
-    const int64_t tmax = ((int64_t)kLdsVecBytes / (4 * nvec) - 1) / 64 * 64;
+    // Each staged slice holds T floats rounded up to 32, then 32 more words whose first
+    // is the zero the padding entries read.
+    const int64_t tmax = ((int64_t)kLdsVecBytes / (4 * nvec) - 64) / 64 * 64;
     const int forced = opt ? opt->gather_mode[side] : 0;
     const int64_t forced_T = opt ? opt->tile_width[side] : 0;
     if (forced_T > tmax)
@@ -247,7 +248,10 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     L.gather = lds ? kGatherLds : kGatherGlobal;
     L.T = (int32_t)T;
     L.P = (int32_t)P;
-    L.idx16 = T < 65536;  // tile-local indices 0..T-1 and the padding index T fit 16 bits
+    L.swz = lds;
+    L.pad = lds ? (int32_t)((T + 31) / 32 * 32) : (int32_t)T;
+    L.Ts = lds ? L.pad + 32 : (int32_t)T + 1;
+    L.idx16 = L.pad < 65536;  // every index, the padding one included, fits 16 bits
 
     // Segments.  P == 1: segment r is row r (rows are relabelled by decreasing
     // length, so the empty ones come last).  P > 1: the non-empty rows of each
@@ -277,81 +281,153 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     while (S_ne > 0 && seg_start[S_ne] == seg_start[S_ne - 1]) --S_ne;
     L.nseg_ne = S_ne;
 
-    // Persistent workgroups.  Workgroup g owns the entries from the first segment
-    // start at or after g * N / G up to the same point for g + 1, so every share is
-    // within one segment of N / G.  A share is processed as one piece per tile it
-    // touches; inside a piece the 16 waves own chunks cut the same way.  Chunk
-    // bounds are kept as segment indices here and turned into padded positions below.
+    // Alignment padding: each tile's entries start at a multiple of kE; the entries
+    // skipped over are padding at the end of the previous tile's last segment.
+    const int64_t S_work = P == 1 ? S_ne : S;  // segments that hold entries
+    std::vector<int32_t> seg_off((size_t)S, 0);
+    std::vector<int64_t> pstart((size_t)S + 1);
+    {
+        std::vector<char> tile_first((size_t)S + 1, 0);
+        for (int64_t p = 0; p < P; ++p) tile_first[tile_seg[p]] = 1;
+        int64_t off = 0;
+        for (int64_t sg = 0; sg < S_work; ++sg) {
+            if (tile_first[sg]) off += (kE - (seg_start[sg] + off) % kE) % kE;
+            seg_off[sg] = (int32_t)off;
+            pstart[sg] = seg_start[sg] + off;
+        }
+        const int64_t NP = (N + off + kE - 1) / kE * kE;
+        if (NP > (int64_t)INT32_MAX - kEntryPad)
+            return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
+        for (int64_t sg = S_work; sg <= S; ++sg) pstart[sg] = NP;
+        L.npad = NP;
+    }
+    const int64_t NP = L.npad;
+    seg_start.swap(pstart);  // from here on, segment starts are padded positions
+
+    // Persistent workgroups own equal shares of the work, cut at multiples of kE; a
+    // share is processed as one piece per tile it touches, and every piece is cut
+    // into kWaves chunks of equal work, one per wave.  The work of a range is its
+    // entries plus seg_weight per segment starting in it (a segment's emission, and
+    // the shorter windows of short segments, cost about that many entries).  Chunk
+    // bounds ignore segment bounds: a segment cut by one or more chunk bounds leaves,
+    // in every chunk it meets, a partial (num, den) in a slot of its own (the chunk's
+    // head slot if the segment began before the chunk, else its tail slot), and the
+    // combine adds a row's partials in entry order.
     int64_t G = opt && opt->workgroups > 0 ? opt->workgroups : (int64_t)h->cus;
     if (!(opt && opt->workgroups > 0))
-        G = std::max<int64_t>(1, std::min<int64_t>(G, (N + kWaves * kWin - 1) / (kWaves * kWin)));
-    const int64_t S_work = P == 1 ? S_ne : S;  // segments that hold entries
-    auto seg_at = [&](int64_t s_lo, int64_t s_hi, int64_t target) -> int64_t {
-        // first segment in [s_lo, s_hi] whose start is >= target (s_hi if none)
-        return std::lower_bound(seg_start.begin() + s_lo, seg_start.begin() + s_hi, target) -
-               seg_start.begin();
+        G = std::max<int64_t>(1, std::min<int64_t>(G, (NP + kWaves * kWin - 1) / (kWaves * kWin)));
+    const int64_t wseg = !opt || opt->seg_weight == 0 ? kSegWeight
+                         : std::max<int64_t>(0, opt->seg_weight);
+    auto up8 = [](int64_t v) { return (v + kE - 1) / kE * kE; };
+    // Last segment of tile p starting at or before position e.
+    auto seg_of = [&](int64_t p, int64_t e) -> int64_t {
+        return std::upper_bound(seg_start.begin() + tile_seg[p], seg_start.begin() + tile_seg[p + 1],
+                                e) - seg_start.begin() - 1;
     };
-    std::vector<int32_t> wg_piece(1, 0), piece_tile, piece_seg;
-    std::vector<int64_t> chunk_segs;  // [npieces * (kWaves + 1)] segment index of each bound
-    std::vector<char> chunk_start((size_t)S + 1, 0);
-    int64_t g_seg = 0;
+    // Work up to position e, and the last position whose work is at most t.
+    auto work_at = [&](int64_t e) -> int64_t {
+        if (S_work == 0) return e;
+        const int64_t sg = std::upper_bound(seg_start.begin(), seg_start.begin() + S_work, e) -
+                           seg_start.begin();  // segments starting at or before e
+        return e + wseg * sg;
+    };
+    auto pos_at = [&](int64_t t) -> int64_t {
+        int64_t lo = 0, hi = NP;  // work_at is increasing: largest e with work_at(e) <= t
+        while (lo < hi) {
+            const int64_t mid = (lo + hi + 1) / 2;
+            if (work_at(mid) <= t) lo = mid; else hi = mid - 1;
+        }
+        return lo;
+    };
+    const int64_t work_total = work_at(NP);
+    std::vector<int32_t> wg_piece(1, 0), piece_tile, piece_seg, chunk_flags;
+    std::vector<int64_t> piece_chunk;
+    std::vector<std::vector<int32_t>> src_of((size_t)S);  // partial slots of each cut segment
+    std::vector<int64_t> gb((size_t)G + 1);
+    for (int64_t g = 0; g <= G; ++g)
+        gb[g] = g == 0 ? 0 : g == G ? NP : std::min(NP, up8(pos_at(work_total / G * g +
+                                                                    work_total % G * g / G)));
     for (int64_t g = 0; g < G; ++g) {
-        const int64_t g_end = g + 1 == G ? S_work : seg_at(g_seg, S_work, N * (g + 1) / G);
-        for (int64_t p = 0; p < P && g_seg < g_end; ++p) {
-            const int64_t a0 = std::max<int64_t>(g_seg, tile_seg[p]);
-            const int64_t a1 = std::min<int64_t>(g_end, tile_seg[p + 1]);
-            if (a0 >= a1 || seg_start[a0] == seg_start[a1]) continue;
-            const int64_t lo = seg_start[a0], hi = seg_start[a1];
+        const int64_t lo = gb[g], hi = std::max(gb[g], gb[g + 1]);
+        for (int64_t p = 0; p < P; ++p) {
+            const int64_t a0 = std::max(lo, seg_start[tile_seg[p]]);
+            const int64_t a1 = std::min(hi, seg_start[tile_seg[p + 1]]);
+            if (a0 >= a1) continue;
+            const int64_t pc = (int64_t)piece_tile.size();
             piece_tile.push_back((int32_t)p);
-            int64_t sw = a0;
+            const int64_t w0 = work_at(a0), w1 = work_at(a1);
+            for (int w = 0; w <= kWaves; ++w)
+                piece_chunk.push_back(w == 0 ? a0 : w == kWaves ? a1
+                                      : std::min(a1, std::max(a0, up8(pos_at(w0 + (w1 - w0) * w / kWaves)))));
             for (int w = 0; w < kWaves; ++w) {
-                chunk_segs.push_back(sw);
-                piece_seg.push_back((int32_t)sw);
-                chunk_start[sw] = 1;
-                sw = w + 1 == kWaves ? a1 : seg_at(sw, a1, lo + (hi - lo) * (w + 1) / kWaves);
+                const int64_t c0 = piece_chunk[pc * (kWaves + 1) + w];
+                const int64_t c1 = piece_chunk[pc * (kWaves + 1) + w + 1];
+                const int64_t gc = pc * kWaves + w;
+                if (c0 >= c1) {
+                    piece_seg.push_back(0);
+                    chunk_flags.push_back(0);
+                    continue;
+                }
+                const int64_t s0 = seg_of(p, c0), s1 = seg_of(p, c1 - 1);
+                const bool mid = seg_start[s0] < c0;     // first segment began earlier
+                const bool cont = seg_start[s1 + 1] > c1;  // last segment goes on
+                piece_seg.push_back((int32_t)s0);
+                chunk_flags.push_back((mid ? kChunkMid : 0) | (cont ? kChunkCont : 0));
+                if (mid) src_of[s0].push_back((int32_t)(S + 2 * gc));
+                if (cont && !(mid && s1 == s0)) src_of[s1].push_back((int32_t)(S + 2 * gc + 1));
             }
-            chunk_segs.push_back(a1);
         }
         wg_piece.push_back((int32_t)piece_tile.size());
-        g_seg = g_end;
     }
     L.grid = (int32_t)G;
     L.npieces = (int32_t)piece_tile.size();
+    const int64_t nslots = S + 2 * (int64_t)L.npieces * kWaves;
+    if (nslots > INT32_MAX) return fail(h, CCDPP_EINVAL, "too many partial slots");
 
-    // Alignment padding: every chunk start moves up to the next multiple of kE; the
-    // entries skipped over are padding at the end of the segment before it.
-    std::vector<int32_t> seg_off((size_t)S, 0);
-    std::vector<int64_t> pstart((size_t)S + 1);
-    int64_t off = 0;
-    for (int64_t sg = 0; sg < S_work; ++sg) {
-        if (chunk_start[sg]) off += (kE - (seg_start[sg] + off) % kE) % kE;
-        seg_off[sg] = (int32_t)off;
-        pstart[sg] = seg_start[sg] + off;
-    }
-    const int64_t NP = (N + off + kE - 1) / kE * kE;
-    if (NP > (int64_t)INT32_MAX - kEntryPad)
-        return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
-    for (int64_t sg = S_work; sg <= S; ++sg) pstart[sg] = NP;
-    L.npad = NP;
-    std::vector<int64_t> piece_chunk(chunk_segs.size());
-    for (size_t i = 0; i < chunk_segs.size(); ++i) piece_chunk[i] = pstart[chunk_segs[i]];
-    seg_start.swap(pstart);
-
-    // Segments of each row in tile order (for the combine of P > 1).
-    if (P > 1) {
-        std::vector<int32_t> rptr(rows + 1, 0), rsegs((size_t)S);
-        for (int64_t r = 0; r < rows; ++r) {
-            int32_t c = 0;
-            for (int64_t p = 0; p < P; ++p) c += segid[p * rows + r] >= 0;
-            rptr[r + 1] = rptr[r] + c;
+    // Combine lists.  P == 1: only the rows whose segment was cut, each from its
+    // partial slots.  P > 1: every row, from its segments in tile order (a cut
+    // segment by its partial slots), plus the segment list for the per-segment
+    // copy of the committed coordinate.
+    {
+        std::vector<int32_t> ids, sptr(1, 0), srcs, gptr, gsegs;
+        auto add_seg = [&](int64_t sg) {
+            if (src_of[sg].empty())
+                srcs.push_back((int32_t)sg);
+            else
+                srcs.insert(srcs.end(), src_of[sg].begin(), src_of[sg].end());
+        };
+        if (P == 1) {
+            for (int64_t sg = 0; sg < S; ++sg)
+                if (!src_of[sg].empty()) {
+                    ids.push_back((int32_t)sg);
+                    add_seg(sg);
+                    sptr.push_back((int32_t)srcs.size());
+                }
+            L.ncomb = (int32_t)ids.size();
+            if (!ids.empty()) RCK(upload(h, &L.comb_rows, ids));
+        } else {
+            gptr.assign(1, 0);
+            for (int64_t r = 0; r < rows; ++r) {
+                for (int64_t p = 0; p < P; ++p) {
+                    const int32_t sg = segid[p * rows + r];
+                    if (sg < 0) continue;
+                    add_seg(sg);
+                    gsegs.push_back(sg);
+                }
+                sptr.push_back((int32_t)srcs.size());
+                gptr.push_back((int32_t)gsegs.size());
+            }
+            L.ncomb = (int32_t)rows;
+            RCK(upload(h, &L.row_seg_ptr, gptr));
+            RCK(upload(h, &L.row_segs, gsegs));
         }
-        std::vector<int32_t> fillp(rptr.begin(), rptr.end() - 1);
-        for (int64_t r = 0; r < rows; ++r)
-            for (int64_t p = 0; p < P; ++p)
-                if (segid[p * rows + r] >= 0) rsegs[fillp[r]++] = segid[p * rows + r];
-        RCK(upload(h, &L.row_seg_ptr, rptr));
-        RCK(upload(h, &L.row_segs, rsegs));
-        HIPCK(h, dalloc(h, &L.part, S));
+        if (L.ncomb > 0) {
+            RCK(upload(h, &L.src_ptr, sptr));
+            RCK(upload(h, &L.srcs, srcs));
+        }
+        L.nsrc = (int64_t)srcs.size();
+        HIPCK(h, dalloc(h, &L.part, nslots));
+        L.nslots = nslots;
     }
     RCK(upload(h, &L.seg_start, seg_start));
     RCK(upload(h, &L.seg_row, seg_row));
@@ -360,6 +436,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     RCK(upload(h, &L.piece_tile, piece_tile));
     RCK(upload(h, &L.piece_chunk, piece_chunk));
     RCK(upload(h, &L.piece_seg, piece_seg));
+    RCK(upload(h, &L.chunk_flags, chunk_flags));
 
     // Sort the entries into layout order and fill index and value arrays.
     const int cbits = bits_for((uint64_t)std::max<int64_t>(T - 1, 1));
@@ -378,7 +455,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         HIPCK(h, dalloc(h, &d, NP + kEntryPad));
         L.idx = d;
     }
-    HIPCK(h, launch_fill_idx(L.idx, L.idx16, (int32_t)T, NP + kEntryPad, s));
+    HIPCK(h, launch_fill_idx(L.idx, L.idx16, L.pad, NP + kEntryPad, s));
     if (N > 0) {
         int32_t *d_segid, *d_off;
         uint64_t *k0, *k1;
@@ -409,7 +486,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             HIPCK(h, hipStreamSynchronize(s));
             if (flag) return fail(h, CCDPP_EDUP, "a position (i, j) occurs more than once");
         }
-        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, d_off, L.idx16, L.idx, L.val, epos,
+        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, d_off, L.swz, L.idx16, L.idx, L.val, epos,
                                     s));
         HIPCK(h, hipStreamSynchronize(s));
     }
@@ -518,12 +595,12 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, launch_fill(h->W, 0.0f, (int64_t)h->k * m, s));
     HIPCK(h, launch_fill(h->u, 0.0f, m, s));
     HIPCK(h, launch_fill(h->v, 0.0f, n, s));
-    for (int li = 0; li < 2; ++li)
-        if (h->L[li].part) {  // partials are written before they are read: start them as NaN
-            HIPCK(h, launch_fill(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
-                                 4 * h->L[li].nseg, s));
-            HIPCK(h, dalloc(h, &h->fseg[li], (int64_t)h->k * h->L[li].nseg));
-        }
+    for (int li = 0; li < 2; ++li) {
+        // Partials are written before they are read: start them as NaN.
+        HIPCK(h, launch_fill(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
+                             4 * h->L[li].nslots, s));
+        if (h->L[li].P > 1) HIPCK(h, dalloc(h, &h->fseg[li], (int64_t)h->k * h->L[li].nseg));
+    }
     {
         std::vector<float> h0((size_t)n * h->k);
         for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
@@ -643,9 +720,12 @@ int pass(ccdpp* h, int li, ccdk::PassMode mode, const float* x, int32_t pcol, in
                                    y, h->lambda, h->sse_part, h->stream));
         tm.done();
     }
-    if (mode != ccdk::kModeFlush && L.P > 1) {
-        float* yseg = commit >= 0 ? seg_col(h, li, commit) : nullptr;
-        Timed tc(h, CCDPP_K_COMBINE, li, 20.0 * L.nseg + 8.0 * L.rows + (yseg ? 4.0 * L.nseg : 0.0));
+    if (mode != ccdk::kModeFlush && L.ncomb > 0) {
+        float* yseg = commit >= 0 && L.P > 1 ? seg_col(h, li, commit) : nullptr;
+        // Partial slots read (16 B) and listed (4 B), per row a list bound, an id and y;
+        // with yseg the segment list and the per-segment copy.
+        Timed tc(h, CCDPP_K_COMBINE, li,
+                 20.0 * L.nsrc + 12.0 * L.ncomb + (yseg ? 12.0 * L.nseg : 0.0));
         HIPCK(h, ccdk::launch_combine(L, y, yseg, h->lambda, h->stream));
         tc.done();
     }

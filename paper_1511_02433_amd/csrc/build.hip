@@ -68,14 +68,15 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
 template <class I>
 __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
                               const float* __restrict__ val_in, int64_t nnz, int cbits,
-                              uint64_t mask, const int32_t* __restrict__ seg_off,
+                              uint64_t mask, const int32_t* __restrict__ seg_off, bool swz,
                               I* __restrict__ idx, float* __restrict__ val,
                               int32_t* __restrict__ pos) {
     for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * kT) {
         const uint64_t key = keys[q];
         const int64_t p = q + seg_off[key >> cbits];
-        idx[p] = (I)(key & mask);
+        const uint32_t c = (uint32_t)(key & mask);
+        idx[p] = (I)(swz ? lds_swizzle(c) : c);
         val[p] = val_in[perm[q]];
         pos[q] = (int32_t)p;
     }
@@ -134,7 +135,7 @@ __global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* 
 template <class I>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
-                          int32_t P, int32_t T, const I* __restrict__ idx,
+                          int32_t P, int32_t T, bool swz, const I* __restrict__ idx,
                           const int32_t* __restrict__ pos, const float* __restrict__ A,
                           const float* __restrict__ W, const float* __restrict__ H, int64_t m,
                           int64_t n, int32_t k, int64_t nnz, float* __restrict__ val) {
@@ -152,7 +153,8 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
             if (tile_seg[mid] <= lo) plo = mid; else phi = mid;
         }
         const int64_t i = seg_row[lo];
-        const int64_t j = (int64_t)plo * T + (int64_t)idx[q];
+        const uint32_t c = (uint32_t)idx[q];
+        const int64_t j = (int64_t)plo * T + (int64_t)(swz ? lds_swizzle(c) : c);
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
@@ -266,17 +268,17 @@ hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hi
 }
 
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, const int32_t* seg_off, bool idx16,
+                              int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
                               void* idx, float* val, int32_t* pos, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
     const uint64_t mask = cbits >= 64 ? ~0ull : ((1ull << cbits) - 1);
     if (idx16)
         hipLaunchKernelGGL(k_layout_fill<uint16_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, cbits, mask, seg_off, static_cast<uint16_t*>(idx), val,
+                           val_in, nnz, cbits, mask, seg_off, swz, static_cast<uint16_t*>(idx), val,
                            pos);
     else
         hipLaunchKernelGGL(k_layout_fill<int32_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, cbits, mask, seg_off, static_cast<int32_t*>(idx), val,
+                           val_in, nnz, cbits, mask, seg_off, swz, static_cast<int32_t*>(idx), val,
                            pos);
     return hipGetLastError();
 }
@@ -331,12 +333,12 @@ hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const fl
     if (L.nnz == 0) return hipSuccess;
     if (L.idx16)
         hipLaunchKernelGGL(k_rebuild<uint16_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
-                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
                            static_cast<const uint16_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
                            L.val);
     else
         hipLaunchKernelGGL(k_rebuild<int32_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
-                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
                            static_cast<const int32_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
                            L.val);
     return hipGetLastError();

@@ -32,19 +32,31 @@ namespace ccdk {
 // P == 1 and gathers from global memory instead ("global" mode).
 //
 // Persistent workgroups of kWG threads each own an equal, contiguous share of
-// the layout's (tile-major) entries, cut on segment boundaries.  A share that
-// crosses tile boundaries is processed as one "piece" per tile, restaging LDS
-// between pieces; inside a piece each of the 16 waves owns one contiguous
-// chunk, again cut on segment boundaries.  Shares, pieces and chunks, and with
-// them every reduction order, are fixed at build time, so results are
-// identical run to run.
+// the layout's (tile-major) entries.  A share that crosses tile boundaries is
+// processed as one "piece" per tile, restaging LDS between pieces; inside a
+// piece each of the 16 waves owns one of 16 equal contiguous chunks.  Chunk
+// bounds do not follow segment bounds, so every wave streams the same number
+// of entries however long the rows are: a segment cut by chunk bounds leaves
+// one partial (num, den) per chunk it meets, in a slot of that chunk, and a
+// combine kernel adds a row's partials in entry order.  Shares, pieces and
+// chunks, and with them every reduction order, are fixed at build time, so
+// results are identical run to run.
 //
-// Every chunk starts at a multiple of kE entries: the build inserts up to
-// kE - 1 padding entries at the end of the segment before each chunk start.  A
-// padding entry holds value 0 and the tile-local index T, which addresses a
-// zero kept after each staged vector slice in LDS (or lies past the vector in
-// global mode, where the bounded buffer load returns 0), so it adds exactly 0
-// to every sum and stays 0 under every residual update.
+// Every tile, and so every piece and chunk, starts at a multiple of kE
+// entries: the build inserts up to kE - 1 padding entries at the end of each
+// tile.  A padding entry holds value 0 and an index that reads 0 (a zero word
+// after each staged slice in LDS, or a position past the vector in global
+// mode, where the bounded buffer load returns 0), so it adds exactly 0 to
+// every sum and stays 0 under every residual update.
+//
+// Staged slices are stored XOR-swizzled: column c of the tile sits at LDS word
+// lds_swizzle(c), which permutes each aligned group of 32 words by the group's
+// index.  Runs of columns with a constant stride (dense rows of heavy users or
+// popular items) then spread over the LDS banks instead of hitting one bank,
+// and the layout stores the swizzled position as the entry's index, so the
+// pass pays nothing for it.  The padding index of a staged layout is the first
+// multiple of 32 at or above T, a word outside the swizzled range that staging
+// sets to zero.
 //
 // The per-row scalars a pass reads (the own factor column of the current and
 // the previous feature) are addressed by segment: with P == 1 segment s is row
@@ -59,7 +71,12 @@ constexpr int kScratch = 160;             // LDS words of per-wave scratch
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
 constexpr int kLdsVecBytes = kLdsBytes - kWaves * kScratch * 4;  // for staged vectors
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
+constexpr int kSegWeight = 12;            // default work of one segment, in entries
+constexpr int kChunkMid = 1;              // chunk flag: its first segment began in an earlier chunk
+constexpr int kChunkCont = 2;             // chunk flag: its last segment goes on past its end
 constexpr int kEntryPad = 64;             // entries of padding after idx and val (loads past the end)
+
+__host__ __device__ inline uint32_t lds_swizzle(uint32_t c) { return c ^ ((c >> 5) & 31u); }
 
 enum PassMode : int32_t {
     kModePlain = 0,     // R-hat read only: y = sum rhat x / (lambda + sum x^2)
@@ -81,17 +98,20 @@ struct PassArgs {
     const int32_t* wg_piece;    // [grid + 1] pieces of each workgroup
     const int32_t* piece_tile;  // [npieces] tile of each piece
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
-    const int32_t* piece_seg;   // [npieces * kWaves] segment starting each chunk
+    const int32_t* piece_seg;   // [npieces * kWaves] segment holding each chunk's first entry
+    const int32_t* chunk_flags; // [npieces * kWaves] kChunkMid | kChunkCont
     const float* x;             // [cols] gathered vector of the update
     const float* p;             // [S] own factor column, current feature, per segment
     const float* pp;            // [S] own factor column, previous feature (committed), per segment
     const float* q;             // [cols] other factor column, current feature
     const float* qq;            // [cols] other factor column, previous feature (committed)
     float* y;                   // [rows] coordinates (P == 1)
-    double2* part;              // [S] partial (num, den) per segment (P > 1)
+    double2* part;              // [S + 2 * chunks] partials: per segment (P > 1), then the
+                                // head and tail slot of every chunk
     double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
     int32_t rows, cols, T, P;
-    int32_t Ts;                 // LDS floats per staged vector slice (T + 1: a trailing zero)
+    int32_t Ts;                 // LDS floats per staged vector slice
+    int32_t pad;                // index held by padding entries (reads 0)
     int32_t nseg;               // S
     int32_t nseg_ne;            // segments with entries (P == 1: rows before the empty ones)
     int32_t vec_floats;         // LDS floats taken by staged vectors (scratch follows)
@@ -99,13 +119,18 @@ struct PassArgs {
     double lambda;
 };
 
+// Finishes rows from partial slots: row ids[i] (or i when ids is null) adds
+// part[srcs[src_ptr[i] .. src_ptr[i + 1])] in order.
 struct CombineArgs {
-    const int32_t* row_seg_ptr;  // [rows + 1]
-    const int32_t* row_segs;     // [S] segments of each row in tile order
+    const int32_t* ids;          // [n] rows, or null
+    const int32_t* src_ptr;      // [n + 1]
+    const int32_t* srcs;
+    const int32_t* seg_ptr;      // [n + 1] segments of each row (with yseg)
+    const int32_t* segs;
     const double2* part;
     float* y;
     float* yseg;                 // optional [S]: y spread over the row's segments
-    int32_t rows;
+    int32_t n;
     double lambda;
 };
 
@@ -115,6 +140,9 @@ struct Layout {
     int64_t npad = 0;                // entries including alignment padding
     int32_t gather = kGatherGlobal;
     int32_t T = 0, P = 1;
+    int32_t Ts = 0;                  // LDS floats per staged slice (swizzled range + zero)
+    int32_t pad = 0;                 // padding index: the zero word (staged) or cols (global)
+    bool swz = false;                // indices are swizzled LDS positions (staged layouts)
     bool idx16 = false;
     void* idx = nullptr;             // [npad + kEntryPad]
     float* val = nullptr;            // [npad + kEntryPad]
@@ -125,10 +153,17 @@ struct Layout {
     int32_t* piece_tile = nullptr;
     int64_t* piece_chunk = nullptr;
     int32_t* piece_seg = nullptr;
+    int32_t* chunk_flags = nullptr;
     int32_t npieces = 0;
-    int32_t* row_seg_ptr = nullptr;  // P > 1
-    int32_t* row_segs = nullptr;     // P > 1
-    double2* part = nullptr;         // P > 1
+    int32_t ncomb = 0;               // rows the combine finishes (P == 1: the cut ones)
+    int32_t* comb_rows = nullptr;    // P == 1: their ids
+    int32_t* src_ptr = nullptr;      // [ncomb + 1] partial slots of each combined row
+    int32_t* srcs = nullptr;
+    int64_t nsrc = 0;
+    int32_t* row_seg_ptr = nullptr;  // P > 1: segments of each row in tile order
+    int32_t* row_segs = nullptr;
+    double2* part = nullptr;         // [nslots]
+    int64_t nslots = 0;
     int64_t nseg = 0;
     int64_t nseg_ne = 0;
     int32_t grid = 0;                // persistent workgroups per pass
@@ -155,7 +190,7 @@ hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32
                            int32_t* ids, hipStream_t s);
 hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hipStream_t s);
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, const int32_t* seg_off, bool idx16,
+                              int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
                               void* idx, float* val, int32_t* pos, hipStream_t s);
 hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);

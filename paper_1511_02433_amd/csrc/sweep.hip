@@ -190,17 +190,10 @@ __device__ __forceinline__ float rhat(float v, float qv, float qqv, float pr, fl
     return v;
 }
 
-template <bool P1>
-__device__ __forceinline__ void emit(const PassArgs& a, int s, double num, double den) {
-    if constexpr (P1)
-        a.y[s] = coordinate(num, den, a.lambda);  // P == 1: segment s is row s
-    else
-        a.part[s] = make_double2(num, den);
-}
 
-// Copy the tile's slice of every gathered vector into LDS, each followed by a
-// zero (the target of padding entries).  Slots come in the order x, q, qq; x
-// shares q's slot when they are the same vector.
+// Copy the tile's slice of every gathered vector into LDS at the swizzled
+// positions, with a zero at the padding index.  Slots come in the order x, q,
+// qq; x shares q's slot when they are the same vector.
 template <int MODE>
 __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* lds, Gather& gx) {
     using N = Needs<MODE>;
@@ -232,16 +225,17 @@ __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* l
         for (int u = 0; u < kU; ++u) {
             const int i = i0 + u * kWG;
             if (i < len) {
-                if (N::x && !alias) sx[i] = vx[u];
-                if (N::q) sq[i] = vq[u];
-                if (N::qq) sqq[i] = vqq[u];
+                const uint32_t li = lds_swizzle((uint32_t)i);
+                if (N::x && !alias) sx[li] = vx[u];
+                if (N::q) sq[li] = vq[u];
+                if (N::qq) sqq[li] = vqq[u];
             }
         }
     }
     if (threadIdx.x == 0) {
-        if (N::x && !alias) sx[T] = 0.0f;
-        if (N::q) sq[T] = 0.0f;
-        if (N::qq) sqq[T] = 0.0f;
+        if (N::x && !alias) sx[a.pad] = 0.0f;
+        if (N::q) sq[a.pad] = 0.0f;
+        if (N::qq) sqq[a.pad] = 0.0f;
     }
     gx.lx = sx;
     gx.lq = sq;
@@ -302,7 +296,23 @@ struct Walk {
     int cid;      // segment left open by the previous window (-1: none), and its sums
     double cn, cd;
     double sse;
+    int mid;      // the chunk's first segment when it began in an earlier chunk, else -1
+    int head;     // the chunk's head partial slot (its tail slot follows)
 };
+
+// A segment's sums over this chunk: its coordinate (P == 1: segment s is row s)
+// or partial, or, for a segment that began in an earlier chunk, the chunk's
+// head partial.
+template <bool P1>
+__device__ __forceinline__ void emit(const PassArgs& a, const Walk& wk, int s, double num,
+                                     double den) {
+    if (s == wk.mid)
+        a.part[wk.head] = make_double2(num, den);
+    else if constexpr (P1)
+        a.y[s] = coordinate(num, den, a.lambda);
+    else
+        a.part[s] = make_double2(num, den);
+}
 
 // One window [elo, we) of a wave's chunk.  Lane l holds entries elo + l*kE ..
 // elo + l*kE + kE - 1; every window starts and ends on a multiple of kE, so a
@@ -392,7 +402,7 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
     } else {
         // A segment left open by the previous window that ended where this one starts.
         if (wk.cid >= 0 && wk.cid != wk.scur) {
-            if (lane == 0) emit<P1>(a, wk.cid, wk.cn, wk.cd);
+            if (lane == 0) emit<P1>(a, wk, wk.cid, wk.cn, wk.cd);
             wk.cid = -1;
         }
         // Scan keys: segment + 1 of the lane's first (hk) and last (tk) entry, 0 on
@@ -438,7 +448,7 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
                     ed += hd;
                 }
                 const int s = idb + __builtin_popcount(bits & ((2u << k) - 1u));
-                emit<P1>(a, s, en, ed);
+                emit<P1>(a, wk, s, en, ed);
                 rem &= rem - 1u;
             }
         }
@@ -459,10 +469,10 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
 // loop turn so the current and next window alternate between two register sets.
 template <int MODE, bool STAGED, bool IDX16, bool P1>
 __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, int64_t c0,
-                                          int64_t c1, int scur, int lane, float* spr,
-                                          float* sppr, uint32_t* bm, double& sse) {
+                                          int64_t c1, int scur, int flags, int gc, int lane,
+                                          float* spr, float* sppr, uint32_t* bm, double& sse) {
     const uint32_t le = (uint32_t)lane * kE;
-    Walk wk{c0, c1, scur, -1, 0.0, 0.0, sse};
+    Walk wk{c0, c1, scur, -1, 0.0, 0.0, sse, (flags & kChunkMid) ? scur : -1, a.nseg + 2 * gc};
     Win wa, wb;
     load_window<MODE, IDX16>(a, c0, c1, le, scur, lane, wa);
     while (true) {
@@ -472,7 +482,14 @@ __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, i
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
-        if (wk.cid >= 0 && lane == 0) emit<P1>(a, wk.cid, wk.cn, wk.cd);
+        // The last segment: finished, or going on past the chunk (a partial in the head
+        // slot when it is also the segment that began earlier, else in the tail slot).
+        if (wk.cid >= 0 && lane == 0) {
+            if (flags & kChunkCont)
+                a.part[wk.head + (wk.cid == wk.mid ? 0 : 1)] = make_double2(wk.cn, wk.cd);
+            else
+                emit<P1>(a, wk, wk.cid, wk.cn, wk.cd);
+        }
     }
     sse = wk.sse;
 }
@@ -519,9 +536,10 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
         }
         const int64_t c0 = a.piece_chunk[pc * (kWaves + 1) + wave];
         const int64_t c1 = a.piece_chunk[pc * (kWaves + 1) + wave + 1];
+        const int gc = pc * kWaves + wave;
         if (c0 < c1)
-            run_chunk<MODE, STAGED, IDX16, P1>(a, gx, c0, c1, a.piece_seg[pc * kWaves + wave],
-                                               lane, spr, sppr, bm, sse);
+            run_chunk<MODE, STAGED, IDX16, P1>(a, gx, c0, c1, a.piece_seg[gc], a.chunk_flags[gc],
+                                               gc, lane, spr, sppr, bm, sse);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -551,28 +569,28 @@ __global__ __launch_bounds__(kWG) void ccd_flush(PassArgs a) {
     pass_main<kModeFlush, STAGED, IDX16, P1>(a);
 }
 
-// Fixed-order combine of the per-tile partials of each row: one wave per row,
-// lane k takes the row's segments k, k + 64, ... in tile order, then a fixed
-// tree.  With yseg, the coordinate is also written to every segment of the row.
+// Fixed-order combine of a row's partials: one wave per row, lane k takes the
+// row's partial slots k, k + 64, ... in entry order, then a fixed tree.  With
+// yseg, the coordinate is also written to every segment of the row.
 __global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
     const int wave = (int)(threadIdx.x >> 6);
     const int lane = (int)(threadIdx.x & 63u);
-    const int r = blockIdx.x * 4 + wave;
-    if (r >= c.rows) return;
-    const int b = c.row_seg_ptr[r];
-    const int e = c.row_seg_ptr[r + 1];
+    const int i = blockIdx.x * 4 + wave;
+    if (i >= c.n) return;
+    const int b = c.src_ptr[i];
+    const int e = c.src_ptr[i + 1];
     double num = 0.0, den = 0.0;
     for (int k = b + lane; k < e; k += 64) {
-        const double2 pv = c.part[c.row_segs[k]];
+        const double2 pv = c.part[c.srcs[k]];
         num += pv.x;
         den += pv.y;
     }
     num = wave_sum(num);
     den = wave_sum(den);
     const float yr = coordinate(num, den, c.lambda);
-    if (lane == 0) c.y[r] = yr;
+    if (lane == 0) c.y[c.ids ? c.ids[i] : i] = yr;
     if (c.yseg)
-        for (int k = b + lane; k < e; k += 64) c.yseg[c.row_segs[k]] = yr;
+        for (int k = c.seg_ptr[i] + lane; k < c.seg_ptr[i + 1]; k += 64) c.yseg[c.segs[k]] = yr;
 }
 
 __global__ __launch_bounds__(256) void ccd_copy(const float* __restrict__ src,
@@ -661,6 +679,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.piece_tile = L.piece_tile;
     a.piece_chunk = L.piece_chunk;
     a.piece_seg = L.piece_seg;
+    a.chunk_flags = L.chunk_flags;
     a.x = x;
     a.p = p;
     a.pp = pp;
@@ -673,7 +692,8 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.cols = (int32_t)L.cols;
     a.T = L.T;
     a.P = L.P;
-    a.Ts = L.T + 1;
+    a.Ts = L.Ts;
+    a.pad = L.pad;
     a.nseg = (int32_t)L.nseg;
     a.nseg_ne = (int32_t)L.nseg_ne;
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
@@ -696,16 +716,20 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
 }
 
 hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda, hipStream_t s) {
-    if (L.P <= 1 || L.rows == 0) return hipSuccess;
+    if (L.ncomb == 0) return hipSuccess;
+    if (yseg && !L.row_seg_ptr) return hipErrorInvalidValue;
     CombineArgs c{};
-    c.row_seg_ptr = L.row_seg_ptr;
-    c.row_segs = L.row_segs;
+    c.ids = L.comb_rows;
+    c.src_ptr = L.src_ptr;
+    c.srcs = L.srcs;
+    c.seg_ptr = L.row_seg_ptr;
+    c.segs = L.row_segs;
     c.part = L.part;
     c.y = y;
     c.yseg = yseg;
-    c.rows = (int32_t)L.rows;
+    c.n = L.ncomb;
     c.lambda = lambda;
-    hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.rows + 3) / 4)), dim3(256), 0, s, c);
+    hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.ncomb + 3) / 4)), dim3(256), 0, s, c);
     return hipGetLastError();
 }
 

@@ -32,6 +32,7 @@ import hashlib
 import json
 import math
 import os
+import sys
 import time
 from dataclasses import dataclass, field
 
@@ -97,7 +98,7 @@ def _streams(config_id: int):
 
 def _log(msg: str, verbose: bool):
     if verbose:
-        print(f"[synth] {msg}", flush=True)
+        print(f"[synth] {msg}", file=sys.stderr, flush=True)
 
 
 def rank_curve(count: int, total: int, alpha: float, dmin: int, dmax: int) -> np.ndarray:
