@@ -60,17 +60,18 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
-    taken on the current kernel source; otherwise None."""
-    p = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+def stored_traffic(key: str, workload: str):
+    """HBM bytes per launch of kernel `key` ("ccd_pass/cols", ...) from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:
         t = json.load(f)
     if t.get("source_digest") != source_digest():
         return None
-    return t.get("bytes_per_launch")
+    k = t.get("kernels", {}).get(key)
+    return None if k is None else k.get("bytes_per_launch")
 
 
 def cpu_baseline(ds, k, inner, budget_s, threads):
@@ -144,25 +145,9 @@ def main():
     info = g.info()
     log(f"device build {info['build_us'] / 1e3:.1f} ms; schedule {info}")
 
-    for _ in range(args.warmup):
-        g.run(1, inner)
-    torch.cuda.synchronize()
-
-    def timed(steps, prof):
-        g.profile(prof)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(steps):
-            g.run(1, inner)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3 / steps
-
-    # The timed region: exactly `steps` steps, kernel events on the library's stream.
-    prof = not args.no_prof
-    ms = timed(args.steps, prof)
-    kinds = {}
-    per_layout = {}
-    if prof:
+    def read_kernels():
+        """Per-kernel and per-(kernel, residual copy) timings collected since profile()."""
+        kinds, per_layout = {}, {}
         for kind, name in KERNEL_NAMES.items():
             n, tot, b = g.profile_read(kind)
             if n:
@@ -172,31 +157,76 @@ def main():
                 n2, t2, b2 = g.profile_read(kind, lay)
                 if n2:
                     per_layout[f"{name}/{lname}"] = {
-                        "kernel": kernel_symbol(kind, info, lay), "launches": n2,
-                        "mean_us": round(t2 / n2 * 1e3, 3), "total_ms": round(t2, 4),
-                        "algo_bytes_per_launch": b2 / n2,
+                        "kernel": kernel_symbol(kind, info, lay), "kind": kind, "layout": lay,
+                        "launches": n2, "mean_us": round(t2 / n2 * 1e3, 3),
+                        "total_ms": round(t2, 4), "algo_bytes_per_launch": b2 / n2,
                         "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
-    g.profile(False)
-    ms_plain = timed(max(2, args.steps // 2), False) if prof else ms
+        return kinds, per_layout
+
+    def timed(steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.run(1, inner)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+
+    # Warmup.  The last warmup step times every kernel, which names the dominant one.
+    kinds, per_layout = {}, {}
+    kinds_steps = 1
+    for i in range(args.warmup):
+        last = i + 1 == args.warmup and not args.no_prof
+        if last:
+            g.profile(True)
+        g.run(1, inner)
+        if last:
+            torch.cuda.synchronize()
+            kinds, per_layout = read_kernels()
+    torch.cuda.synchronize()
+    dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"]) if per_layout else None
+
+    # The timed region: exactly `steps` steps.  HIP events on the library's stream
+    # bracket every launch of the dominant kernel (of every kernel without warmup).
+    prof = not args.no_prof
+    if prof:
+        g.profile(True)
+        if dom:
+            g.profile_only(per_layout[dom]["kind"], per_layout[dom]["layout"])
+    ms = timed(args.steps)
+    if prof:
+        if dom:
+            d = per_layout[dom]
+            n, tot, b = g.profile_read(d["kind"], d["layout"])
+            live = {"launches": n, "mean_us": round(tot / n * 1e3, 3), "total_ms": round(tot, 4),
+                    "algo_bytes_per_launch": b / n}
+        else:
+            kinds, per_layout = read_kernels()
+            kinds_steps = args.steps
+            dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"])
+            live = per_layout[dom]
+        g.profile_only(-1, -1)
+        g.profile(False)
+    ms_plain = timed(max(2, args.steps // 2)) if prof else ms
     visits = 2.0 * inner * k * w.nnz
     value = visits / (ms * 1e-3) / 1e9
-    log(f"{ms:.3f} ms/step with kernel events, {ms_plain:.3f} ms/step without; {value:.1f} Gnnz/s")
+    log(f"{ms:.3f} ms/step (events on the dominant kernel), {ms_plain:.3f} ms/step without; "
+        f"{value:.1f} Gnnz/s")
 
     # Roofline of the dominant kernel: the (kernel, residual copy) pair with the most
-    # device time per step.
+    # device time per step, timed live in the timed region.
     roofline = None
-    if per_layout:
-        dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"])
+    if prof and dom:
         d = per_layout[dom]
-        achieved = d["algo_bytes_per_launch"] / (d["mean_us"] * 1e-6) / 1e9
+        achieved = live["algo_bytes_per_launch"] / (live["mean_us"] * 1e-6) / 1e9
         roofline = {"kernel": d["kernel"], "layout": dom.split("/")[1], "bound": "hbm",
                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": stored_traffic(dom.replace("/", "_"), w.name),
-                    "mean_us": d["mean_us"], "algo_bytes_per_launch": d["algo_bytes_per_launch"]}
+                    "traffic": stored_traffic(dom, w.name), "mean_us": live["mean_us"],
+                    "launches": live["launches"],
+                    "algo_bytes_per_launch": live["algo_bytes_per_launch"]}
     train_rmse = g.train_rmse()
     test_rmse = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
-    model_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / args.steps \
+    model_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / kinds_steps \
         if kinds else None
     g.close()
 
@@ -227,6 +257,8 @@ def main():
         "model_bytes_per_step": model_bytes,
         "model_gbs": round(model_bytes / (ms * 1e-3) / 1e9, 1) if model_bytes else None,
         "ms_per_step_without_kernel_events": round(ms_plain, 4),
+        "kernels_note": ("per-kernel timings: the last warmup step" if kinds_steps == 1
+                         else "per-kernel timings: the timed steps"),
         "kernels": kinds,
         "kernels_by_layout": per_layout,
         "train_rmse": train_rmse,

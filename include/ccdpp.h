@@ -68,9 +68,10 @@ enum ccdpp_status {
  *   out     : receives the handle
  * Validation of sizes, ranges and values happens on the host before any HIP
  * call.  Returns EDUP if a position repeats, ENOMEM or EDEVICE on device
- * failure.  The device layout (row and column compressed copies of the
- * residual, the map between them and the degree-binned schedule) is built on
- * the device during this call.
+ * failure.  The device layout (user-major and item-major copies of the
+ * residual, tiled so that the gathered vectors fit in LDS, the map between
+ * them and the equal-work schedule of persistent workgroups) is built on the
+ * device during this call.
  */
 int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
                  const int32_t *row, const int32_t *col, const float *val,
@@ -85,7 +86,9 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 global memory; 2 stage them in LDS, cut into tiles of
  *                 tile_width columns when they do not fit
  *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
- *                 163840 / (4 * v) where v = 2 for index 0 and 3 for index 1
+ *                 153600 / (4 * v) - 64, rounded down to a multiple of 64,
+ *                 where v = 2 for index 0 and 3 for index 1 (the vectors the
+ *                 first pass of a feature stages)
  *   workgroups  : persistent workgroups per pass (0: one per compute unit)
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 12;
@@ -165,6 +168,10 @@ enum ccdpp_kernel_kind {
     CCDPP_K_COUNT = 5
 };
 int ccdpp_profile(ccdpp_t *h, int32_t enable);
+/* Restrict kernel timing to launches of one kind (CCDPP_K_*) on one residual
+ * copy (0 or 1); -1 for either means all.  Fewer events disturb the stream
+ * less.  The selection persists until changed; the default is all. */
+int ccdpp_profile_only(ccdpp_t *h, int32_t kind, int32_t layout);
 int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launches,
                        double *total_ms, double *algo_bytes);
 

@@ -74,6 +74,7 @@ struct ccdpp {
     std::vector<void*> allocs;
     // kernel timing
     bool prof = false;
+    int32_t prof_kind = -1, prof_layout = -1;  // restrict timing to one kind / copy (-1: all)
     std::vector<ProfEvent> prof_pending;
     std::vector<hipEvent_t> event_pool;
     int64_t prof_launch[CCDPP_K_COUNT][2] = {};
@@ -650,13 +651,14 @@ struct Timed {
     hipEvent_t a = nullptr;
     Timed(ccdpp* h_, int kind_, int layout_, double bytes_)
         : h(h_), kind(kind_), layout(layout_), bytes(bytes_) {
-        if (h->prof) {
+        if (h->prof && (h->prof_kind < 0 || h->prof_kind == kind) &&
+            (h->prof_layout < 0 || h->prof_layout == layout)) {
             a = take_event(h);
             if (a) (void)hipEventRecord(a, h->stream);
         }
     }
     void done() {
-        if (h->prof && a) {
+        if (a) {
             hipEvent_t b = take_event(h);
             if (b) {
                 (void)hipEventRecord(b, h->stream);
@@ -752,6 +754,7 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
             if (opts->tile_width[i] < 0) return fail(nullptr, CCDPP_EINVAL, "tile_width < 0");
         }
         if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
+        if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
     }
     for (int64_t e = 0; e < nnz; ++e) {
         if (row[e] < 0 || row[e] >= m)
@@ -1006,6 +1009,15 @@ int ccdpp_profile(ccdpp_t* h, int32_t enable) {
             h->prof_ms[i][l] = 0.0;
             h->prof_bytes[i][l] = 0.0;
         }
+    return CCDPP_OK;
+}
+
+int ccdpp_profile_only(ccdpp_t* h, int32_t kind, int32_t layout) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (kind < -1 || kind >= CCDPP_K_COUNT) return fail(h, CCDPP_EINVAL, "bad kernel kind");
+    if (layout < -1 || layout > 1) return fail(h, CCDPP_EINVAL, "bad layout");
+    h->prof_kind = kind;
+    h->prof_layout = layout;
     return CCDPP_OK;
 }
 

@@ -1,0 +1,92 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/ccdpp.h declares, and rejects bad arguments on the host, before any
+HIP call, with the documented status codes."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import paper_1511_02433_amd.ccdpp as C
+
+
+def _lib_or_skip():
+    try:
+        return C.lib()
+    except RuntimeError as e:  # not built in this checkout
+        pytest.skip(str(e))
+
+
+def test_every_declared_function_is_exported():
+    L = _lib_or_skip()
+    names = C.declared_symbols()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(L, name), name
+    # and the binding knows a signature for each of them
+    for name in names:
+        assert getattr(L, name).argtypes is not None or name == "ccdpp_destroy", name
+
+
+def _create(m=10, n=8, k=2, lam=0.1, row=(0, 1), col=(0, 1), val=(1.0, 2.0), opts=None):
+    return C.ccdpp_create_ex(m, n, k, lam, np.array(row, np.int32), np.array(col, np.int32),
+                             np.array(val, np.float32), 0, opts)
+
+
+@pytest.mark.parametrize("kw, msg", [
+    (dict(m=0), "m and n"),
+    (dict(n=0), "m and n"),
+    (dict(m=1 << 30), "m and n"),
+    (dict(k=0), "k must be"),
+    (dict(lam=-1.0), "lambda"),
+    (dict(lam=float("nan")), "lambda"),
+    (dict(row=(0, 10)), "out of range"),
+    (dict(col=(0, -1)), "out of range"),
+    (dict(val=(1.0, float("inf"))), "not finite"),
+])
+def test_create_rejects_bad_arguments_on_the_host(kw, msg):
+    _lib_or_skip()
+    with pytest.raises(C.CCDPPError) as ei:
+        _create(**kw)
+    assert ei.value.code == C.CCDPP_EINVAL
+    assert msg in str(ei.value)
+
+
+def test_create_rejects_bad_options():
+    _lib_or_skip()
+    with pytest.raises(C.CCDPPError) as ei:
+        _create(opts=C.make_options(gather_mode=(7, 0)))
+    assert ei.value.code == C.CCDPP_EINVAL
+
+
+def test_null_pointers_and_handles():
+    L = _lib_or_skip()
+    out = ctypes.c_void_p()
+    # NULL out-parameter
+    rc = L.ccdpp_create(4, 4, 1, 0.1, 0, None, None, None, 0, None)
+    assert rc == C.CCDPP_EINVAL
+    assert L.ccdpp_last_error(None)  # the failed create left a message
+    # nnz > 0 with NULL arrays
+    rc = L.ccdpp_create(4, 4, 1, 0.1, 3, None, None, None, 0, ctypes.byref(out))
+    assert rc == C.CCDPP_EINVAL
+    # every call on a NULL handle answers ESTATE; destroy accepts NULL
+    assert L.ccdpp_run(None, 1, 1) == C.CCDPP_ESTATE
+    assert L.ccdpp_get_factors(None, None, None) == C.CCDPP_ESTATE
+    assert L.ccdpp_set_factors(None, None, None) == C.CCDPP_ESTATE
+    assert L.ccdpp_train_rmse(None, None) == C.CCDPP_ESTATE
+    assert L.ccdpp_check_consistency(None, None) == C.CCDPP_ESTATE
+    assert L.ccdpp_profile(None, 1) == C.CCDPP_ESTATE
+    assert L.ccdpp_profile_only(None, 0, 0) == C.CCDPP_ESTATE
+    buf = (ctypes.c_int64 * 4)()
+    assert L.ccdpp_info(None, buf, 4) == C.CCDPP_ESTATE
+    L.ccdpp_destroy(None)
+
+
+def test_without_a_device_create_reports_edevice():
+    """On a machine without a GPU, a valid problem fails with EDEVICE (no fallback)."""
+    _lib_or_skip()
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(C.CCDPPError) as ei:
+        _create()
+    assert ei.value.code == C.CCDPP_EDEVICE
