@@ -89,7 +89,7 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 153600 / (4 * v) - 64, rounded down to a multiple of 64,
  *                 where v = 2 for index 0 and 3 for index 1 (the vectors the
  *                 first pass of a feature stages)
- *   workgroups  : persistent workgroups per pass (0: one per compute unit)
+ *   workgroups  : persistent workgroups per pass (0: two per compute unit)
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 12;
  *                 -1: shares by entries alone)

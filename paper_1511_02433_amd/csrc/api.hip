@@ -314,7 +314,10 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // in every chunk it meets, a partial (num, den) in a slot of its own (the chunk's
     // head slot if the segment began before the chunk, else its tail slot), and the
     // combine adds a row's partials in entry order.
-    int64_t G = opt && opt->workgroups > 0 ? opt->workgroups : (int64_t)h->cus;
+    // Two shares per compute unit: a workgroup holds a whole CU's LDS, so the second
+    // round of workgroups goes to whichever CUs finish first, which evens out the
+    // remaining differences in speed between shares.
+    int64_t G = opt && opt->workgroups > 0 ? opt->workgroups : 2 * (int64_t)h->cus;
     if (!(opt && opt->workgroups > 0))
         G = std::max<int64_t>(1, std::min<int64_t>(G, (NP + kWaves * kWin - 1) / (kWaves * kWin)));
     const int64_t wseg = !opt || opt->seg_weight == 0 ? kSegWeight

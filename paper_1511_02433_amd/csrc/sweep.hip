@@ -382,17 +382,25 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
         }
     }
     if constexpr (N::store) {
-        if (lv) {
-            f32x4 w0, w1;
+        // Write R-hat back so that each store instruction covers contiguous memory:
+        // lane l writes entries 4l .. 4l + 3 of the window, then 256 + 4l .. 256 + 4l + 3,
+        // which are half (l & 1) of lane l / 2 and of lane 32 + l / 2.  Stores of half
+        // lines from strided lanes cost far more HBM time than whole lines.
+        const int srcA = (lane >> 1) << 2, srcB = (32 + (lane >> 1)) << 2;
+        const bool odd = lane & 1;
+        f32x4 w0, w1;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                w0[k] = r[k];
-                w1[k] = r[4 + k];
-            }
-            f32x4* wp = reinterpret_cast<f32x4*>(a.val + b + le);
-            __builtin_nontemporal_store(w0, wp);
-            __builtin_nontemporal_store(w1, wp + 1);
+        for (int k = 0; k < 4; ++k) {
+            const int lo = __builtin_bit_cast(int, r[k]), hi = __builtin_bit_cast(int, r[4 + k]);
+            const int a0 = __builtin_amdgcn_ds_bpermute(srcA, lo), a1 = __builtin_amdgcn_ds_bpermute(srcA, hi);
+            const int b0 = __builtin_amdgcn_ds_bpermute(srcB, lo), b1 = __builtin_amdgcn_ds_bpermute(srcB, hi);
+            w0[k] = __builtin_bit_cast(float, odd ? a1 : a0);
+            w1[k] = __builtin_bit_cast(float, odd ? b1 : b0);
         }
+        const int pieces = 2 * nl;  // 4-entry pieces in this window
+        float* wp = a.val + b + 4 * lane;
+        if (lane < pieces) __builtin_nontemporal_store(w0, reinterpret_cast<f32x4*>(wp));
+        if (lane + 64 < pieces) __builtin_nontemporal_store(w1, reinterpret_cast<f32x4*>(wp + 256));
     }
     if constexpr (MODE == kModeFlush) {
         float s2 = 0.0f;
