@@ -1,0 +1,121 @@
+"""GPU path against the fp64 oracle at the benchmark workloads' full sizes.
+
+Every matrix here is the full synthetic workload, created with the default
+layout options, which is the configuration bench.py times.  The oracle runs the
+same iterations on the host (OpenMP), so W, H and the RMSEs are compared in
+full rather than on samples:
+
+* after one outer iteration, W and H within 1e-3 (per-feature scaled max
+  relative error);
+* after the workload's full schedule, train and test RMSE within 1e-4;
+* the two residual copies agree bit for bit.
+
+The rank sweep runs the large matrix at k = 10 and k = 100 (one outer
+iteration).  Each test prints what it runs before it starts.
+"""
+import os
+import time
+
+import numpy as np
+import pytest
+
+from oracle import Oracle
+from paper_1511_02433_amd import synth
+from paper_1511_02433_amd.ccdpp import CCDPP
+from gpu_util import colscaled_max_rel_err
+
+pytestmark = pytest.mark.gpu
+
+W_TOL = 1e-3
+RMSE_TOL = 1e-4
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def _say(msg):
+    print(f"[fullsize] {msg}", flush=True)
+
+
+def _gpu(ds, k):
+    w = ds.workload
+    g = CCDPP(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val)
+    g.set_factors(np.zeros((w.m, k), np.float32), ds.h0(k))
+    return g
+
+
+def _oracle(ds, k):
+    w = ds.workload
+    return Oracle(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val, ds.h0(k), threads=THREADS)
+
+
+def _one_outer(name, k=None):
+    ds = synth.load(name)
+    w = ds.workload
+    k = k or w.k
+    _say(f"{name}: {w.m} x {w.n}, nnz {w.nnz}, k {k}, one outer iteration x {w.inner} inner")
+    g = _gpu(ds, k)
+    g.run(1, w.inner)
+    Wg, Hg = g.factors()
+    assert g.check_consistency() == 0
+    g.close()
+    t0 = time.perf_counter()
+    o = _oracle(ds, k)
+    o.run(1, w.inner)
+    Wo, Ho = o.factors()
+    o.close()
+    ew, eh = colscaled_max_rel_err(Wg, Wo), colscaled_max_rel_err(Hg, Ho)
+    _say(f"{name}: oracle {time.perf_counter() - t0:.1f} s; W err {ew:.2e}, H err {eh:.2e}")
+    assert ew <= W_TOL and eh <= W_TOL
+
+
+def _full_run(name):
+    ds = synth.load(name)
+    w = ds.workload
+    _say(f"{name}: full schedule {w.outer} x {w.inner}, k {w.k}")
+    g = _gpu(ds, w.k)
+    g.run(w.outer, w.inner)
+    tr_g = g.train_rmse()
+    te_g = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
+    assert g.check_consistency() == 0
+    g.close()
+    t0 = time.perf_counter()
+    o = _oracle(ds, w.k)
+    o.run(w.outer, w.inner)
+    tr_o = o.train_rmse()
+    te_o = o.test_rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
+    o.close()
+    _say(f"{name}: oracle {time.perf_counter() - t0:.1f} s; train RMSE gpu {tr_g:.7f} "
+         f"oracle {tr_o:.7f}; test RMSE gpu {te_g} oracle {te_o}")
+    assert abs(tr_g - tr_o) <= RMSE_TOL
+    if te_g is not None:
+        assert abs(te_g - te_o) <= RMSE_TOL
+
+
+@pytest.mark.timeout(600)
+def test_medium_one_outer_and_full_run():
+    _one_outer("medium")
+    _full_run("medium")
+
+
+@pytest.mark.timeout(600)
+def test_large_one_outer():
+    _one_outer("large")
+
+
+@pytest.mark.timeout(900)
+def test_large_full_run():
+    _full_run("large")
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("k", [10, 100])
+def test_rank_sweep_one_outer(k):
+    _one_outer("large", k)
+
+
+@pytest.mark.timeout(1100)
+@pytest.mark.skipif(os.environ.get("CCDPP_VLARGE_TEST") != "1",
+                    reason="drawing the 252.8M-entry very large matrix takes about 9 minutes on "
+                           "the host; set CCDPP_VLARGE_TEST=1 to run it")
+def test_vlarge_one_outer():
+    synth.load("vlarge", verbose=True)  # progress lines while the matrix is drawn
+    _one_outer("vlarge")
