@@ -67,7 +67,8 @@ constexpr int kWG = 1024;                 // threads per persistent workgroup
 constexpr int kWaves = kWG / 64;          // 16 waves
 constexpr int kE = 8;                     // entries per lane per window
 constexpr int kWin = 64 * kE;             // entries per window
-constexpr int kScratch = 160;             // LDS words of per-wave scratch
+constexpr int kScratch = 160;             // LDS words of per-wave scratch, at most
+
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
 constexpr int kLdsVecBytes = kLdsBytes - kWaves * kScratch * 4;  // for staged vectors
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
@@ -84,6 +85,14 @@ enum PassMode : int32_t {
     kModeSubAdd = 2,    // rhat = fma(p, q, fma(-pp, qq, val)); store; then as plain
     kModeFlush = 3,     // r = fma(-pp, qq, val); store; per-wave sum of r^2
 };
+
+// Per-wave scratch of a pass: the window's segment-start bitmap, then 64 slots
+// for each per-row scalar the mode reads (p for the fused modes, pp for the
+// subtracting modes, in that order).
+constexpr int scratch_words(int mode) {
+    return kWin / 32 + 64 * ((mode == kModeAdd || mode == kModeSubAdd) +
+                             (mode == kModeSubAdd || mode == kModeFlush));
+}
 
 enum GatherMode : int32_t {
     kGatherAuto = 0,

@@ -519,10 +519,11 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
     }
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = (int)(threadIdx.x & 63u);
-    uint32_t* scr = reinterpret_cast<uint32_t*>(lds + a.vec_floats) + wave * kScratch;
-    uint32_t* bm = scr;                                             // kWin / 32 words
-    float* spr = reinterpret_cast<float*>(scr + kWin / 32);        // 64 row scalars p
-    float* sppr = reinterpret_cast<float*>(scr + kWin / 32 + 64);  // 64 row scalars pp
+    uint32_t* scr = reinterpret_cast<uint32_t*>(lds + a.vec_floats) + wave * scratch_words(MODE);
+    // Scratch layout (scratch_words): the bitmap, then the slots of p, then of pp.
+    uint32_t* bm = scr;                                              // kWin / 32 words
+    float* spr = reinterpret_cast<float*>(scr + kWin / 32);         // 64 row scalars p
+    float* sppr = reinterpret_cast<float*>(scr + kWin / 32 + (N::p ? 64 : 0));  // 64 pp
 
     if constexpr (MODE != kModeFlush && P1) {
         // The rows after the last non-empty one have no entries: coordinate 0.
@@ -707,7 +708,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
     a.lambda = lambda;
     a.vec_floats = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
-    const size_t lds = (size_t)a.vec_floats * sizeof(float) + (size_t)kWaves * kScratch * 4;
+    const size_t lds = (size_t)a.vec_floats * sizeof(float) + (size_t)kWaves * scratch_words(mode) * 4;
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     const dim3 grid(L.grid);
     if (staged) {
