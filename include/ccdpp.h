@@ -155,9 +155,8 @@ int ccdpp_set_stream(ccdpp_t *h, void *hip_stream);
  * (CCDPP_K_*) and per residual copy (layout 0: row-compressed, the u-passes of
  * eq. 15; layout 1: column-compressed, the v-passes of eq. 16; -1: both):
  * launch count, summed device time in milliseconds, and the algorithmic bytes
- * those launches had to move (index and value arrays, residual writes, row
- * pointers, per-row scalars and outputs, and one read of each gathered
- * vector).  Enabling or disabling clears the counters. */
+ * those launches had to move (index and value arrays, residual writes,
+ * per-row scalars and outputs, and one read of each gathered vector).  Enabling or disabling clears the counters. */
 enum ccdpp_kernel_kind {
     CCDPP_K_PASS_FUSED = 0,  /* first u- or v-pass of a feature: eq. 18 of the previous
                                 feature, eq. 13, then eq. 15 or eq. 16 */

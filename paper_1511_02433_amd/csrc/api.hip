@@ -252,7 +252,8 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     L.swz = lds;
     L.pad = lds ? (int32_t)((T + 31) / 32 * 32) : (int32_t)T;
     L.Ts = lds ? L.pad + 32 : (int32_t)T + 1;
-    L.idx16 = L.pad < 65536;  // every index, the padding one included, fits 16 bits
+    // Every index, the padding one included, fits 15 bits (the 16th is the start bit).
+    L.idx16 = L.pad < (int32_t)IndexBits<uint16_t>::start;
 
     // Segments.  P == 1: segment r is row r (rows are relabelled by decreasing
     // length, so the empty ones come last).  P > 1: the non-empty rows of each
@@ -282,8 +283,9 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     while (S_ne > 0 && seg_start[S_ne] == seg_start[S_ne - 1]) --S_ne;
     L.nseg_ne = S_ne;
 
-    // Alignment padding: each tile's entries start at a multiple of kE; the entries
-    // skipped over are padding at the end of the previous tile's last segment.
+    // Alignment padding: every segment starts at a multiple of kE, every tile at a
+    // multiple of kAlign; the entries skipped over are padding at the end of the
+    // previous segment.
     const int64_t S_work = P == 1 ? S_ne : S;  // segments that hold entries
     std::vector<int32_t> seg_off((size_t)S, 0);
     std::vector<int64_t> pstart((size_t)S + 1);
@@ -292,11 +294,14 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         for (int64_t p = 0; p < P; ++p) tile_first[tile_seg[p]] = 1;
         int64_t off = 0;
         for (int64_t sg = 0; sg < S_work; ++sg) {
-            if (tile_first[sg]) off += (kE - (seg_start[sg] + off) % kE) % kE;
+            const int64_t al = tile_first[sg] ? kAlign : kE;
+            off += (al - (seg_start[sg] + off) % al) % al;
+            if (seg_start[sg] + off > (int64_t)INT32_MAX - kEntryPad)
+                return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
             seg_off[sg] = (int32_t)off;
             pstart[sg] = seg_start[sg] + off;
         }
-        const int64_t NP = (N + off + kE - 1) / kE * kE;
+        const int64_t NP = (N + off + kAlign - 1) / kAlign * kAlign;
         if (NP > (int64_t)INT32_MAX - kEntryPad)
             return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
         for (int64_t sg = S_work; sg <= S; ++sg) pstart[sg] = NP;
@@ -305,7 +310,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     const int64_t NP = L.npad;
     seg_start.swap(pstart);  // from here on, segment starts are padded positions
 
-    // Persistent workgroups own equal shares of the work, cut at multiples of kE; a
+    // Persistent workgroups own equal shares of the work, cut at multiples of kAlign; a
     // share is processed as one piece per tile it touches, and every piece is cut
     // into kWaves chunks of equal work, one per wave.  The work of a range is its
     // entries plus seg_weight per segment starting in it (a segment's emission, and
@@ -322,7 +327,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         G = std::max<int64_t>(1, std::min<int64_t>(G, (NP + kWaves * kWin - 1) / (kWaves * kWin)));
     const int64_t wseg = !opt || opt->seg_weight == 0 ? kSegWeight
                          : std::max<int64_t>(0, opt->seg_weight);
-    auto up8 = [](int64_t v) { return (v + kE - 1) / kE * kE; };
+    auto upa = [](int64_t v) { return (v + kAlign - 1) / kAlign * kAlign; };
     // Last segment of tile p starting at or before position e.
     auto seg_of = [&](int64_t p, int64_t e) -> int64_t {
         return std::upper_bound(seg_start.begin() + tile_seg[p], seg_start.begin() + tile_seg[p + 1],
@@ -349,7 +354,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     std::vector<std::vector<int32_t>> src_of((size_t)S);  // partial slots of each cut segment
     std::vector<int64_t> gb((size_t)G + 1);
     for (int64_t g = 0; g <= G; ++g)
-        gb[g] = g == 0 ? 0 : g == G ? NP : std::min(NP, up8(pos_at(work_total / G * g +
+        gb[g] = g == 0 ? 0 : g == G ? NP : std::min(NP, upa(pos_at(work_total / G * g +
                                                                     work_total % G * g / G)));
     for (int64_t g = 0; g < G; ++g) {
         const int64_t lo = gb[g], hi = std::max(gb[g], gb[g + 1]);
@@ -362,7 +367,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             const int64_t w0 = work_at(a0), w1 = work_at(a1);
             for (int w = 0; w <= kWaves; ++w)
                 piece_chunk.push_back(w == 0 ? a0 : w == kWaves ? a1
-                                      : std::min(a1, std::max(a0, up8(pos_at(w0 + (w1 - w0) * w / kWaves)))));
+                                      : std::min(a1, std::max(a0, upa(pos_at(w0 + (w1 - w0) * w / kWaves)))));
             for (int w = 0; w < kWaves; ++w) {
                 const int64_t c0 = piece_chunk[pc * (kWaves + 1) + w];
                 const int64_t c1 = piece_chunk[pc * (kWaves + 1) + w + 1];
@@ -688,12 +693,12 @@ void collect_profile(ccdpp* h) {
 }
 
 // Algorithmic bytes of one pass over layout L (see ccdpp_profile_read): index and
-// value arrays, residual write-back, segment table, per-segment row scalars,
-// outputs, and every gathered vector read once.
+// value arrays, residual write-back, per-segment row scalars, outputs, and every
+// gathered vector read once.
 double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors) {
     using namespace ccdk;
     const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
-    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz + 8.0 * S;
+    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz;
     if (mode != kModePlain) b += 4.0 * nnz;
     if (mode != kModeFlush) b += L.P == 1 ? 4.0 * S : 16.0 * S;
     if (mode == kModeAdd || mode == kModeSubAdd) b += 4.0 * S;

@@ -76,7 +76,8 @@ __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* 
         const uint64_t key = keys[q];
         const int64_t p = q + seg_off[key >> cbits];
         const uint32_t c = (uint32_t)(key & mask);
-        idx[p] = (I)(swz ? lds_swizzle(c) : c);
+        const bool first = q == 0 || (keys[q - 1] >> cbits) != (key >> cbits);
+        idx[p] = (I)((swz ? lds_swizzle(c) : c) | (first ? IndexBits<I>::start : 0u));
         val[p] = val_in[perm[q]];
         pos[q] = (int32_t)p;
     }
@@ -153,7 +154,7 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
             if (tile_seg[mid] <= lo) plo = mid; else phi = mid;
         }
         const int64_t i = seg_row[lo];
-        const uint32_t c = (uint32_t)idx[q];
+        const uint32_t c = (uint32_t)idx[q] & IndexBits<I>::mask;
         const int64_t j = (int64_t)plo * T + (int64_t)(swz ? lds_swizzle(c) : c);
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)

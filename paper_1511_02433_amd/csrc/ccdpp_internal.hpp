@@ -42,9 +42,11 @@ namespace ccdk {
 // chunks, and with them every reduction order, are fixed at build time, so
 // results are identical run to run.
 //
-// Every tile, and so every piece and chunk, starts at a multiple of kE
-// entries: the build inserts up to kE - 1 padding entries at the end of each
-// tile.  A padding entry holds value 0 and an index that reads 0 (a zero word
+// Every segment starts at a multiple of kE entries, and every tile, workgroup
+// share and chunk at a multiple of kAlign, so that a window's loads cover whole
+// cache lines: the build inserts padding entries after a segment up to the next
+// multiple of kE (of kAlign before a new tile), and cuts shares and chunks at
+// multiples of kAlign.  A padding entry holds value 0 and an index that reads 0 (a zero word
 // after each staged slice in LDS, or a position past the vector in global
 // mode, where the bounded buffer load returns 0), so it adds exactly 0 to
 // every sum and stays 0 under every residual update.
@@ -67,10 +69,10 @@ constexpr int kWG = 1024;                 // threads per persistent workgroup
 constexpr int kWaves = kWG / 64;          // 16 waves
 constexpr int kE = 8;                     // entries per lane per window
 constexpr int kWin = 64 * kE;             // entries per window
-constexpr int kScratch = 160;             // LDS words of per-wave scratch, at most
+constexpr int kAlign = 64;                // tile, share and chunk starts: 256 B of values, 128 B of indices
 
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
-constexpr int kLdsVecBytes = kLdsBytes - kWaves * kScratch * 4;  // for staged vectors
+constexpr int kLdsVecBytes = kLdsBytes;   // all of it holds staged vectors
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
 constexpr int kSegWeight = 12;            // default work of one segment, in entries
 constexpr int kChunkMid = 1;              // chunk flag: its first segment began in an earlier chunk
@@ -86,13 +88,19 @@ enum PassMode : int32_t {
     kModeFlush = 3,     // r = fma(-pp, qq, val); store; per-wave sum of r^2
 };
 
-// Per-wave scratch of a pass: the window's segment-start bitmap, then 64 slots
-// for each per-row scalar the mode reads (p for the fused modes, pp for the
-// subtracting modes, in that order).
-constexpr int scratch_words(int mode) {
-    return kWin / 32 + 64 * ((mode == kModeAdd || mode == kModeSubAdd) +
-                             (mode == kModeSubAdd || mode == kModeFlush));
-}
+// Segments are aligned to lanes: every segment starts at a multiple of kE, the
+// entries between its last entry and the next multiple of kE are padding, and
+// the index of a segment's first entry carries a start bit (the top bit of the
+// index word; 16-bit indices are therefore below 0x8000).  A lane's kE entries
+// thus always belong to one segment, and the lane learns whether that segment
+// starts with it from its own first index.
+template <class I> struct IndexBits;
+template <> struct IndexBits<uint16_t> {
+    static constexpr uint32_t start = 0x8000u, mask = 0x7FFFu;
+};
+template <> struct IndexBits<int32_t> {
+    static constexpr uint32_t start = 0x80000000u, mask = 0x7FFFFFFFu;
+};
 
 enum GatherMode : int32_t {
     kGatherAuto = 0,
@@ -103,7 +111,6 @@ enum GatherMode : int32_t {
 struct PassArgs {
     const void* idx;            // [npad] uint16 or int32 tile-local column
     float* val;                 // [npad] residual / R-hat
-    const int64_t* seg_start;   // [S + 1]
     const int32_t* wg_piece;    // [grid + 1] pieces of each workgroup
     const int32_t* piece_tile;  // [npieces] tile of each piece
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
@@ -123,7 +130,7 @@ struct PassArgs {
     int32_t pad;                // index held by padding entries (reads 0)
     int32_t nseg;               // S
     int32_t nseg_ne;            // segments with entries (P == 1: rows before the empty ones)
-    int32_t vec_floats;         // LDS floats taken by staged vectors (scratch follows)
+    int32_t vec_floats;         // LDS floats taken by staged vectors
     int32_t x_is_q;             // x and q are the same vector (staged once)
     double lambda;
 };

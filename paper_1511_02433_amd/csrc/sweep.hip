@@ -24,6 +24,8 @@
 // identical run to run.  The coordinate num / (lambda + den) is an IEEE fp64
 // division rounded once to fp32; a coordinate whose denominator is exactly zero
 // (lambda = 0 and an empty row) is set to zero.
+#include <type_traits>
+
 #include "ccdpp_internal.hpp"
 
 namespace ccdk {
@@ -50,7 +52,6 @@ constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0
 constexpr int kBcast15 = 0x142;   // lane 15 of each row to the next row
 constexpr int kBcast31 = 0x143;   // lane 31 to rows 2 and 3
 constexpr int kWaveShr1 = 0x138;  // lane l reads lane l - 1
-constexpr int kWaveShl1 = 0x130;  // lane l reads lane l + 1
 
 // Lanes whose source is out of range, or whose row is masked off, get `old`
 // (with BC, out-of-range sources read 0 instead).
@@ -65,36 +66,48 @@ __device__ __forceinline__ float dpp_f(float old, float v) {
                                                                  ROWS, 0xF, BC));
 }
 
-// Inclusive prefix sum over the 64 lanes.
-__device__ __forceinline__ int scan_i(int v) {
-    v += dpp_i<kRowShr1, 0xF, true>(0, v);
-    v += dpp_i<kRowShr2, 0xF, true>(0, v);
-    v += dpp_i<kRowShr4, 0xF, true>(0, v);
-    v += dpp_i<kRowShr8, 0xF, true>(0, v);
-    v += dpp_i<kBcast15, 0xA>(0, v);
-    v += dpp_i<kBcast31, 0xC>(0, v);
-    return v;
+// 1.0 on the lanes whose bit is set in the wave-uniform mask m, else 0.0.
+__device__ __forceinline__ float lane_factor(uint64_t m) {
+    return __builtin_amdgcn_inverse_ballot_w64(m) ? 1.0f : 0.0f;
 }
 
-// One step of an inclusive segmented scan keyed by segment: add the values of
-// the lane CTRL reads when it holds the same key.  Keys are segment id + 1 on
-// lanes that carry data and 0 elsewhere; they never decrease over the lanes
-// that carry data, so equal keys are contiguous and the steps below compose to
-// the full segmented scan.  A source out of range or masked off contributes 0.
+// One step of an inclusive segmented scan over lanes: the lanes set in m add
+// the value of the lane CTRL reads (sources out of range, or in rows outside
+// ROWS, contribute 0).  Every lane takes part, so every source is well defined.
 template <int CTRL, int ROWS = 0xF>
-__device__ __forceinline__ void seg_step(int key, float& n, float& d) {
-    const int pk = dpp_i<CTRL, ROWS, true>(0, key);
-    const float f = pk == key ? 1.0f : 0.0f;
+__device__ __forceinline__ void seg_step(uint64_t m, float& n, float& d) {
+    const float f = lane_factor(m);
     n = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, n), f, n);
     d = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, d), f, d);
 }
-__device__ __forceinline__ void seg_scan(int key, float& n, float& d) {
-    seg_step<kRowShr1>(key, n, d);
-    seg_step<kRowShr2>(key, n, d);
-    seg_step<kRowShr4>(key, n, d);
-    seg_step<kRowShr8>(key, n, d);
-    seg_step<kBcast15, 0xA>(key, n, d);
-    seg_step<kBcast31, 0xC>(key, n, d);
+
+// Lanes below the first set bit of a 16- or 32-lane group (all of them if none).
+__device__ __forceinline__ uint64_t before_first16(uint64_t bits, int lo) {
+    const uint32_t g = (uint32_t)(bits >> lo) & 0xFFFFu;
+    return (uint64_t)((1u << __builtin_ctz(g | 0x10000u)) - 1u) << lo;
+}
+__device__ __forceinline__ uint64_t before_first32(uint64_t bits) {
+    const uint32_t g = (uint32_t)(bits >> 32);
+    return g ? ((uint64_t)((1u << __builtin_ctz(g)) - 1u) << 32) : 0xFFFFFFFF00000000ull;
+}
+
+// Inclusive segmented scan of (n, d) over the 64 lanes, restarting at the lanes
+// set in `starts`.  In the step that adds the value from s lanes back, lane l
+// takes it when none of lanes l - s + 1 .. l starts a segment; the row
+// broadcasts extend a lane's sum into the previous row (lanes 15 and 47) and the
+// previous half (lane 31) when no segment starts between that row's (or half's)
+// first lane and the lane itself.  The masks are wave-uniform bit arithmetic.
+__device__ __forceinline__ void seg_scan(uint64_t starts, float& n, float& d) {
+    uint64_t m = ~starts;
+    seg_step<kRowShr1>(m, n, d);
+    m &= m << 1;
+    seg_step<kRowShr2>(m, n, d);
+    m &= m << 2;
+    seg_step<kRowShr4>(m, n, d);
+    m &= m << 4;
+    seg_step<kRowShr8>(m, n, d);
+    seg_step<kBcast15, 0xA>(before_first16(starts, 16) | before_first16(starts, 48), n, d);
+    seg_step<kBcast31, 0xC>(before_first32(starts), n, d);
 }
 
 template <int CTRL>
@@ -243,22 +256,20 @@ __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* l
 }
 
 // What a window needs from memory before its arithmetic: the lane's kE values
-// and indices, the start of segment scur + 1 + lane and the row scalars of
-// segment scur + lane.
+// and indices, and the row scalars of segment sb + lane (the window's segments
+// are sb .. sb + 64, sb being the one open before its first entry).
 struct Win {
     f32x4 v0, v1;
     u32x4 c0, c1;  // IDX16: c0 holds the 8 indices packed in pairs
-    int64_t st;
     float pr, ppr;
 };
 
-// Loads of the window at b (a multiple of kE).  Lanes at or past `lim` all read
-// entry b instead, so every address stays inside the arrays (whose padding
+// Data loads of the window at b (a multiple of kE).  Lanes at or past `lim` all
+// read entry b instead, so every address stays inside the arrays (whose padding
 // covers the last window) and a window past the chunk costs one cache line.
-template <int MODE, bool IDX16>
-__device__ __forceinline__ void load_window(const PassArgs& a, int64_t b, int64_t lim, uint32_t le,
-                                            int scur, int lane, Win& w) {
-    using N = Needs<MODE>;
+template <bool IDX16>
+__device__ __forceinline__ void load_data(const PassArgs& a, int64_t b, int64_t lim, uint32_t le,
+                                          Win& w) {
     const int64_t eb = b + (b + (int64_t)le < lim ? (int64_t)le : 0);
     const f32x4* vp = reinterpret_cast<const f32x4*>(a.val + eb);
     w.v0 = __builtin_nontemporal_load(vp);
@@ -271,30 +282,50 @@ __device__ __forceinline__ void load_window(const PassArgs& a, int64_t b, int64_
         w.c0 = __builtin_nontemporal_load(ip);
         w.c1 = __builtin_nontemporal_load(ip + 1);
     }
-    w.st = a.seg_start[min(scur + 1 + lane, a.nseg)];
-    const int sj = min(scur + lane, a.nseg - 1);
-    if constexpr (N::p) w.pr = a.p[sj];
-    if constexpr (N::pp) w.ppr = a.pp[sj];
 }
-
-template <bool IDX16>
-__device__ __forceinline__ uint32_t col_of(const Win& w, int k) {
-    if constexpr (IDX16) {
-        const uint32_t d = w.c0[k >> 1];
-        return (k & 1) ? (d >> 16) : (d & 0xFFFFu);
-    } else {
-        return k < 4 ? w.c0[k] : w.c1[k - 4];
+// Row scalars of segments sb .. sb + 63, one per lane.
+template <int MODE>
+__device__ __forceinline__ void load_slots(const PassArgs& a, int sb, int lane, Win& w) {
+    using N = Needs<MODE>;
+    if constexpr (N::p || N::pp) {
+        const int sj = min(max(sb + lane, 0), a.nseg - 1);
+        if constexpr (N::p) w.pr = a.p[sj];
+        if constexpr (N::pp) w.ppr = a.pp[sj];
     }
 }
+
+// Index of entry k of the lane, without the segment start bit.
+template <bool IDX16>
+__device__ __forceinline__ uint32_t col_of(const Win& w, int k) {
+    using B = IndexBits<typename std::conditional<IDX16, uint16_t, int32_t>::type>;
+    uint32_t c;
+    if constexpr (IDX16) {
+        const uint32_t d = w.c0[k >> 1];
+        c = (k & 1) ? (d >> 16) : (d & 0xFFFFu);
+    } else {
+        c = k < 4 ? w.c0[k] : w.c1[k - 4];
+    }
+    return k == 0 ? (c & B::mask) : c;  // only a lane's first entry carries the bit
+}
+template <bool IDX16>
+__device__ __forceinline__ bool starts_segment(const Win& w) {
+    using B = IndexBits<typename std::conditional<IDX16, uint16_t, int32_t>::type>;
+    return (w.c0[0] & B::start) != 0u;
+}
 __device__ __forceinline__ float val_of(const Win& w, int k) { return k < 4 ? w.v0[k] : w.v1[k - 4]; }
+
+__device__ __forceinline__ float lane_pick(float v, uint32_t src) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((int)(src << 2),
+                                                                  __builtin_bit_cast(int, v)));
+}
 
 // State a wave carries from window to window of its chunk.
 struct Walk {
     int64_t elo;  // first entry of the next window (a multiple of kE)
     int64_t c1;   // end of the chunk (a multiple of kE)
-    int scur;     // segment holding entry elo
-    int cid;      // segment left open by the previous window (-1: none), and its sums
-    double cn, cd;
+    int sb;       // segment of the entry before elo (the open one, when `open`)
+    bool open;    // a segment is open: it has entries before elo in this chunk
+    double cn, cd;  // sums of the open segment so far
     double sse;
     int mid;      // the chunk's first segment when it began in an earlier chunk, else -1
     int head;     // the chunk's head partial slot (its tail slot follows)
@@ -314,71 +345,64 @@ __device__ __forceinline__ void emit(const PassArgs& a, const Walk& wk, int s, d
         a.part[s] = make_double2(num, den);
 }
 
-// One window [elo, we) of a wave's chunk.  Lane l holds entries elo + l*kE ..
-// elo + l*kE + kE - 1; every window starts and ends on a multiple of kE, so a
-// lane's entries are either all inside the window or all outside.  The window
-// ends at the chunk end, after 64 lanes, or at the last multiple of kE not past
-// the start of segment scur + 64, so it meets at most 64 segments and their row
-// scalars fit one LDS slot per lane.  The segment of each entry comes from a
-// bitmap of the segment starts inside the window (built in the wave's LDS
-// scratch from one coalesced read of the segment table) and a prefix count over
-// lanes.  The loads of the next window are issued before the arithmetic.
+// One window [elo, we) of a wave's chunk: up to 64 lanes of kE entries, lane l
+// holding entries elo + l*kE .. elo + l*kE + kE - 1, all of one segment.  A lane
+// whose first index carries the start bit begins a new segment, so the lanes'
+// segments follow from a ballot of those bits and a masked bit count.  Each lane
+// sums R-hat*x and x^2 over its entries; a segmented scan over the lanes then
+// gives every segment's window sum at its last lane, and the lane that starts
+// the next segment emits it.  The data of the window after next is requested
+// first, so two windows' loads are in flight while this one is reduced.
 template <int MODE, bool STAGED, bool IDX16, bool P1>
 __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk& wk,
-                                       const Win& cur, Win& nxt, int lane, uint32_t le, float* spr,
-                                       float* sppr, uint32_t* bm) {
+                                       const Win& cur, Win& nxt, Win& nn, int lane, uint32_t le) {
     using N = Needs<MODE>;
     const int64_t b = wk.elo;
-    const int64_t st = cur.st;
-    int64_t we = min(b + (int64_t)kWin, wk.c1);
-    const int64_t st63 = lane_i64(st, 63);
-    if (st63 < we) we = st63 & ~(int64_t)(kE - 1);
-    const int adv = __builtin_popcountll(__ballot(st <= we));
-    // Row scalars of the window's segments, one LDS slot per lane.
-    if constexpr (N::p) spr[lane] = cur.pr;
-    if constexpr (N::pp) sppr[lane] = cur.ppr;
-    // Bitmap of the segment starts inside (b, we); this lane's kE bits.
-    if (lane < kWin / 32) bm[lane] = 0u;
-    __builtin_amdgcn_wave_barrier();
-    if (st < we) {
-        const uint32_t off = (uint32_t)(st - b);
-        atomicOr(&bm[off >> 5], 1u << (off & 31u));
-    }
-    __builtin_amdgcn_wave_barrier();
-    const uint32_t bits = (bm[le >> 5] >> (le & 31u)) & ((1u << kE) - 1u);
-
-    // Next window's loads (a harmless reload of b when this window is the last).
-    const int scur_n = wk.scur + adv;
+    const int64_t we = min(b + (int64_t)kWin, wk.c1);
+    // Data of the window after next, before anything waits on this one (a harmless
+    // reload of b past the chunk's end).
     {
-        const bool more = we < wk.c1;
-        load_window<MODE, IDX16>(a, more ? we : b, more ? wk.c1 : b, le, scur_n, lane, nxt);
+        const int64_t b2 = we + kWin;
+        const bool more = b2 < wk.c1;
+        load_data<IDX16>(a, more ? b2 : b, more ? wk.c1 : b, le, nn);
     }
-
     const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
     const bool lv = lane < nl;
-    const int nb = __builtin_popcount(bits);
-    const int idb = wk.scur + scan_i(nb) - nb;  // segment of this lane's first entry
+    const bool fl = lv && starts_segment<IDX16>(cur);
+    const uint64_t starts = __ballot(fl);
+    const int sb_n = wk.sb + __builtin_popcountll(starts);
+    load_slots<MODE>(a, sb_n, lane, nxt);  // the next window's row scalars
 
-    // Gathers, residual bookkeeping, and running sums restarted at segment starts.
-    float r[kE], sn[kE], sd[kE];
+    // Segments started at lanes 0 .. lane: the lane's segment is sb + cl.
+    const uint64_t sh = starts >> 1;
+    const uint32_t cl = __builtin_amdgcn_mbcnt_hi(
+        (uint32_t)(sh >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)sh, (uint32_t)(starts & 1u)));
+
+    // Row scalars of the lane's segment, from the window's slots; with 64 starts the
+    // last lane's segment is sb + 64, past the slots.
+    float pr = 0.0f, ppr = 0.0f;
+    if constexpr (N::p) pr = lane_pick(cur.pr, cl);
+    if constexpr (N::pp) ppr = lane_pick(cur.ppr, cl);
+    if constexpr (N::p || N::pp) {
+        if (starts == ~0ull && lane == 63) {
+            if constexpr (N::p) pr = a.p[wk.sb + 64];
+            if constexpr (N::pp) ppr = a.pp[wk.sb + 64];
+        }
+    }
+
+    // Gathers, residual bookkeeping, and the lane's sums.
+    float r[kE];
     float an = 0.0f, ad = 0.0f;
-    int slot = idb - wk.scur;
 #pragma unroll
     for (int k = 0; k < kE; ++k) {
-        const bool fk = (bits >> k) & 1u;
-        if constexpr (N::p || N::pp) slot += fk ? 1 : 0;
         const uint32_t c = col_of<IDX16>(cur, k);
-        const float pr = N::p ? spr[slot] : 0.0f;
-        const float ppr = N::pp ? sppr[slot] : 0.0f;
         const float qv = N::q ? gat<STAGED>(gx.lq, gx.gq, c) : 0.0f;
         const float qqv = N::qq ? gat<STAGED>(gx.lqq, gx.gqq, c) : 0.0f;
         r[k] = rhat<MODE>(val_of(cur, k), qv, qqv, pr, ppr);
         if constexpr (N::x) {
             const float xv = gat<STAGED>(gx.lx, gx.gx, c);
-            an = __builtin_fmaf(r[k], xv, fk ? 0.0f : an);
-            ad = __builtin_fmaf(xv, xv, fk ? 0.0f : ad);
-            sn[k] = an;
-            sd[k] = ad;
+            an = __builtin_fmaf(r[k], xv, an);
+            ad = __builtin_fmaf(xv, xv, ad);
         }
     }
     if constexpr (N::store) {
@@ -408,95 +432,76 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
         for (int k = 0; k < kE; ++k) s2 = __builtin_fmaf(r[k], r[k], s2);
         if (lv) wk.sse += (double)s2;
     } else {
-        // A segment left open by the previous window that ended where this one starts.
-        if (wk.cid >= 0 && wk.cid != wk.scur) {
-            if (lane == 0) emit<P1>(a, wk, wk.cid, wk.cn, wk.cd);
-            wk.cid = -1;
+        if (!lv) {
+            an = 0.0f;
+            ad = 0.0f;
         }
-        // Scan keys: segment + 1 of the lane's first (hk) and last (tk) entry, 0 on
-        // lanes without entries.
-        const int hk = lv ? idb + (int)(bits & 1u) + 1 : 0;
-        const int tk = lv ? idb + nb + 1 : 0;
-        float scn = an, scd = ad;
-        seg_scan(tk, scn, scd);
-        // Sums of this lane's first segment over earlier lanes, and from earlier windows.
-        const int pk1 = dpp_i<kWaveShr1, 0xF, true>(0, tk);
-        const float pn1 = dpp_f<kWaveShr1, 0xF, true>(0.0f, scn);
-        const float pd1 = dpp_f<kWaveShr1, 0xF, true>(0.0f, scd);
-        double hn = 0.0, hd = 0.0;
-        if (pk1 == hk) {
-            hn = (double)pn1;
-            hd = (double)pd1;
-        }
-        if (hk == wk.cid + 1) {
-            hn += wk.cn;
-            hd += wk.cd;
-        }
-        // Entry k ends a segment when entry k + 1 starts one; the lane's last entry
-        // when the next lane's first does.  The window's last entry stays open.
-        const uint32_t nb0 = (uint32_t)dpp_i<kWaveShl1, 0xF, true>(0, (int)(bits & 1u));
-        uint32_t ends = (bits >> 1) | ((lane + 1 < nl ? nb0 : 0u) << (kE - 1));
-        if (!lv) ends = 0u;
-        const uint32_t ff = bits ? (uint32_t)__builtin_ctz(bits) : (uint32_t)kE;  // head: k < ff
-        // Emit one end per lane per round; most windows need one round.
-        uint32_t rem = ends;
-        while (__ballot(rem != 0u)) {
-            if (rem != 0u) {
-                const uint32_t k = (uint32_t)__builtin_ctz(rem);
-                float vn = sn[0], vd = sd[0];
-#pragma unroll
-                for (int j = 1; j < kE; ++j)
-                    if (k == (uint32_t)j) {
-                        vn = sn[j];
-                        vd = sd[j];
-                    }
-                double en = (double)vn, ed = (double)vd;
-                if (k < ff) {
-                    en += hn;
-                    ed += hd;
-                }
-                const int s = idb + __builtin_popcount(bits & ((2u << k) - 1u));
-                emit<P1>(a, wk, s, en, ed);
-                rem &= rem - 1u;
+        seg_scan(starts, an, ad);
+        // A lane that starts a segment emits the previous one: its sum over the
+        // earlier lanes of the window (the scan at the lane before), plus the sums
+        // from earlier windows when it is the window's first segment.
+        const float pn = dpp_f<kWaveShr1, 0xF, true>(0.0f, an);
+        const float pd = dpp_f<kWaveShr1, 0xF, true>(0.0f, ad);
+        if (fl) {
+            const bool first = lane == (int)__builtin_ctzll(starts);
+            double en = (double)pn, ed = (double)pd;
+            if (first) {
+                en += wk.cn;
+                ed += wk.cd;
             }
+            if (wk.open || lane > 0) emit<P1>(a, wk, wk.sb + (int)cl - 1, en, ed);
         }
-        // The segment of the window's last entry stays open; one that started in that
-        // lane has no earlier sums.
+        // The segment of the window's last lane stays open.
         const int ll = nl - 1;
-        const double ln = (double)an + (bits == 0u ? hn : 0.0);
-        const double ld = (double)ad + (bits == 0u ? hd : 0.0);
-        wk.cid = __builtin_amdgcn_readlane(tk, ll) - 1;
-        wk.cn = lane_f64(ln, ll);
-        wk.cd = lane_f64(ld, ll);
+        const double ln = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, an), ll));
+        const double ld = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ad), ll));
+        if (starts == 0ull) {
+            wk.cn += ln;
+            wk.cd += ld;
+        } else {
+            wk.cn = ln;
+            wk.cd = ld;
+        }
+        wk.open = true;
     }
-    wk.scur = scur_n;
+    wk.sb = sb_n;
     wk.elo = we;
 }
 
-// One wave's chunk [c0, c1) (whole segments, the first one scur), two windows per
-// loop turn so the current and next window alternate between two register sets.
+// One wave's chunk [c0, c1), three windows per loop turn so that the current
+// window and the two whose data is in flight rotate over three register sets.  s0 is the segment holding entry
+// c0; it began in an earlier chunk when the chunk's first lane does not start it
+// (flag kChunkMid).
 template <int MODE, bool STAGED, bool IDX16, bool P1>
 __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, int64_t c0,
-                                          int64_t c1, int scur, int flags, int gc, int lane,
-                                          float* spr, float* sppr, uint32_t* bm, double& sse) {
+                                          int64_t c1, int s0, int flags, int gc, int lane,
+                                          double& sse) {
     const uint32_t le = (uint32_t)lane * kE;
-    Walk wk{c0, c1, scur, -1, 0.0, 0.0, sse, (flags & kChunkMid) ? scur : -1, a.nseg + 2 * gc};
-    Win wa, wb;
-    load_window<MODE, IDX16>(a, c0, c1, le, scur, lane, wa);
+    const bool mid = flags & kChunkMid;
+    Walk wk{c0, c1, mid ? s0 : s0 - 1, mid, 0.0, 0.0, sse, mid ? s0 : -1, a.nseg + 2 * gc};
+    Win wa, wb, wc;
+    load_data<IDX16>(a, c0, c1, le, wa);
+    load_slots<MODE>(a, wk.sb, lane, wa);
+    {
+        const bool more = c0 + kWin < c1;
+        load_data<IDX16>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
+    }
     while (true) {
-        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wa, wb, lane, le, spr, sppr, bm);
+        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wa, wb, wc, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wb, wa, lane, le, spr, sppr, bm);
+        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wb, wc, wa, lane, le);
+        if (wk.elo >= c1) break;
+        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wc, wa, wb, lane, le);
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
         // The last segment: finished, or going on past the chunk (a partial in the head
         // slot when it is also the segment that began earlier, else in the tail slot).
-        if (wk.cid >= 0 && lane == 0) {
+        if (lane == 0) {
             if (flags & kChunkCont)
-                a.part[wk.head + (wk.cid == wk.mid ? 0 : 1)] = make_double2(wk.cn, wk.cd);
+                a.part[wk.head + (wk.sb == wk.mid ? 0 : 1)] = make_double2(wk.cn, wk.cd);
             else
-                emit<P1>(a, wk, wk.cid, wk.cn, wk.cd);
+                emit<P1>(a, wk, wk.sb, wk.cn, wk.cd);
         }
     }
     sse = wk.sse;
@@ -519,11 +524,6 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
     }
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = (int)(threadIdx.x & 63u);
-    uint32_t* scr = reinterpret_cast<uint32_t*>(lds + a.vec_floats) + wave * scratch_words(MODE);
-    // Scratch layout (scratch_words): the bitmap, then the slots of p, then of pp.
-    uint32_t* bm = scr;                                              // kWin / 32 words
-    float* spr = reinterpret_cast<float*>(scr + kWin / 32);         // 64 row scalars p
-    float* sppr = reinterpret_cast<float*>(scr + kWin / 32 + (N::p ? 64 : 0));  // 64 pp
 
     if constexpr (MODE != kModeFlush && P1) {
         // The rows after the last non-empty one have no entries: coordinate 0.
@@ -548,7 +548,7 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
         const int gc = pc * kWaves + wave;
         if (c0 < c1)
             run_chunk<MODE, STAGED, IDX16, P1>(a, gx, c0, c1, a.piece_seg[gc], a.chunk_flags[gc],
-                                               gc, lane, spr, sppr, bm, sse);
+                                               gc, lane, sse);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -683,7 +683,6 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     PassArgs a{};
     a.idx = L.idx;
     a.val = L.val;
-    a.seg_start = L.seg_start;
     a.wg_piece = L.wg_piece;
     a.piece_tile = L.piece_tile;
     a.piece_chunk = L.piece_chunk;
@@ -708,7 +707,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
     a.lambda = lambda;
     a.vec_floats = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
-    const size_t lds = (size_t)a.vec_floats * sizeof(float) + (size_t)kWaves * scratch_words(mode) * 4;
+    const size_t lds = (size_t)a.vec_floats * sizeof(float);
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     const dim3 grid(L.grid);
     if (staged) {

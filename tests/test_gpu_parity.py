@@ -205,6 +205,40 @@ def test_layout_strategies_match_oracle(name):
         assert info["u_gather"] == 1 and info["v_gather"] == 1
 
 
+@pytest.mark.parametrize("layout", ["auto", "global"])
+@pytest.mark.parametrize("transpose", [False, True])
+def test_short_segments_fill_windows(layout, transpose):
+    # Rows of 1..8 entries: every segment fills one lane after alignment padding, so
+    # full windows hold 64 segment starts (the last lane's segment lies past the
+    # window's row-scalar slots).  40,000 columns need 32-bit indices in global mode.
+    from paper_1511_02433_amd.ccdpp import make_options
+    lens = list(np.random.default_rng(51).integers(1, 9, 6000))
+    row, col, val, H0 = synth.lengths_problem(lens, 40_000, 3, seed=52)
+    m, n = len(lens), 40_000
+    if transpose:
+        row, col = col, row
+        m, n = n, m
+        H0 = (np.random.default_rng(53).standard_normal((n, 3)) * 0.1).astype(np.float32)
+    print(f"case: short segments layout={layout} transpose={transpose} nnz={row.size}",
+          flush=True)
+    opts = make_options(gather_mode=(1, 1)) if layout == "global" else make_options()
+    g = CCDPP(m, n, 3, 0.1, row, col, val, opts=opts)
+    print({k: v for k, v in g.info().items() if k.startswith(("u_", "v_"))})
+    g.set_factors(np.zeros((m, 3), np.float32), H0)
+    o = Oracle(m, n, 3, 0.1, row, col, val, H0)
+    g.run(1, 2)
+    o.run(1, 2)
+    Wg, Hg = g.factors()
+    Wo, Ho = o.factors()
+    ew, eh = colscaled_max_rel_err(Wg, Wo), colscaled_max_rel_err(Hg, Ho)
+    print(f"W err {ew:.3e}  H err {eh:.3e}")
+    assert ew <= W_TOL and eh <= W_TOL
+    g.run(1, 2)
+    o.run(1, 2)
+    assert abs(g.train_rmse() - o.train_rmse()) <= RMSE_TOL
+    assert g.check_consistency() == 0
+
+
 def test_heavy_rows_in_tiles_and_layout_equivalence():
     # Rows far longer than kGroupMaxLen inside tiles, plus the same problem under two
     # layouts: results agree to summation-order rounding.
