@@ -86,12 +86,12 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 global memory; 2 stage them in LDS, cut into tiles of
  *                 tile_width columns when they do not fit
  *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
- *                 153600 / (4 * v) - 64, rounded down to a multiple of 64,
+ *                 163840 / (4 * v) - 64, rounded down to a multiple of 64,
  *                 where v = 2 for index 0 and 3 for index 1 (the vectors the
  *                 first pass of a feature stages)
  *   workgroups  : persistent workgroups per pass (0: two per compute unit)
  *   seg_weight  : work of one row segment, in entries, when the entries are
- *                 shared out among workgroups and waves (0: the default, 12;
+ *                 shared out among workgroups and waves (0: the default, 4;
  *                 -1: shares by entries alone)
  * Results differ between layouts only by floating-point summation order.
  */

@@ -74,7 +74,7 @@ constexpr int kAlign = 64;                // tile, share and chunk starts: 256 B
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
 constexpr int kLdsVecBytes = kLdsBytes;   // all of it holds staged vectors
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
-constexpr int kSegWeight = 12;            // default work of one segment, in entries
+constexpr int kSegWeight = 4;             // default work of one segment, in entries
 constexpr int kChunkMid = 1;              // chunk flag: its first segment began in an earlier chunk
 constexpr int kChunkCont = 2;             // chunk flag: its last segment goes on past its end
 constexpr int kEntryPad = 64;             // entries of padding after idx and val (loads past the end)

@@ -222,9 +222,9 @@ __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* l
     if (N::q) sq = lds + (slot++) * Ts;
     if (alias) sx = sq;
     if (N::qq) sqq = lds + (slot++) * Ts;
-    // Four strided elements per thread per step, loads first, so that a step costs
-    // one memory latency rather than four.
-    constexpr int kU = 4;
+    // Sixteen strided elements per thread per step, loads first, so that a step
+    // costs one memory latency (one or two steps cover a tile).
+    constexpr int kU = 16;
     for (int i0 = (int)threadIdx.x; i0 < len; i0 += kU * kWG) {
         float vx[kU], vq[kU], vqq[kU];
 #pragma unroll
@@ -353,7 +353,7 @@ __device__ __forceinline__ void emit(const PassArgs& a, const Walk& wk, int s, d
 // gives every segment's window sum at its last lane, and the lane that starts
 // the next segment emits it.  The data of the window after next is requested
 // first, so two windows' loads are in flight while this one is reduced.
-template <int MODE, bool STAGED, bool IDX16, bool P1>
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
 __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk& wk,
                                        const Win& cur, Win& nxt, Win& nn, int lane, uint32_t le) {
     using N = Needs<MODE>;
@@ -400,7 +400,7 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
         const float qqv = N::qq ? gat<STAGED>(gx.lqq, gx.gqq, c) : 0.0f;
         r[k] = rhat<MODE>(val_of(cur, k), qv, qqv, pr, ppr);
         if constexpr (N::x) {
-            const float xv = gat<STAGED>(gx.lx, gx.gx, c);
+            const float xv = XQ ? qv : gat<STAGED>(gx.lx, gx.gx, c);
             an = __builtin_fmaf(r[k], xv, an);
             ad = __builtin_fmaf(xv, xv, ad);
         }
@@ -469,29 +469,36 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
 }
 
 // One wave's chunk [c0, c1), three windows per loop turn so that the current
-// window and the two whose data is in flight rotate over three register sets.  s0 is the segment holding entry
+// window and the two whose data is in flight rotate over three register sets.
+// begin_chunk requests the first two windows, so that a caller can overlap them
+// with the staging of the tile.  s0 is the segment holding entry
 // c0; it began in an earlier chunk when the chunk's first lane does not start it
 // (flag kChunkMid).
-template <int MODE, bool STAGED, bool IDX16, bool P1>
+template <int MODE, bool IDX16>
+__device__ __forceinline__ void begin_chunk(const PassArgs& a, int64_t c0, int64_t c1, int s0,
+                                            int flags, int lane, Win& wa, Win& wb) {
+    const uint32_t le = (uint32_t)lane * kE;
+    load_data<IDX16>(a, c0, c1, le, wa);
+    load_slots<MODE>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
+    const bool more = c0 + kWin < c1;
+    load_data<IDX16>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
+}
+
+// wa and wb hold the requests of begin_chunk.
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
 __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, int64_t c0,
                                           int64_t c1, int s0, int flags, int gc, int lane,
-                                          double& sse) {
+                                          Win& wa, Win& wb, double& sse) {
     const uint32_t le = (uint32_t)lane * kE;
     const bool mid = flags & kChunkMid;
     Walk wk{c0, c1, mid ? s0 : s0 - 1, mid, 0.0, 0.0, sse, mid ? s0 : -1, a.nseg + 2 * gc};
-    Win wa, wb, wc;
-    load_data<IDX16>(a, c0, c1, le, wa);
-    load_slots<MODE>(a, wk.sb, lane, wa);
-    {
-        const bool more = c0 + kWin < c1;
-        load_data<IDX16>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
-    }
+    Win wc;
     while (true) {
-        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wa, wb, wc, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wa, wb, wc, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wb, wc, wa, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wb, wc, wa, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1>(a, gx, wk, wc, wa, wb, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wc, wa, wb, lane, le);
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
@@ -508,8 +515,9 @@ __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, i
 }
 
 // One pass: the workgroup's pieces in order, each staging its tile (when it
-// differs from the one staged) and then giving every wave its chunk.
-template <int MODE, bool STAGED, bool IDX16, bool P1>
+// differs from the one staged) and then giving every wave its chunk.  XQ: the
+// update gathers the same vector as the add-back (x == q), read once per entry.
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
 __device__ __forceinline__ void pass_main(const PassArgs& a) {
     using N = Needs<MODE>;
     extern __shared__ float lds[];
@@ -534,6 +542,14 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
     double sse = 0.0;
     int staged = -1;
     for (int pc = a.wg_piece[wg]; pc < a.wg_piece[wg + 1]; ++pc) {
+        const int64_t c0 = a.piece_chunk[pc * (kWaves + 1) + wave];
+        const int64_t c1 = a.piece_chunk[pc * (kWaves + 1) + wave + 1];
+        const int gc = pc * kWaves + wave;
+        const int s0 = a.piece_seg[gc], flags = a.chunk_flags[gc];
+        // The chunk's first windows are requested before the staging, which they do
+        // not depend on.
+        Win wa, wb;
+        if (c0 < c1) begin_chunk<MODE, IDX16>(a, c0, c1, s0, flags, lane, wa, wb);
         if constexpr (STAGED) {
             const int tile = a.piece_tile[pc];
             if (tile != staged) {
@@ -543,12 +559,8 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
                 staged = tile;
             }
         }
-        const int64_t c0 = a.piece_chunk[pc * (kWaves + 1) + wave];
-        const int64_t c1 = a.piece_chunk[pc * (kWaves + 1) + wave + 1];
-        const int gc = pc * kWaves + wave;
         if (c0 < c1)
-            run_chunk<MODE, STAGED, IDX16, P1>(a, gx, c0, c1, a.piece_seg[gc], a.chunk_flags[gc],
-                                               gc, lane, sse);
+            run_chunk<MODE, STAGED, IDX16, P1, XQ>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -563,43 +575,60 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
 // are rows (P == 1).
 template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass(PassArgs a) {
-    pass_main<kModePlain, STAGED, IDX16, P1>(a);
+    pass_main<kModePlain, STAGED, IDX16, P1, false>(a);
 }
 template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused_first(PassArgs a) {
-    pass_main<kModeAdd, STAGED, IDX16, P1>(a);
+    if (a.x_is_q)
+        pass_main<kModeAdd, STAGED, IDX16, P1, true>(a);
+    else
+        pass_main<kModeAdd, STAGED, IDX16, P1, false>(a);
 }
 template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused(PassArgs a) {
-    pass_main<kModeSubAdd, STAGED, IDX16, P1>(a);
+    if (a.x_is_q)
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, true>(a);
+    else
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, false>(a);
 }
 template <bool STAGED, bool IDX16, bool P1>
 __global__ __launch_bounds__(kWG) void ccd_flush(PassArgs a) {
-    pass_main<kModeFlush, STAGED, IDX16, P1>(a);
+    pass_main<kModeFlush, STAGED, IDX16, P1, false>(a);
 }
 
-// Fixed-order combine of a row's partials: one wave per row, lane k takes the
-// row's partial slots k, k + 64, ... in entry order, then a fixed tree.  With
-// yseg, the coordinate is also written to every segment of the row.
+// x summed over the 16 lanes of a DPP row; every lane of the row gets the same
+// bits (each step adds two values that the partner lane adds in swapped order).
+__device__ __forceinline__ double row16_sum(double x) {
+    x += dppq_d<0xB1>(x);   // quad_perm [1,0,3,2]: lane ^ 1
+    x += dppq_d<0x4E>(x);   // quad_perm [2,3,0,1]: lane ^ 2
+    x += dppq_d<0x141>(x);  // row_half_mirror: the other quad of 8
+    x += dppq_d<0x140>(x);  // row_mirror: the other half of 16
+    return x;
+}
+
+// Fixed-order combine of a row's partials: 16 lanes (one DPP row) per row; lane
+// l adds the row's partial slots l, l + 16, ... in entry order, then a fixed
+// tree over the 16 lanes.  With yseg, the coordinate is also written to every
+// segment of the row.
+constexpr int kCombineLanes = 16;
 __global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
-    const int wave = (int)(threadIdx.x >> 6);
-    const int lane = (int)(threadIdx.x & 63u);
-    const int i = blockIdx.x * 4 + wave;
-    if (i >= c.n) return;
+    const int l = (int)(threadIdx.x & (kCombineLanes - 1));
+    const int i = blockIdx.x * (256 / kCombineLanes) + (int)(threadIdx.x / kCombineLanes);
+    if (i >= c.n) return;  // whole 16-lane rows leave together
     const int b = c.src_ptr[i];
     const int e = c.src_ptr[i + 1];
     double num = 0.0, den = 0.0;
-    for (int k = b + lane; k < e; k += 64) {
+    for (int k = b + l; k < e; k += kCombineLanes) {
         const double2 pv = c.part[c.srcs[k]];
         num += pv.x;
         den += pv.y;
     }
-    num = wave_sum(num);
-    den = wave_sum(den);
+    num = row16_sum(num);
+    den = row16_sum(den);
     const float yr = coordinate(num, den, c.lambda);
-    if (lane == 0) c.y[c.ids ? c.ids[i] : i] = yr;
+    if (l == 0) c.y[c.ids ? c.ids[i] : i] = yr;
     if (c.yseg)
-        for (int k = c.seg_ptr[i] + lane; k < c.seg_ptr[i + 1]; k += 64) c.yseg[c.segs[k]] = yr;
+        for (int k = c.seg_ptr[i] + l; k < c.seg_ptr[i + 1]; k += kCombineLanes) c.yseg[c.segs[k]] = yr;
 }
 
 __global__ __launch_bounds__(256) void ccd_copy(const float* __restrict__ src,
@@ -737,7 +766,9 @@ hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda,
     c.yseg = yseg;
     c.n = L.ncomb;
     c.lambda = lambda;
-    hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.ncomb + 3) / 4)), dim3(256), 0, s, c);
+    constexpr int rows_per_block = 256 / kCombineLanes;
+    hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.ncomb + rows_per_block - 1) / rows_per_block)),
+                       dim3(256), 0, s, c);
     return hipGetLastError();
 }
 
