@@ -52,8 +52,8 @@ struct ccdpp {
     int32_t* cold2new = nullptr;
     // Entry e of the user-major copy in layout order, padding excluded:
     int32_t* perm0 = nullptr;      // e -> input triplet index
-    int32_t* pos0 = nullptr;       // e -> padded position in the user-major copy
-    int32_t* map01 = nullptr;      // e -> padded position in the item-major copy
+    int32_t* pos0 = nullptr;       // e -> value slot in the user-major copy
+    int32_t* map01 = nullptr;      // e -> value slot in the item-major copy
     float* A = nullptr;            // A[e], the rating of entry e
     float* fseg[2] = {};           // P > 1: own factor columns spread over segments (k x S)
     float* W = nullptr;            // k x m: W[t*m + i]
@@ -189,7 +189,7 @@ void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
 // input triplet (device).  side 0 is the user-major copy (its first pass stages
 // q and qq, x being q), side 1 the item-major copy (first pass stages x, q, qq).
 // On return, for every entry e in layout order (padding excluded), perm[e] holds
-// its input triplet index and epos[e] its padded position.
+// its input triplet index and epos[e] the slot of its value (val_slot).
 int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, const int32_t* lrow,
                  const int32_t* lcol, const float* val_in, const ccdpp_options_t* opt,
                  int32_t* perm, int32_t* epos, hipStream_t s) {

@@ -64,7 +64,8 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
         if (keys[p] == keys[p + 1]) *flag = 1;
 }
 
-// Entry q of the sorted order goes to padded position q + seg_off[segment].
+// Entry q of the sorted order goes to padded position p = q + seg_off[segment]:
+// its index to idx[p], its value to val[val_slot(p)]; pos[q] is the value slot.
 template <class I>
 __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
                               const float* __restrict__ val_in, int64_t nnz, int cbits,
@@ -78,8 +79,9 @@ __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* 
         const uint32_t c = (uint32_t)(key & mask);
         const bool first = q == 0 || (keys[q - 1] >> cbits) != (key >> cbits);
         idx[p] = (I)((swz ? lds_swizzle(c) : c) | (first ? IndexBits<I>::start : 0u));
-        val[p] = val_in[perm[q]];
-        pos[q] = (int32_t)p;
+        const int64_t f = val_slot(p);
+        val[f] = val_in[perm[q]];
+        pos[q] = (int32_t)f;
     }
 }
 
@@ -131,7 +133,7 @@ __global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* 
 
 // R = A - w_i^T h_j for every entry of the user-major layout (prediction summed
 // in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
-// unpadded layout order) sits at position pos[e]; its segment, and from it the
+// unpadded layout order) has its value in slot pos[e]; its segment, and from it the
 // row and the tile, are found by binary search.
 template <class I>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
@@ -142,7 +144,8 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           int64_t n, int32_t k, int64_t nnz, float* __restrict__ val) {
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
          e += (int64_t)gridDim.x * kT) {
-        const int64_t q = pos[e];
+        const int64_t f = pos[e];         // value slot
+        const int64_t q = val_entry(f);   // entry position
         int64_t lo = 0, hi = nseg;  // last s with seg_start[s] <= q
         while (hi - lo > 1) {
             const int64_t mid = (lo + hi) >> 1;
@@ -159,7 +162,7 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
-        val[q] = (float)((double)A[e] - pred);
+        val[f] = (float)((double)A[e] - pred);
     }
 }
 

@@ -43,10 +43,15 @@ namespace ccdk {
 // results are identical run to run.
 //
 // Every segment starts at a multiple of kE entries, and every tile, workgroup
-// share and chunk at a multiple of kAlign, so that a window's loads cover whole
-// cache lines: the build inserts padding entries after a segment up to the next
-// multiple of kE (of kAlign before a new tile), and cuts shares and chunks at
-// multiples of kAlign.  A padding entry holds value 0 and an index that reads 0 (a zero word
+// share and chunk at a multiple of kAlign = kWin, so that every window a pass
+// reads is one whole, aligned block of kWin entries: the build inserts padding
+// entries after a segment up to the next multiple of kE (of kAlign before a new
+// tile), and cuts shares and chunks at multiples of kAlign.  Inside a block the
+// values are stored lane-split (val_slot): lane l's kE values sit at 4l .. 4l + 3
+// and kWin/2 + 4l .. kWin/2 + 4l + 3, so that each 128-bit load or store of the
+// wave covers 1 KB of contiguous memory; the indices stay in entry order (one
+// 128-bit load per lane already covers 16 contiguous bytes).  A padding entry
+// holds value 0 and an index that reads 0 (a zero word
 // after each staged slice in LDS, or a position past the vector in global
 // mode, where the bounded buffer load returns 0), so it adds exactly 0 to
 // every sum and stays 0 under every residual update.
@@ -69,7 +74,7 @@ constexpr int kWG = 1024;                 // threads per persistent workgroup
 constexpr int kWaves = kWG / 64;          // 16 waves
 constexpr int kE = 8;                     // entries per lane per window
 constexpr int kWin = 64 * kE;             // entries per window
-constexpr int kAlign = 64;                // tile, share and chunk starts: 256 B of values, 128 B of indices
+constexpr int kAlign = kWin;              // tile, share and chunk starts: whole window blocks
 
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
 constexpr int kLdsVecBytes = kLdsBytes;   // all of it holds staged vectors
@@ -80,6 +85,17 @@ constexpr int kChunkCont = 2;             // chunk flag: its last segment goes o
 constexpr int kEntryPad = 64;             // entries of padding after idx and val (loads past the end)
 
 __host__ __device__ inline uint32_t lds_swizzle(uint32_t c) { return c ^ ((c >> 5) & 31u); }
+
+// Storage slot of the value of entry p (see above), and its inverse.
+static_assert(kWin == 512 && kE == 8, "val_slot assumes 64 lanes of 8 entries");
+__host__ __device__ inline int64_t val_slot(int64_t p) {
+    const int64_t o = p & (kWin - 1);
+    return (p - o) + ((o & 4) << 6) + ((o >> 3) << 2) + (o & 3);
+}
+__host__ __device__ inline int64_t val_entry(int64_t f) {
+    const int64_t o = f & (kWin - 1);
+    return (f - o) + (((o & 255) >> 2) << 3) + ((o >> 8) << 2) + (o & 3);
+}
 
 enum PassMode : int32_t {
     kModePlain = 0,     // R-hat read only: y = sum rhat x / (lambda + sum x^2)
@@ -110,7 +126,7 @@ enum GatherMode : int32_t {
 
 struct PassArgs {
     const void* idx;            // [npad] uint16 or int32 tile-local column
-    float* val;                 // [npad] residual / R-hat
+    float* val;                 // [npad] residual / R-hat, in val_slot order
     const int32_t* wg_piece;    // [grid + 1] pieces of each workgroup
     const int32_t* piece_tile;  // [npieces] tile of each piece
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves

@@ -264,16 +264,18 @@ struct Win {
     float pr, ppr;
 };
 
-// Data loads of the window at b (a multiple of kE).  Lanes at or past `lim` all
-// read entry b instead, so every address stays inside the arrays (whose padding
-// covers the last window) and a window past the chunk costs one cache line.
+// Data loads of the window block at b (a multiple of kWin): lane l's values from
+// the two halves of the block (val_slot order), its indices in entry order.
+// Lanes at or past `lim` read lane 0's part instead, so every address stays
+// inside the arrays; a window past the chunk rereads block b.
 template <bool IDX16>
 __device__ __forceinline__ void load_data(const PassArgs& a, int64_t b, int64_t lim, uint32_t le,
                                           Win& w) {
-    const int64_t eb = b + (b + (int64_t)le < lim ? (int64_t)le : 0);
-    const f32x4* vp = reinterpret_cast<const f32x4*>(a.val + eb);
+    const bool in = b + (int64_t)le < lim;
+    const f32x4* vp = reinterpret_cast<const f32x4*>(a.val + b + (in ? (int64_t)(le >> 1) : 0));
     w.v0 = __builtin_nontemporal_load(vp);
-    w.v1 = __builtin_nontemporal_load(vp + 1);
+    w.v1 = __builtin_nontemporal_load(vp + kWin / 8);
+    const int64_t eb = b + (in ? (int64_t)le : 0);
     if constexpr (IDX16) {
         w.c0 = __builtin_nontemporal_load(
             reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + eb));
@@ -406,25 +408,13 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
         }
     }
     if constexpr (N::store) {
-        // Write R-hat back so that each store instruction covers contiguous memory:
-        // lane l writes entries 4l .. 4l + 3 of the window, then 256 + 4l .. 256 + 4l + 3,
-        // which are half (l & 1) of lane l / 2 and of lane 32 + l / 2.  Stores of half
-        // lines from strided lanes cost far more HBM time than whole lines.
-        const int srcA = (lane >> 1) << 2, srcB = (32 + (lane >> 1)) << 2;
-        const bool odd = lane & 1;
-        f32x4 w0, w1;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int lo = __builtin_bit_cast(int, r[k]), hi = __builtin_bit_cast(int, r[4 + k]);
-            const int a0 = __builtin_amdgcn_ds_bpermute(srcA, lo), a1 = __builtin_amdgcn_ds_bpermute(srcA, hi);
-            const int b0 = __builtin_amdgcn_ds_bpermute(srcB, lo), b1 = __builtin_amdgcn_ds_bpermute(srcB, hi);
-            w0[k] = __builtin_bit_cast(float, odd ? a1 : a0);
-            w1[k] = __builtin_bit_cast(float, odd ? b1 : b0);
+        // R-hat back to the lane's two value groups: each store instruction of the
+        // wave covers 1 KB of contiguous memory.
+        if (lv) {
+            f32x4* wp = reinterpret_cast<f32x4*>(a.val + b + (le >> 1));
+            __builtin_nontemporal_store(f32x4{r[0], r[1], r[2], r[3]}, wp);
+            __builtin_nontemporal_store(f32x4{r[4], r[5], r[6], r[7]}, wp + kWin / 8);
         }
-        const int pieces = 2 * nl;  // 4-entry pieces in this window
-        float* wp = a.val + b + 4 * lane;
-        if (lane < pieces) __builtin_nontemporal_store(w0, reinterpret_cast<f32x4*>(wp));
-        if (lane + 64 < pieces) __builtin_nontemporal_store(w1, reinterpret_cast<f32x4*>(wp + 256));
     }
     if constexpr (MODE == kModeFlush) {
         float s2 = 0.0f;
