@@ -53,6 +53,8 @@ def lib():
         L.oracle_train_rmse.argtypes = [P]
         L.oracle_test_rmse.restype = dbl
         L.oracle_test_rmse.argtypes = [P, i64, P, P, P]
+        L.oracle_run_until.restype = ctypes.c_int32
+        L.oracle_run_until.argtypes = [P, i32, i32, ctypes.c_double, i64, P, P, P, P]
         _lib = L
     return _lib
 
@@ -113,6 +115,25 @@ class Oracle:
         if rc:
             raise ValueError("oracle_rank: bad arguments")
         return tr, rh, uh, vh
+
+    def run_until(self, max_outer: int, inner: int, rel_tol: float, test=None):
+        """Algorithm 3 with its outer loop open (see oracle_run_until).  Returns (number
+        of outer iterations run, history array of shape (that number, 3): objective,
+        train RMSE, test RMSE (NaN without a test set))."""
+        if test is None:
+            r = c = a = None
+            tn = 0
+        else:
+            r = np.ascontiguousarray(test[0], dtype=np.int32)
+            c = np.ascontiguousarray(test[1], dtype=np.int32)
+            a = np.ascontiguousarray(test[2], dtype=np.float64)
+            tn = r.size
+        hist = np.zeros((max(int(max_outer), 1), 3))
+        done = lib().oracle_run_until(self._h, int(max_outer), int(inner), float(rel_tol), tn,
+                                      _ptr(r), _ptr(c), _ptr(a), _ptr(hist))
+        if done < 0:
+            raise ValueError("oracle_run_until: bad arguments")
+        return done, hist[:done]
 
     def ccd_run(self, outer: int):
         if lib().oracle_ccd_run(self._h, int(outer)):

@@ -259,6 +259,30 @@ int oracle_run(oracle_ccdpp *o, int32_t outer, int32_t inner, double *trace) {
     return 0;
 }
 
+int oracle_run_until(oracle_ccdpp *o, int32_t max_outer, int32_t inner, double rel_tol,
+                     int64_t test_nnz, const int32_t *test_row, const int32_t *test_col,
+                     const double *test_a, double *history) {
+    if (max_outer < 0 || inner < 1 || test_nnz < 0) return -1;
+    if (test_nnz > 0 && (!test_row || !test_col || !test_a)) return -1;
+    double prev = 0.0;
+    int32_t done = 0;
+    for (int32_t it = 0; it < max_outer; ++it) {
+        int rc = oracle_run(o, 1, inner, NULL);
+        if (rc) return rc;
+        const double f = oracle_objective(o);
+        if (history) {
+            history[3 * (int64_t)it] = f;
+            history[3 * (int64_t)it + 1] = o->nnz > 0 ? oracle_train_rmse(o) : 0.0;
+            history[3 * (int64_t)it + 2] =
+                test_nnz > 0 ? oracle_test_rmse(o, test_nnz, test_row, test_col, test_a) : NAN;
+        }
+        done = it + 1;
+        if (it >= 1 && rel_tol >= 0.0 && prev - f <= rel_tol * prev) break;
+        prev = f;
+    }
+    return done;
+}
+
 int oracle_ccd_run(oracle_ccdpp *o, int32_t outer) {
     if (outer < 0) return -1;
     const int64_t m = o->m, n = o->n, k = o->k;

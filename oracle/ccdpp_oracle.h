@@ -62,6 +62,17 @@ int oracle_run(oracle_ccdpp *o, int32_t outer, int32_t inner, double *trace);
 int oracle_rank(oracle_ccdpp *o, int32_t t, int32_t inner, double *trace,
                 double *rhat, double *u_hist, double *v_hist);
 
+/* Algorithm 3 with its outer loop left open ("until convergence", Section
+ * 3.2.2): outer iterations of oracle_run(o, 1, inner), each followed by the
+ * objective f of eq. 1; stop after iteration o >= 2 when f_(o-1) - f_o <=
+ * rel_tol * f_(o-1), or after max_outer iterations (rel_tol < 0: never early).
+ * history (optional, 3 per iteration run): f, the training RMSE and the RMSE
+ * on the held-out triplets (NaN when test_nnz == 0).  Returns the number of
+ * iterations run, or a negative value on invalid input. */
+int oracle_run_until(oracle_ccdpp *o, int32_t max_outer, int32_t inner, double rel_tol,
+                     int64_t test_nnz, const int32_t *test_row, const int32_t *test_col,
+                     const double *test_a, double *history);
+
 /* Algorithm 2 (element-wise CCD): `outer` iterations of, for every row i and
  * feature t, eq. 5 then eq. 6-7, followed by, for every column j and feature
  * t, eq. 8 then eq. 9-10. */

@@ -11,7 +11,10 @@ by re-typing the oracle's own formulas.
   singular triple, and with k > 1 to the soft-thresholded truncated SVD;
 * k = 1 CCD++ with one inner iteration equals element-wise CCD (Algorithm 2);
 * noiseless low-rank data is recovered as lambda -> 0;
-* results do not depend on the thread count.
+* results do not depend on the thread count;
+* the open outer loop equals single outer iterations, its history equals eq. 1
+  and the RMSEs evaluated from the factors, and it stops at the first
+  iteration whose relative decrease of eq. 1 is within the tolerance.
 """
 import os
 from fractions import Fraction
@@ -241,6 +244,57 @@ def test_train_rmse_matches_prediction_error_on_training_set():
     o = Oracle(m, n, k, lam, row, col, val, H0)
     o.run(2, 2)
     assert abs(o.train_rmse() - o.test_rmse(row, col, val)) < 1e-12
+
+
+def _numpy_objective_and_rmse(W, H, lam, row, col, val, trow, tcol, tval):
+    """Eq. 1 and the two RMSEs evaluated directly from the factors."""
+    pred = np.einsum("ij,ij->i", W[row], H[col])
+    sse = float(np.sum((val - pred) ** 2))
+    f = sse + lam * (float(np.sum(W * W)) + float(np.sum(H * H)))
+    tpred = np.einsum("ij,ij->i", W[trow], H[tcol])
+    return f, np.sqrt(sse / row.size), np.sqrt(float(np.mean((tval - tpred) ** 2)))
+
+
+def test_open_outer_loop_matches_stepwise_runs():
+    # Algorithm 3 with its outer loop open: with early stopping disabled it is the
+    # same computation as single outer iterations, and its history equals eq. 1 and
+    # the RMSEs evaluated from the factors after each iteration.
+    m, n, k, nnz, lam = 60, 45, 3, 700, 0.1
+    row, col, val, H0 = synth.small_random(m, n, nnz, k, seed=8)
+    trow, tcol, tval, _ = synth.small_random(m, n, 120, k, seed=9)
+    a = Oracle(m, n, k, lam, row, col, val, H0)
+    done, hist = a.run_until(5, 2, -1.0, test=(trow, tcol, tval))
+    assert done == 5 and hist.shape == (5, 3)
+    b = Oracle(m, n, k, lam, row, col, val, H0)
+    for it in range(5):
+        b.run(1, 2)
+        W, H = b.factors()
+        f, tr, te = _numpy_objective_and_rmse(W, H, lam, np.asarray(row), np.asarray(col),
+                                              np.asarray(val, np.float64), np.asarray(trow),
+                                              np.asarray(tcol), np.asarray(tval, np.float64))
+        np.testing.assert_allclose(hist[it], [f, tr, te], rtol=1e-10)
+    Wa, Ha = a.factors()
+    Wb, Hb = b.factors()
+    assert np.array_equal(Wa, Wb) and np.array_equal(Ha, Hb)
+    assert np.all(np.diff(hist[:, 0]) <= 1e-12 * hist[:-1, 0])  # CCD++ never increases eq. 1
+    # Without a test set the third column is NaN.
+    c = Oracle(m, n, k, lam, row, col, val, H0)
+    _, h2 = c.run_until(2, 2, -1.0)
+    assert np.all(np.isnan(h2[:, 2]))
+
+
+def test_open_outer_loop_stops_at_first_small_decrease():
+    m, n, k, nnz, lam = 60, 45, 3, 700, 0.1
+    row, col, val, H0 = synth.small_random(m, n, nnz, k, seed=8)
+    _, full = Oracle(m, n, k, lam, row, col, val, H0).run_until(10, 2, -1.0)
+    f = full[:, 0]
+    dec = (f[:-1] - f[1:]) / f[:-1]  # dec[o - 1]: relative decrease into iteration o + 1
+    for tol in (dec[2] * 1.001, dec[4] * 1.001, 0.0):
+        hits = [o + 2 for o in range(len(dec)) if dec[o] <= tol]
+        expect = hits[0] if hits else 10
+        done, hist = Oracle(m, n, k, lam, row, col, val, H0).run_until(10, 2, tol)
+        assert done == expect, (tol, done, expect)
+        np.testing.assert_array_equal(hist, full[:done])
 
 
 def test_rejects_bad_input():
