@@ -116,6 +116,23 @@ int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  */
 int ccdpp_run(ccdpp_t *h, int32_t outer_iters, int32_t inner_iters);
 
+/* Algorithm 3 with its outer loop left open (Section 3.2.2: iterate until
+ * convergence or a bound on the iterations): outer iterations of
+ * ccdpp_run(h, 1, inner_iters), each followed by the objective f of eq. 1
+ * (float64: the training sum of squares plus lambda (||W||^2 + ||H||^2)).
+ * Stops after iteration o >= 2 when f_(o-1) - f_o <= rel_tol * f_(o-1), or
+ * after max_outer iterations; rel_tol < 0 never stops early.
+ *   test_nnz, test_row/col/val : held-out triplets (host memory, copied once),
+ *                                or test_nnz = 0 and NULL pointers
+ *   history    : NULL, or 3 * max_outer doubles; iteration o writes f, the
+ *                training RMSE and the held-out RMSE (NaN without a test set)
+ *                at history[3 o .. 3 o + 2]
+ *   outer_done : receives the number of outer iterations run (not NULL)
+ * Arguments are checked before any iteration runs (EINVAL).  Blocking. */
+int ccdpp_run_until(ccdpp_t *h, int32_t max_outer, int32_t inner_iters, double rel_tol,
+                    int64_t test_nnz, const int32_t *test_row, const int32_t *test_col,
+                    const float *test_val, double *history, int32_t *outer_done);
+
 /* Copy the factors out: W as m x k, H as n x k, row-major float32.  Either
  * pointer may be NULL to skip it.  Blocking. */
 int ccdpp_get_factors(ccdpp_t *h, float *W, float *H);

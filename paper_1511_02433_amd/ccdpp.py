@@ -62,6 +62,8 @@ def lib() -> ctypes.CDLL:
             "ccdpp_create_ex": ([i64, i64, i32, dbl, i64, P, P, P, u64, ctypes.POINTER(Options),
                                  ctypes.POINTER(P)], ctypes.c_int),
             "ccdpp_run": ([P, i32, i32], ctypes.c_int),
+            "ccdpp_run_until": ([P, i32, i32, dbl, i64, P, P, P, P, ctypes.POINTER(i32)],
+                                ctypes.c_int),
             "ccdpp_get_factors": ([P, P, P], ctypes.c_int),
             "ccdpp_set_factors": ([P, P, P], ctypes.c_int),
             "ccdpp_rmse": ([P, i64, P, P, P, ctypes.POINTER(dbl)], ctypes.c_int),
@@ -127,6 +129,26 @@ def ccdpp_create_ex(m, n, k, lam, row, col, val, seed=0, opts=None):
 
 def ccdpp_run(h, outer_iters, inner_iters):
     _check(h, lib().ccdpp_run(h, int(outer_iters), int(inner_iters)))
+
+
+def ccdpp_run_until(h, max_outer, inner_iters, rel_tol, test=None):
+    """Returns (outer iterations run, history (that many x 3): objective of eq. 1,
+    training RMSE, held-out RMSE or NaN)."""
+    if test is None:
+        r = c = v = None
+        tn = 0
+    else:
+        r = np.ascontiguousarray(test[0], dtype=np.int32)
+        c = np.ascontiguousarray(test[1], dtype=np.int32)
+        v = np.ascontiguousarray(test[2], dtype=np.float32)
+        if not (r.size == c.size == v.size):
+            raise ValueError("test row, col and val must have the same length")
+        tn = r.size
+    hist = np.zeros((max(int(max_outer), 1), 3))
+    done = ctypes.c_int32(0)
+    _check(h, lib().ccdpp_run_until(h, int(max_outer), int(inner_iters), float(rel_tol), tn, _p(r),
+                                    _p(c), _p(v), _p(hist), ctypes.byref(done)))
+    return done.value, hist[:done.value]
 
 
 def ccdpp_get_factors(h, m, n, k):
@@ -236,6 +258,9 @@ class CCDPP:
 
     def run(self, outer_iters, inner_iters):
         ccdpp_run(self._h, outer_iters, inner_iters)
+
+    def run_until(self, max_outer, inner_iters, rel_tol, test=None):
+        return ccdpp_run_until(self._h, max_outer, inner_iters, rel_tol, test)
 
     def factors(self):
         return ccdpp_get_factors(self._h, self.m, self.n, self.k)

@@ -862,6 +862,75 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
     return CCDPP_OK;
 }
 
+int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol,
+                    int64_t test_nnz, const int32_t* test_row, const int32_t* test_col,
+                    const float* test_val, double* history, int32_t* outer_done) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (!outer_done) return fail(h, CCDPP_EINVAL, "outer_done is NULL");
+    if (max_outer < 0 || inner < 1)
+        return fail(h, CCDPP_EINVAL, "max_outer must be >= 0 and inner_iters >= 1");
+    if (std::isnan(rel_tol)) return fail(h, CCDPP_EINVAL, "rel_tol is NaN");
+    if (test_nnz < 0 || test_nnz > kMaxNnz)
+        return fail(h, CCDPP_EINVAL, "test_nnz must be in [0, 2^31-1]");
+    if (test_nnz > 0) {
+        if (!test_row || !test_col || !test_val)
+            return fail(h, CCDPP_EINVAL, "test arrays must be non-NULL when test_nnz > 0");
+        for (int64_t e = 0; e < test_nnz; ++e) {
+            if (test_row[e] < 0 || test_row[e] >= h->m || test_col[e] < 0 || test_col[e] >= h->n)
+                return fail(h, CCDPP_EINVAL, "test entry %lld out of range", (long long)e);
+            if (!std::isfinite(test_val[e]))
+                return fail(h, CCDPP_EINVAL, "test value %lld is not finite", (long long)e);
+        }
+    }
+    hipStream_t s = h->stream;
+    int32_t *dr = nullptr, *dc = nullptr;
+    float* dv = nullptr;
+    Tmp tr, tc, tv;
+    if (test_nnz > 0) {
+        HIPCK(h, talloc(tr, &dr, test_nnz));
+        HIPCK(h, talloc(tc, &dc, test_nnz));
+        HIPCK(h, talloc(tv, &dv, test_nnz));
+        HIPCK(h, hipMemcpyAsync(dr, test_row, test_nnz * 4, hipMemcpyHostToDevice, s));
+        HIPCK(h, hipMemcpyAsync(dc, test_col, test_nnz * 4, hipMemcpyHostToDevice, s));
+        HIPCK(h, hipMemcpyAsync(dv, test_val, test_nnz * 4, hipMemcpyHostToDevice, s));
+    }
+    // A fixed-order float64 sum on the device, read back.
+    auto reduce = [&](double* out) -> int {
+        HIPCK(h, ccdk::launch_reduce_sum(h->sse_part, kReduceParts, h->d_scalar, s));
+        HIPCK(h, hipMemcpyAsync(out, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
+        HIPCK(h, hipStreamSynchronize(s));
+        return CCDPP_OK;
+    };
+    double prev = 0.0;
+    int32_t done = 0;
+    for (int32_t it = 0; it < max_outer; ++it) {
+        RCK(ccdpp_run(h, 1, inner));
+        double w2 = 0.0, h2 = 0.0, te = std::nan("");
+        HIPCK(h, ccdk::launch_sq_sum(h->W, h->m * h->k, h->sse_part, kReduceParts, s));
+        RCK(reduce(&w2));
+        HIPCK(h, ccdk::launch_sq_sum(h->H, h->n * h->k, h->sse_part, kReduceParts, s));
+        RCK(reduce(&h2));
+        if (test_nnz > 0) {
+            HIPCK(h, ccdk::launch_test_err(dr, dc, dv, test_nnz, h->rold2new, h->cold2new, h->W,
+                                           h->H, h->m, h->n, h->k, h->sse_part, kReduceParts, s));
+            double sum = 0.0;
+            RCK(reduce(&sum));
+            te = std::sqrt(sum / (double)test_nnz);
+        }
+        const double f = h->train_sse + h->lambda * (w2 + h2);
+        if (history) {
+            history[3 * (int64_t)it] = f;
+            history[3 * (int64_t)it + 1] = h->nnz > 0 ? std::sqrt(h->train_sse / (double)h->nnz) : 0.0;
+            history[3 * (int64_t)it + 2] = te;
+        }
+        done = it + 1;
+        if (it >= 1 && rel_tol >= 0.0 && prev - f <= rel_tol * prev) break;
+        prev = f;
+    }
+    *outer_done = done;
+    return CCDPP_OK;
+}
+
 int ccdpp_get_factors(ccdpp_t* h, float* W, float* H) {
     if (!usable(h)) return CCDPP_ESTATE;
     hipStream_t s = h->stream;
