@@ -34,18 +34,19 @@ LAYOUT_NAMES = {0: "rows", 1: "cols"}
 
 def kernel_symbol(kind: int, info: dict, layout: int) -> str:
     """The kernel's name as a trace shows it (the sweep kernels are templated on
-    LDS staging, 16-bit indices and P == 1)."""
+    LDS staging, 16-bit indices, P == 1 and the value type)."""
+    v = "double" if info.get("value_bytes", 4) == 8 else "float"
     if kind == 2:
-        return "ccdk::ccd_combine(ccdk::CombineArgs)"
+        return f"void ccdk::ccd_combine<{v}>(ccdk::CombineArgs<{v}>)"
     if kind == 3:
-        return "ccdk::ccd_copy(float const*, float*, long)"
+        return f"void ccdk::ccd_copy<{v}>({v} const*, {v}*, long)"
     pre = "u" if layout == 0 else "v"
     staged = info[f"{pre}_gather"] == 2
-    idx16 = staged or info[f"{pre}_tile_width"] < 65536
+    idx16 = staged or info[f"{pre}_tile_width"] < 32768
     p1 = info[f"{pre}_tiles"] == 1
     name = KERNEL_NAMES[kind]
     b = lambda x: "true" if x else "false"
-    return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}>(ccdk::PassArgs)"
+    return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}, {v}>(ccdk::PassArgs<{v}>)"
 
 
 def log(msg):
@@ -60,10 +61,11 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(key: str, workload: str):
+def stored_traffic(key: str, workload: str, precision: str = "f32"):
     """HBM bytes per launch of kernel `key` ("ccd_pass/cols", ...) from the committed
     rocprofv3 counter summary, if it was taken on the current kernel source; else None."""
-    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    suffix = "" if precision == "f32" else f"_{precision}"
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}{suffix}.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:
@@ -107,6 +109,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--precision", default="f32", choices=["f32", "f64"],
+                    help="value type of the residual, factors and sweep arithmetic")
     ap.add_argument("--no-open-loop", action="store_true",
                     help="skip the open-loop (run until converged) measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -141,7 +145,9 @@ def main():
     inner = w.inner
     log(f"workload {w.describe()} (k={k})")
 
-    g = CCDPP(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val)
+    from paper_1511_02433_amd.ccdpp import make_options
+    g = CCDPP(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val,
+              opts=make_options(precision=1 if args.precision == "f64" else 0))
     g.use_torch_stream()
     g.set_factors(np.zeros((w.m, k), np.float32), ds.h0(k))
     info = g.info()
@@ -223,7 +229,7 @@ def main():
         roofline = {"kernel": d["kernel"], "layout": dom.split("/")[1], "bound": "hbm",
                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": stored_traffic(dom, w.name), "mean_us": live["mean_us"],
+                    "traffic": stored_traffic(dom, w.name, args.precision), "mean_us": live["mean_us"],
                     "launches": live["launches"],
                     "algo_bytes_per_launch": live["algo_bytes_per_launch"]}
     train_rmse = g.train_rmse()
@@ -266,7 +272,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": args.precision,
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.m}x{w.n}, nnz={w.nnz}, k={k}, lambda={w.lam}, "
                                f"inner={inner}; step = 1 outer iteration",

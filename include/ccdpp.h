@@ -93,6 +93,10 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 4;
  *                 -1: shares by entries alone)
+ *   precision   : 0 float32 residual, factors and sweep arithmetic (the
+ *                 paper's float version, Section 8); 1 float64 throughout
+ *                 (its double version).  Partial sums across windows and the
+ *                 coordinate division are float64 in both.
  * Results differ between layouts only by floating-point summation order.
  */
 typedef struct ccdpp_options {
@@ -100,6 +104,7 @@ typedef struct ccdpp_options {
     int32_t tile_width[2];
     int32_t workgroups;
     int32_t seg_weight;
+    int32_t precision;
 } ccdpp_options_t;
 
 /* ccdpp_create with explicit layout options (opts may be NULL). */
@@ -136,11 +141,15 @@ int ccdpp_run_until(ccdpp_t *h, int32_t max_outer, int32_t inner_iters, double r
 /* Copy the factors out: W as m x k, H as n x k, row-major float32.  Either
  * pointer may be NULL to skip it.  Blocking. */
 int ccdpp_get_factors(ccdpp_t *h, float *W, float *H);
+/* The same in float64 (exact for a float64 handle). */
+int ccdpp_get_factors_f64(ccdpp_t *h, double *W, double *H);
 
 /* Replace the factors (row-major m x k and n x k, finite; either may be NULL
  * to keep the current one) and rebuild the residual R = A - W H^T on Omega
  * (Section 3.2) on the device.  Blocking. */
 int ccdpp_set_factors(ccdpp_t *h, const float *W, const float *H);
+/* The same from float64 arrays (rounded to float on a float32 handle). */
+int ccdpp_set_factors_f64(ccdpp_t *h, const double *W, const double *H);
 
 /* Root mean squared error of the predictions w_i^T h_j against held-out
  * triplets (Section 8: RMSE on the probe set; predictions are not clipped):
@@ -156,6 +165,8 @@ int ccdpp_train_rmse(ccdpp_t *h, double *rmse_out);
 /* Residual R in the order of the triplets given to ccdpp_create
  * (float32[nnz]).  Diagnostic.  Blocking. */
 int ccdpp_get_residual(ccdpp_t *h, float *R);
+/* The same in float64 (exact for a float64 handle). */
+int ccdpp_get_residual_f64(ccdpp_t *h, double *R);
 
 /* Count the observed entries whose residual differs, bit for bit, between
  * the row-compressed and the column-compressed device copies (0 when the two
@@ -196,7 +207,7 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   [5] user-major copy gather mode (1 global memory, 2 LDS-staged),
  *   [6] its number of tiles P, [7] tile width T, [8] persistent workgroups per
  *   pass, [9] row segments, [10..14] the same five for the item-major copy,
- *   [15] device bytes held.
+ *   [15] device bytes held, [16] bytes per value (4: float, 8: double).
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

@@ -27,15 +27,19 @@ class Options(ctypes.Structure):
     """ccdpp_options_t: layout knobs (0 = automatic).  Index 0 is the user-major copy,
     1 the item-major copy.  gather_mode: 1 global memory, 2 LDS-staged."""
     _fields_ = [("gather_mode", ctypes.c_int32 * 2), ("tile_width", ctypes.c_int32 * 2),
-                ("workgroups", ctypes.c_int32), ("seg_weight", ctypes.c_int32)]
+                ("workgroups", ctypes.c_int32), ("seg_weight", ctypes.c_int32),
+                ("precision", ctypes.c_int32)]
 
 
-def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight=0) -> Options:
+def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight=0,
+                 precision=0) -> Options:
+    """precision: 0 float32 residual and factors, 1 float64."""
     o = Options()
     o.gather_mode[0], o.gather_mode[1] = gather_mode
     o.tile_width[0], o.tile_width[1] = tile_width
     o.workgroups = workgroups
     o.seg_weight = seg_weight
+    o.precision = precision
     return o
 
 
@@ -65,10 +69,13 @@ def lib() -> ctypes.CDLL:
             "ccdpp_run_until": ([P, i32, i32, dbl, i64, P, P, P, P, ctypes.POINTER(i32)],
                                 ctypes.c_int),
             "ccdpp_get_factors": ([P, P, P], ctypes.c_int),
+            "ccdpp_get_factors_f64": ([P, P, P], ctypes.c_int),
             "ccdpp_set_factors": ([P, P, P], ctypes.c_int),
+            "ccdpp_set_factors_f64": ([P, P, P], ctypes.c_int),
             "ccdpp_rmse": ([P, i64, P, P, P, ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_train_rmse": ([P, ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_get_residual": ([P, P], ctypes.c_int),
+            "ccdpp_get_residual_f64": ([P, P], ctypes.c_int),
             "ccdpp_check_consistency": ([P, ctypes.POINTER(i64)], ctypes.c_int),
             "ccdpp_set_stream": ([P, P], ctypes.c_int),
             "ccdpp_profile": ([P, i32], ctypes.c_int),
@@ -158,10 +165,23 @@ def ccdpp_get_factors(h, m, n, k):
     return W, H
 
 
+def ccdpp_get_factors_f64(h, m, n, k):
+    W = np.empty((m, k), dtype=np.float64)
+    H = np.empty((n, k), dtype=np.float64)
+    _check(h, lib().ccdpp_get_factors_f64(h, _p(W), _p(H)))
+    return W, H
+
+
 def ccdpp_set_factors(h, W=None, H=None):
     W = None if W is None else np.ascontiguousarray(W, dtype=np.float32)
     H = None if H is None else np.ascontiguousarray(H, dtype=np.float32)
     _check(h, lib().ccdpp_set_factors(h, _p(W), _p(H)))
+
+
+def ccdpp_set_factors_f64(h, W=None, H=None):
+    W = None if W is None else np.ascontiguousarray(W, dtype=np.float64)
+    H = None if H is None else np.ascontiguousarray(H, dtype=np.float64)
+    _check(h, lib().ccdpp_set_factors_f64(h, _p(W), _p(H)))
 
 
 def ccdpp_rmse(h, row, col, val):
@@ -182,6 +202,12 @@ def ccdpp_train_rmse(h):
 def ccdpp_get_residual(h, nnz):
     R = np.empty(nnz, dtype=np.float32)
     _check(h, lib().ccdpp_get_residual(h, _p(R)))
+    return R
+
+
+def ccdpp_get_residual_f64(h, nnz):
+    R = np.empty(nnz, dtype=np.float64)
+    _check(h, lib().ccdpp_get_residual_f64(h, _p(R)))
     return R
 
 
@@ -212,7 +238,7 @@ def ccdpp_profile_read(h, kind, layout=-1):
 
 INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_width",
                "u_workgroups", "u_segments", "v_gather", "v_tiles", "v_tile_width", "v_workgroups",
-               "v_segments", "device_bytes")
+               "v_segments", "device_bytes", "value_bytes")
 
 
 def ccdpp_info(h):
@@ -267,6 +293,15 @@ class CCDPP:
 
     def set_factors(self, W=None, H=None):
         ccdpp_set_factors(self._h, W, H)
+
+    def factors_f64(self):
+        return ccdpp_get_factors_f64(self._h, self.m, self.n, self.k)
+
+    def set_factors_f64(self, W=None, H=None):
+        ccdpp_set_factors_f64(self._h, W, H)
+
+    def residual_f64(self):
+        return ccdpp_get_residual_f64(self._h, self.nnz)
 
     def rmse(self, row, col, val):
         return ccdpp_rmse(self._h, row, col, val)

@@ -54,12 +54,15 @@ struct ccdpp {
     int32_t* perm0 = nullptr;      // e -> input triplet index
     int32_t* pos0 = nullptr;       // e -> value slot in the user-major copy
     int32_t* map01 = nullptr;      // e -> value slot in the item-major copy
-    float* A = nullptr;            // A[e], the rating of entry e
-    float* fseg[2] = {};           // P > 1: own factor columns spread over segments (k x S)
-    float* W = nullptr;            // k x m: W[t*m + i]
-    float* H = nullptr;            // k x n
-    float* u = nullptr;
-    float* v = nullptr;
+    // Value type of the residual, the factors and the sweep arithmetic: float, or
+    // double with options.precision = 1.  The arrays below hold that type.
+    bool dbl = false;
+    void* A = nullptr;             // A[e], the rating of entry e
+    void* fseg[2] = {};            // P > 1: own factor columns spread over segments (k x S)
+    void* W = nullptr;             // k x m: W[t*m + i]
+    void* H = nullptr;             // k x n
+    void* u = nullptr;
+    void* v = nullptr;
     double* sse_part = nullptr;
     int32_t sse_nparts = 0;
     double* d_scalar = nullptr;
@@ -112,6 +115,16 @@ int fail(ccdpp* h, int code, const char* fmt, ...) {
         int r_ = (expr);               \
         if (r_ != CCDPP_OK) return r_; \
     } while (0)
+
+// Calls f with a value of the handle's value type (float or double).
+template <class F>
+auto with_value_type(const ccdpp* h, F&& f) {
+    return h->dbl ? f(double{}) : f(float{});
+}
+template <class V>
+V* as(void* p) {
+    return static_cast<V*>(p);
+}
 
 template <class T>
 hipError_t dalloc(ccdpp* h, T** p, int64_t count) {
@@ -201,7 +214,8 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     const int nvec = side == 0 ? 2 : 3;
     // Each staged slice holds T floats rounded up to 32, then 32 more words whose first
     // is the zero the padding entries read.
-    const int64_t tmax = ((int64_t)kLdsVecBytes / (4 * nvec) - 64) / 64 * 64;
+    const int64_t vbytes = h->dbl ? 8 : 4;
+    const int64_t tmax = ((int64_t)kLdsVecBytes / (vbytes * nvec) - 64) / 64 * 64;
     const int forced = opt ? opt->gather_mode[side] : 0;
     const int64_t forced_T = opt ? opt->tile_width[side] : 0;
     if (forced_T > tmax)
@@ -453,8 +467,14 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     if (cbits + sbits > 64) return fail(h, CCDPP_EDEVICE, "internal: sort key too wide");
     // Padding entries (and kEntryPad more after the end, for whole-lane vector loads)
     // hold value 0 and the padding index T.
-    HIPCK(h, dalloc(h, &L.val, NP + kEntryPad));
-    HIPCK(h, launch_fill(L.val, 0.0f, NP + kEntryPad, s));
+    RCK(with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        V* pv;
+        HIPCK(h, dalloc(h, &pv, NP + kEntryPad));
+        L.val = pv;
+        HIPCK(h, launch_fill<V>(pv, V(0), NP + kEntryPad, s));
+        return CCDPP_OK;
+    }));
     if (L.idx16) {
         uint16_t* d;
         HIPCK(h, dalloc(h, &d, NP + kEntryPad));
@@ -495,8 +515,12 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             HIPCK(h, hipStreamSynchronize(s));
             if (flag) return fail(h, CCDPP_EDUP, "a position (i, j) occurs more than once");
         }
-        HIPCK(h, launch_layout_fill(k1, perm, val_in, N, cbits, d_off, L.swz, L.idx16, L.idx, L.val, epos,
-                                    s));
+        RCK(with_value_type(h, [&](auto z) -> int {
+            using V = decltype(z);
+            HIPCK(h, launch_layout_fill<V>(k1, perm, val_in, N, cbits, d_off, L.swz, L.idx16, L.idx,
+                                           as<V>(L.val), epos, s));
+            return CCDPP_OK;
+        }));
         HIPCK(h, hipStreamSynchronize(s));
     }
     return CCDPP_OK;
@@ -504,13 +528,17 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
 
 // Refresh the per-segment copies of W (user-major copy) and H (item-major copy).
 int spread_factors(ccdpp* h) {
-    for (int li = 0; li < 2; ++li)
-        if (h->fseg[li]) {
-            const Layout& L = h->L[li];
-            HIPCK(h, ccdk::launch_seg_spread(li == 0 ? h->W : h->H, L.rows, L.seg_row, L.nseg,
-                                             h->k, h->fseg[li], h->stream));
-        }
-    return CCDPP_OK;
+    return with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        for (int li = 0; li < 2; ++li)
+            if (h->fseg[li]) {
+                const Layout& L = h->L[li];
+                HIPCK(h, ccdk::launch_seg_spread<V>(as<V>(li == 0 ? h->W : h->H), L.rows,
+                                                    L.seg_row, L.nseg, h->k, as<V>(h->fseg[li]),
+                                                    h->stream));
+            }
+        return CCDPP_OK;
+    });
 }
 
 int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float* val,
@@ -589,38 +617,48 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, launch_compose(pos1, e01, N, h->map01, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
-    HIPCK(h, dalloc(h, &h->A, N));
-    HIPCK(h, launch_copy_mapped(h->L[0].val, h->pos0, h->A, nullptr, N, s));
-
-    // Factors: W = 0 (Algorithm 3), H from the seed; scratch.
-    HIPCK(h, dalloc(h, &h->W, (int64_t)h->k * m));
-    HIPCK(h, dalloc(h, &h->H, (int64_t)h->k * n));
-    HIPCK(h, dalloc(h, &h->u, m));
-    HIPCK(h, dalloc(h, &h->v, n));
     h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid) * kWaves, kReduceParts);
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
     HIPCK(h, dalloc(h, &h->d_count, 1));
-    HIPCK(h, launch_fill(h->W, 0.0f, (int64_t)h->k * m, s));
-    HIPCK(h, launch_fill(h->u, 0.0f, m, s));
-    HIPCK(h, launch_fill(h->v, 0.0f, n, s));
-    for (int li = 0; li < 2; ++li) {
-        // Partials are written before they are read: start them as NaN.
-        HIPCK(h, launch_fill(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
-                             4 * h->L[li].nslots, s));
-        if (h->L[li].P > 1) HIPCK(h, dalloc(h, &h->fseg[li], (int64_t)h->k * h->L[li].nseg));
-    }
-    {
+    for (int li = 0; li < 2; ++li)  // partials are written before they are read: start them as NaN
+        HIPCK(h, launch_fill<float>(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
+                                    4 * h->L[li].nslots, s));
+    RCK(with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        V *A, *W, *H, *u, *v;
+        HIPCK(h, dalloc(h, &A, N));
+        HIPCK(h, (launch_copy_mapped<V, V>(as<V>(h->L[0].val), h->pos0, A, nullptr, N, s)));
+        // Factors: W = 0 (Algorithm 3), H from the seed; scratch.
+        HIPCK(h, dalloc(h, &W, (int64_t)h->k * m));
+        HIPCK(h, dalloc(h, &H, (int64_t)h->k * n));
+        HIPCK(h, dalloc(h, &u, m));
+        HIPCK(h, dalloc(h, &v, n));
+        h->A = A;
+        h->W = W;
+        h->H = H;
+        h->u = u;
+        h->v = v;
+        HIPCK(h, launch_fill<V>(W, V(0), (int64_t)h->k * m, s));
+        HIPCK(h, launch_fill<V>(u, V(0), m, s));
+        HIPCK(h, launch_fill<V>(v, V(0), n, s));
+        for (int li = 0; li < 2; ++li)
+            if (h->L[li].P > 1) {
+                V* f;
+                HIPCK(h, dalloc(h, &f, (int64_t)h->k * h->L[li].nseg));
+                h->fseg[li] = f;
+            }
         std::vector<float> h0((size_t)n * h->k);
         for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
         float* d_h0;
         Tmp th0;
         HIPCK(h, talloc(th0, &d_h0, n * h->k));
         HIPCK(h, hipMemcpyAsync(d_h0, h0.data(), h0.size() * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, launch_scatter_factor_in(d_h0, h->cnew2old, n, h->k, h->H, s));
+        HIPCK(h, (launch_scatter_factor_in<float, V>(d_h0, h->cnew2old, n, h->k, H, s)));
         RCK(spread_factors(h));
         HIPCK(h, hipStreamSynchronize(s));
-    }
+        return CCDPP_OK;
+    }));
     h->pending = -1;
     h->build_us = std::chrono::duration_cast<std::chrono::microseconds>(
                       std::chrono::steady_clock::now() - t0)
@@ -695,48 +733,51 @@ void collect_profile(ccdpp* h) {
 // Algorithmic bytes of one pass over layout L (see ccdpp_profile_read): index and
 // value arrays, residual write-back, per-segment row scalars, outputs, and every
 // gathered vector read once.
-double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors) {
+double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors, double vb) {
     using namespace ccdk;
     const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
-    double b = (L.idx16 ? 2.0 : 4.0) * nnz + 4.0 * nnz;
-    if (mode != kModePlain) b += 4.0 * nnz;
-    if (mode != kModeFlush) b += L.P == 1 ? 4.0 * S : 16.0 * S;
-    if (mode == kModeAdd || mode == kModeSubAdd) b += 4.0 * S;
-    if (mode == kModeSubAdd || mode == kModeFlush) b += 4.0 * S;
-    b += 4.0 * cols * gathered_vectors;
+    double b = (L.idx16 ? 2.0 : 4.0) * nnz + vb * nnz;
+    if (mode != kModePlain) b += vb * nnz;
+    if (mode != kModeFlush) b += L.P == 1 ? vb * S : 16.0 * S;
+    if (mode == kModeAdd || mode == kModeSubAdd) b += vb * S;
+    if (mode == kModeSubAdd || mode == kModeFlush) b += vb * S;
+    b += vb * cols * gathered_vectors;
     return b;
 }
 
 // Own factor column t of layout li as the pass reads it: by segment, which with
 // P == 1 is the column itself.
-float* seg_col(ccdpp* h, int li, int32_t t) {
+template <class V>
+V* seg_col(ccdpp* h, int li, int32_t t) {
     const Layout& L = h->L[li];
     if (t < 0) return nullptr;
-    if (L.P == 1) return (li == 0 ? h->W : h->H) + (int64_t)t * L.rows;
-    return h->fseg[li] + (int64_t)t * L.nseg;
+    if (L.P == 1) return as<V>(li == 0 ? h->W : h->H) + (int64_t)t * L.rows;
+    return as<V>(h->fseg[li]) + (int64_t)t * L.nseg;
 }
 
 // One pass over layout li, then (P > 1) the combine, which also refreshes the
 // per-segment copy of column `commit` when the pass produces a committed column.
-int pass(ccdpp* h, int li, ccdk::PassMode mode, const float* x, int32_t pcol, int32_t ppcol,
-         const float* q, const float* qq, float* y, int32_t commit, int gathered) {
+template <class V>
+int pass(ccdpp* h, int li, ccdk::PassMode mode, const V* x, int32_t pcol, int32_t ppcol,
+         const V* q, const V* qq, V* y, int32_t commit, int gathered) {
     const Layout& L = h->L[li];
     const int kind = mode == ccdk::kModePlain ? CCDPP_K_PASS
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
                                                 : CCDPP_K_PASS_FUSED;
+    const double vb = sizeof(V);
     {
-        Timed tm(h, kind, li, pass_bytes(L, mode, gathered));
-        HIPCK(h, ccdk::launch_pass(L, mode, x, seg_col(h, li, pcol), seg_col(h, li, ppcol), q, qq,
-                                   y, h->lambda, h->sse_part, h->stream));
+        Timed tm(h, kind, li, pass_bytes(L, mode, gathered, vb));
+        HIPCK(h, ccdk::launch_pass<V>(L, mode, x, seg_col<V>(h, li, pcol), seg_col<V>(h, li, ppcol),
+                                      q, qq, y, h->lambda, h->sse_part, h->stream));
         tm.done();
     }
     if (mode != ccdk::kModeFlush && L.ncomb > 0) {
-        float* yseg = commit >= 0 && L.P > 1 ? seg_col(h, li, commit) : nullptr;
+        V* yseg = commit >= 0 && L.P > 1 ? seg_col<V>(h, li, commit) : nullptr;
         // Partial slots read (16 B) and listed (4 B), per row a list bound, an id and y;
         // with yseg the segment list and the per-segment copy.
         Timed tc(h, CCDPP_K_COMBINE, li,
-                 20.0 * L.nsrc + 12.0 * L.ncomb + (yseg ? 12.0 * L.nseg : 0.0));
-        HIPCK(h, ccdk::launch_combine(L, y, yseg, h->lambda, h->stream));
+                 20.0 * L.nsrc + (8.0 + vb) * L.ncomb + (yseg ? (4.0 + vb) * L.nseg : 0.0));
+        HIPCK(h, ccdk::launch_combine<V>(L, y, yseg, h->lambda, h->stream));
         tc.done();
     }
     return CCDPP_OK;
@@ -763,6 +804,8 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
         }
         if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
         if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
+        if (opts->precision != 0 && opts->precision != 1)
+            return fail(nullptr, CCDPP_EINVAL, "precision must be 0 (float) or 1 (double)");
     }
     for (int64_t e = 0; e < nnz; ++e) {
         if (row[e] < 0 || row[e] >= m)
@@ -779,6 +822,7 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
     h->k = k;
     h->lambda = lambda;
     h->nnz = nnz;
+    h->dbl = opts && opts->precision == 1;
     int rc = create_device(h, row, col, val, seed, opts);
     if (rc != CCDPP_OK) {
         g_create_error = h->err;
@@ -790,6 +834,174 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
     return CCDPP_OK;
 }
 
+}  // namespace
+
+namespace {
+// Fixed-order device sums into h->sse_part (kReduceParts parts) for the value type.
+int launch_sq_sum_any(ccdpp* h, void* p, int64_t n) {
+    return with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        HIPCK(h, ccdk::launch_sq_sum<V>(as<V>(p), n, h->sse_part, kReduceParts, h->stream));
+        return CCDPP_OK;
+    });
+}
+int launch_test_err_any(ccdpp* h, const int32_t* dr, const int32_t* dc, const float* dv,
+                        int64_t nnz) {
+    return with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        HIPCK(h, ccdk::launch_test_err<V>(dr, dc, dv, nnz, h->rold2new, h->cold2new, as<V>(h->W),
+                                          as<V>(h->H), h->m, h->n, h->k, h->sse_part, kReduceParts,
+                                          h->stream));
+        return CCDPP_OK;
+    });
+}
+
+template <class V>
+int run_impl(ccdpp* h, int32_t outer, int32_t inner) {
+    using namespace ccdk;
+    const int64_t m = h->m, n = h->n;
+    V* const W = as<V>(h->W);
+    V* const H = as<V>(h->H);
+    V* const u = as<V>(h->u);
+    V* const v = as<V>(h->v);
+    for (int32_t it = 0; it < outer; ++it) {
+        for (int32_t t = 0; t < h->k; ++t) {
+            V* Wt = W + (int64_t)t * m;
+            V* Ht = H + (int64_t)t * n;
+            const bool prev = h->pending >= 0;
+            const V* Wp = prev ? W + (int64_t)h->pending * m : nullptr;
+            const V* Hp = prev ? H + (int64_t)h->pending * n : nullptr;
+            const PassMode first = prev ? kModeSubAdd : kModeAdd;
+            const int32_t pend = prev ? h->pending : -1;
+            const int g1 = prev ? 2 : 1;
+            const int32_t c1 = inner == 1 ? t : -1;  // with one inner pass, u and v are committed
+            // First u-pass: eq. 18 of the pending feature, eq. 13, eq. 15 with v = hbar_t.
+            RCK(pass<V>(h, 0, first, Ht, t, pend, Ht, Hp, u, c1, g1));
+            // First v-pass: the same residual update on the item-major copy, eq. 16 with the new u.
+            V* yv = inner == 1 ? Ht : v;
+            RCK(pass<V>(h, 1, first, u, t, pend, Wt, Wp, yv, c1, g1 + 1));
+            for (int32_t s = 2; s <= inner; ++s) {
+                const bool last = s == inner;
+                V* yu = last ? Wt : u;  // the last u is committed in place (eq. 17)
+                RCK(pass<V>(h, 0, kModePlain, v, -1, -1, nullptr, nullptr, yu, last ? t : -1, 1));
+                RCK(pass<V>(h, 1, kModePlain, yu, -1, -1, nullptr, nullptr, last ? Ht : v,
+                            last ? t : -1, 1));
+            }
+            if (inner == 1) {
+                Timed tm(h, CCDPP_K_COMMIT, 0, 2.0 * sizeof(V) * m);
+                HIPCK(h, launch_copy<V>(u, Wt, m, h->stream));
+                tm.done();
+            }
+            h->pending = t;
+        }
+    }
+    if (h->pending >= 0) {
+        // Final eq. 18 on both copies; the user-major one also sums R^2 for the training RMSE.
+        const V* Wp = W + (int64_t)h->pending * m;
+        const V* Hp = H + (int64_t)h->pending * n;
+        RCK(pass<V>(h, 0, kModeFlush, nullptr, -1, h->pending, nullptr, Hp, nullptr, -1, 1));
+        HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
+        RCK(pass<V>(h, 1, kModeFlush, nullptr, -1, h->pending, nullptr, Wp, nullptr, -1, 1));
+        h->pending = -1;
+        double sse = 0.0;
+        HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
+        HIPCK(h, hipStreamSynchronize(h->stream));
+        h->train_sse = h->L[0].grid ? sse : 0.0;
+        h->train_sse_valid = true;
+    } else {
+        HIPCK(h, hipStreamSynchronize(h->stream));
+    }
+    if (h->prof) collect_profile(h);
+    return CCDPP_OK;
+}
+
+template <class S>
+int get_factors_impl(ccdpp* h, S* W, S* H) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    hipStream_t s = h->stream;
+    return with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        if (W) {
+            S* d;
+            Tmp t;
+            HIPCK(h, talloc(t, &d, h->m * h->k));
+            HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->W), h->rold2new, h->m, h->k, d, s)));
+            HIPCK(h, hipMemcpyAsync(W, d, h->m * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
+            HIPCK(h, hipStreamSynchronize(s));
+        }
+        if (H) {
+            S* d;
+            Tmp t;
+            HIPCK(h, talloc(t, &d, h->n * h->k));
+            HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->H), h->cold2new, h->n, h->k, d, s)));
+            HIPCK(h, hipMemcpyAsync(H, d, h->n * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
+            HIPCK(h, hipStreamSynchronize(s));
+        }
+        return CCDPP_OK;
+    });
+}
+
+template <class S>
+int set_factors_impl(ccdpp* h, const S* W, const S* H) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (W)
+        for (int64_t e = 0; e < h->m * h->k; ++e)
+            if (!std::isfinite(W[e]))
+                return fail(h, CCDPP_EINVAL, "W[%lld] is not finite", (long long)e);
+    if (H)
+        for (int64_t e = 0; e < h->n * h->k; ++e)
+            if (!std::isfinite(H[e]))
+                return fail(h, CCDPP_EINVAL, "H[%lld] is not finite", (long long)e);
+    hipStream_t s = h->stream;
+    RCK(with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        if (W) {
+            S* d;
+            Tmp t;
+            HIPCK(h, talloc(t, &d, h->m * h->k));
+            HIPCK(h, hipMemcpyAsync(d, W, h->m * h->k * sizeof(S), hipMemcpyHostToDevice, s));
+            HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(d, h->rnew2old, h->m, h->k, as<V>(h->W), s)));
+            HIPCK(h, hipStreamSynchronize(s));
+        }
+        if (H) {
+            S* d;
+            Tmp t;
+            HIPCK(h, talloc(t, &d, h->n * h->k));
+            HIPCK(h, hipMemcpyAsync(d, H, h->n * h->k * sizeof(S), hipMemcpyHostToDevice, s));
+            HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(d, h->cnew2old, h->n, h->k, as<V>(h->H), s)));
+            HIPCK(h, hipStreamSynchronize(s));
+        }
+        RCK(spread_factors(h));
+        HIPCK(h, ccdk::launch_rebuild_residual<V>(h->L[0], h->pos0, as<V>(h->A), as<V>(h->W),
+                                                  as<V>(h->H), h->m, h->n, h->k, s));
+        HIPCK(h, (ccdk::launch_copy_mapped<V, V>(as<V>(h->L[0].val), h->pos0, as<V>(h->L[1].val),
+                                                h->map01, h->nnz, s)));
+        HIPCK(h, hipStreamSynchronize(s));
+        return CCDPP_OK;
+    }));
+    h->pending = -1;
+    h->train_sse_valid = false;
+    return CCDPP_OK;
+}
+
+template <class S>
+int get_residual_impl(ccdpp* h, S* R) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (!R && h->nnz) return fail(h, CCDPP_EINVAL, "R is NULL");
+    if (h->nnz == 0) return CCDPP_OK;
+    hipStream_t s = h->stream;
+    S* d;
+    Tmp t;
+    HIPCK(h, talloc(t, &d, h->nnz));
+    RCK(with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        HIPCK(h, (ccdk::launch_copy_mapped<V, S>(as<V>(h->L[0].val), h->pos0, d, h->perm0, h->nnz, s)));
+        return CCDPP_OK;
+    }));
+    HIPCK(h, hipMemcpyAsync(R, d, h->nnz * sizeof(S), hipMemcpyDeviceToHost, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    return CCDPP_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -805,61 +1017,12 @@ int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
     return create_impl(m, n, k, lambda, nnz, row, col, val, seed, opts, out);
 }
 
+
 int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
-    using namespace ccdk;
     if (!usable(h)) return CCDPP_ESTATE;
     if (outer < 0 || inner < 1)
         return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0 and inner_iters >= 1");
-    const int64_t m = h->m, n = h->n;
-    for (int32_t it = 0; it < outer; ++it) {
-        for (int32_t t = 0; t < h->k; ++t) {
-            float* Wt = h->W + (int64_t)t * m;
-            float* Ht = h->H + (int64_t)t * n;
-            const bool prev = h->pending >= 0;
-            const float* Wp = prev ? h->W + (int64_t)h->pending * m : nullptr;
-            const float* Hp = prev ? h->H + (int64_t)h->pending * n : nullptr;
-            const PassMode first = prev ? kModeSubAdd : kModeAdd;
-            const int32_t pend = prev ? h->pending : -1;
-            const int g1 = prev ? 2 : 1;
-            const int32_t c1 = inner == 1 ? t : -1;  // with one inner pass, u and v are committed
-            // First u-pass: eq. 18 of the pending feature, eq. 13, eq. 15 with v = hbar_t.
-            RCK(pass(h, 0, first, Ht, t, pend, Ht, Hp, h->u, c1, g1));
-            // First v-pass: the same residual update on the item-major copy, eq. 16 with the new u.
-            float* yv = inner == 1 ? Ht : h->v;
-            RCK(pass(h, 1, first, h->u, t, pend, Wt, Wp, yv, c1, g1 + 1));
-            for (int32_t s = 2; s <= inner; ++s) {
-                const bool last = s == inner;
-                float* yu = last ? Wt : h->u;  // the last u is committed in place (eq. 17)
-                RCK(pass(h, 0, kModePlain, h->v, -1, -1, nullptr, nullptr, yu, last ? t : -1, 1));
-                RCK(pass(h, 1, kModePlain, yu, -1, -1, nullptr, nullptr, last ? Ht : h->v,
-                         last ? t : -1, 1));
-            }
-            if (inner == 1) {
-                Timed tm(h, CCDPP_K_COMMIT, 0, 8.0 * m);
-                HIPCK(h, launch_copy(h->u, Wt, m, h->stream));
-                tm.done();
-            }
-            h->pending = t;
-        }
-    }
-    if (h->pending >= 0) {
-        // Final eq. 18 on both copies; the user-major one also sums R^2 for the training RMSE.
-        const float* Wp = h->W + (int64_t)h->pending * m;
-        const float* Hp = h->H + (int64_t)h->pending * n;
-        RCK(pass(h, 0, kModeFlush, nullptr, -1, h->pending, nullptr, Hp, nullptr, -1, 1));
-        HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
-        RCK(pass(h, 1, kModeFlush, nullptr, -1, h->pending, nullptr, Wp, nullptr, -1, 1));
-        h->pending = -1;
-        double sse = 0.0;
-        HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
-        HIPCK(h, hipStreamSynchronize(h->stream));
-        h->train_sse = h->L[0].grid ? sse : 0.0;
-        h->train_sse_valid = true;
-    } else {
-        HIPCK(h, hipStreamSynchronize(h->stream));
-    }
-    if (h->prof) collect_profile(h);
-    return CCDPP_OK;
+    return h->dbl ? run_impl<double>(h, outer, inner) : run_impl<float>(h, outer, inner);
 }
 
 int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol,
@@ -906,13 +1069,12 @@ int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol
     for (int32_t it = 0; it < max_outer; ++it) {
         RCK(ccdpp_run(h, 1, inner));
         double w2 = 0.0, h2 = 0.0, te = std::nan("");
-        HIPCK(h, ccdk::launch_sq_sum(h->W, h->m * h->k, h->sse_part, kReduceParts, s));
+        RCK(launch_sq_sum_any(h, h->W, h->m * h->k));
         RCK(reduce(&w2));
-        HIPCK(h, ccdk::launch_sq_sum(h->H, h->n * h->k, h->sse_part, kReduceParts, s));
+        RCK(launch_sq_sum_any(h, h->H, h->n * h->k));
         RCK(reduce(&h2));
         if (test_nnz > 0) {
-            HIPCK(h, ccdk::launch_test_err(dr, dc, dv, test_nnz, h->rold2new, h->cold2new, h->W,
-                                           h->H, h->m, h->n, h->k, h->sse_part, kReduceParts, s));
+            RCK(launch_test_err_any(h, dr, dc, dv, test_nnz));
             double sum = 0.0;
             RCK(reduce(&sum));
             te = std::sqrt(sum / (double)test_nnz);
@@ -931,63 +1093,16 @@ int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol
     return CCDPP_OK;
 }
 
-int ccdpp_get_factors(ccdpp_t* h, float* W, float* H) {
-    if (!usable(h)) return CCDPP_ESTATE;
-    hipStream_t s = h->stream;
-    if (W) {
-        float* d;
-        Tmp t;
-        HIPCK(h, talloc(t, &d, h->m * h->k));
-        HIPCK(h, ccdk::launch_gather_factor_out(h->W, h->rold2new, h->m, h->k, d, s));
-        HIPCK(h, hipMemcpyAsync(W, d, h->m * h->k * 4, hipMemcpyDeviceToHost, s));
-        HIPCK(h, hipStreamSynchronize(s));
-    }
-    if (H) {
-        float* d;
-        Tmp t;
-        HIPCK(h, talloc(t, &d, h->n * h->k));
-        HIPCK(h, ccdk::launch_gather_factor_out(h->H, h->cold2new, h->n, h->k, d, s));
-        HIPCK(h, hipMemcpyAsync(H, d, h->n * h->k * 4, hipMemcpyDeviceToHost, s));
-        HIPCK(h, hipStreamSynchronize(s));
-    }
-    return CCDPP_OK;
-}
 
+int ccdpp_get_factors(ccdpp_t* h, float* W, float* H) { return get_factors_impl<float>(h, W, H); }
+int ccdpp_get_factors_f64(ccdpp_t* h, double* W, double* H) {
+    return get_factors_impl<double>(h, W, H);
+}
 int ccdpp_set_factors(ccdpp_t* h, const float* W, const float* H) {
-    if (!usable(h)) return CCDPP_ESTATE;
-    if (W)
-        for (int64_t e = 0; e < h->m * h->k; ++e)
-            if (!std::isfinite(W[e]))
-                return fail(h, CCDPP_EINVAL, "W[%lld] is not finite", (long long)e);
-    if (H)
-        for (int64_t e = 0; e < h->n * h->k; ++e)
-            if (!std::isfinite(H[e]))
-                return fail(h, CCDPP_EINVAL, "H[%lld] is not finite", (long long)e);
-    hipStream_t s = h->stream;
-    if (W) {
-        float* d;
-        Tmp t;
-        HIPCK(h, talloc(t, &d, h->m * h->k));
-        HIPCK(h, hipMemcpyAsync(d, W, h->m * h->k * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, ccdk::launch_scatter_factor_in(d, h->rnew2old, h->m, h->k, h->W, s));
-        HIPCK(h, hipStreamSynchronize(s));
-    }
-    if (H) {
-        float* d;
-        Tmp t;
-        HIPCK(h, talloc(t, &d, h->n * h->k));
-        HIPCK(h, hipMemcpyAsync(d, H, h->n * h->k * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, ccdk::launch_scatter_factor_in(d, h->cnew2old, h->n, h->k, h->H, s));
-        HIPCK(h, hipStreamSynchronize(s));
-    }
-    RCK(spread_factors(h));
-    HIPCK(h, ccdk::launch_rebuild_residual(h->L[0], h->pos0, h->A, h->W, h->H, h->m, h->n, h->k,
-                                           s));
-    HIPCK(h, ccdk::launch_copy_mapped(h->L[0].val, h->pos0, h->L[1].val, h->map01, h->nnz, s));
-    HIPCK(h, hipStreamSynchronize(s));
-    h->pending = -1;
-    h->train_sse_valid = false;
-    return CCDPP_OK;
+    return set_factors_impl<float>(h, W, H);
+}
+int ccdpp_set_factors_f64(ccdpp_t* h, const double* W, const double* H) {
+    return set_factors_impl<double>(h, W, H);
 }
 
 int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, const float* val,
@@ -1012,8 +1127,7 @@ int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, 
     HIPCK(h, hipMemcpyAsync(dr, row, nnz * 4, hipMemcpyHostToDevice, s));
     HIPCK(h, hipMemcpyAsync(dc, col, nnz * 4, hipMemcpyHostToDevice, s));
     HIPCK(h, hipMemcpyAsync(dv, val, nnz * 4, hipMemcpyHostToDevice, s));
-    HIPCK(h, ccdk::launch_test_err(dr, dc, dv, nnz, h->rold2new, h->cold2new, h->W, h->H, h->m,
-                                   h->n, h->k, h->sse_part, kReduceParts, s));
+    RCK(launch_test_err_any(h, dr, dc, dv, nnz));
     HIPCK(h, ccdk::launch_reduce_sum(h->sse_part, kReduceParts, h->d_scalar, s));
     double sum = 0.0;
     HIPCK(h, hipMemcpyAsync(&sum, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
@@ -1028,7 +1142,7 @@ int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
     if (h->nnz < 1) return fail(h, CCDPP_EINVAL, "no observed entries");
     if (!h->train_sse_valid) {
         hipStream_t s = h->stream;
-        HIPCK(h, ccdk::launch_sq_sum(h->L[0].val, h->L[0].npad, h->sse_part, kReduceParts, s));
+        RCK(launch_sq_sum_any(h, h->L[0].val, h->L[0].npad));
         HIPCK(h, ccdk::launch_reduce_sum(h->sse_part, kReduceParts, h->d_scalar, s));
         double sum = 0.0;
         HIPCK(h, hipMemcpyAsync(&sum, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
@@ -1040,27 +1154,21 @@ int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
     return CCDPP_OK;
 }
 
-int ccdpp_get_residual(ccdpp_t* h, float* R) {
-    if (!usable(h)) return CCDPP_ESTATE;
-    if (!R && h->nnz) return fail(h, CCDPP_EINVAL, "R is NULL");
-    if (h->nnz == 0) return CCDPP_OK;
-    hipStream_t s = h->stream;
-    float* d;
-    Tmp t;
-    HIPCK(h, talloc(t, &d, h->nnz));
-    HIPCK(h, ccdk::launch_copy_mapped(h->L[0].val, h->pos0, d, h->perm0, h->nnz, s));
-    HIPCK(h, hipMemcpyAsync(R, d, h->nnz * 4, hipMemcpyDeviceToHost, s));
-    HIPCK(h, hipStreamSynchronize(s));
-    return CCDPP_OK;
-}
+
+int ccdpp_get_residual(ccdpp_t* h, float* R) { return get_residual_impl<float>(h, R); }
+int ccdpp_get_residual_f64(ccdpp_t* h, double* R) { return get_residual_impl<double>(h, R); }
 
 int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (!mismatches) return fail(h, CCDPP_EINVAL, "mismatches is NULL");
     hipStream_t s = h->stream;
     HIPCK(h, hipMemsetAsync(h->d_count, 0, 8, s));
-    HIPCK(h, ccdk::launch_consistency(h->L[0].val, h->pos0, h->L[1].val, h->map01, h->nnz,
-                                      h->d_count, s));
+    RCK(with_value_type(h, [&](auto z) -> int {
+        using V = decltype(z);
+        HIPCK(h, ccdk::launch_consistency<V>(as<V>(h->L[0].val), h->pos0, as<V>(h->L[1].val),
+                                             h->map01, h->nnz, h->d_count, s));
+        return CCDPP_OK;
+    }));
     unsigned long long c = 0;
     HIPCK(h, hipMemcpyAsync(&c, h->d_count, 8, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
@@ -1120,11 +1228,12 @@ int ccdpp_profile_read(ccdpp_t* h, int32_t kind, int32_t layout, int64_t* launch
 int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     if (!h) return CCDPP_ESTATE;
     if (!out || len < 0) return fail(h, CCDPP_EINVAL, "bad output buffer");
-    const int64_t v[16] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[17] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  h->L[0].T,
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
-                           h->L[1].T,    h->L[1].grid, h->L[1].nseg, h->bytes_held};
-    int32_t w = std::min<int32_t>(len, 16);
+                           h->L[1].T,    h->L[1].grid, h->L[1].nseg, h->bytes_held,
+                           h->dbl ? 8 : 4};
+    int32_t w = std::min<int32_t>(len, 17);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

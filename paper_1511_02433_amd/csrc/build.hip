@@ -9,6 +9,8 @@
 // Adjacent equal keys after the user-major sort are repeated positions.
 #include <hipcub/hipcub.hpp>
 
+#include <type_traits>
+
 #include "ccdpp_internal.hpp"
 
 namespace ccdk {
@@ -66,11 +68,11 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
 
 // Entry q of the sorted order goes to padded position p = q + seg_off[segment]:
 // its index to idx[p], its value to val[val_slot(p)]; pos[q] is the value slot.
-template <class I>
+template <class I, class V>
 __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
                               const float* __restrict__ val_in, int64_t nnz, int cbits,
                               uint64_t mask, const int32_t* __restrict__ seg_off, bool swz,
-                              I* __restrict__ idx, float* __restrict__ val,
+                              I* __restrict__ idx, V* __restrict__ val,
                               int32_t* __restrict__ pos) {
     for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * kT) {
@@ -79,8 +81,8 @@ __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* 
         const uint32_t c = (uint32_t)(key & mask);
         const bool first = q == 0 || (keys[q - 1] >> cbits) != (key >> cbits);
         idx[p] = (I)((swz ? lds_swizzle(c) : c) | (first ? IndexBits<I>::start : 0u));
-        const int64_t f = val_slot(p);
-        val[f] = val_in[perm[q]];
+        const int64_t f = val_slot<V>(p);
+        val[f] = (V)val_in[perm[q]];
         pos[q] = (int32_t)f;
     }
 }
@@ -102,32 +104,35 @@ __global__ void k_compose(const int32_t* __restrict__ a, const int32_t* __restri
         out[q] = a[b[q]];
 }
 
-__global__ void k_fill(float* __restrict__ dst, float value, int64_t n) {
+template <class V>
+__global__ void k_fill(V* __restrict__ dst, V value, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
         dst[i] = value;
 }
 
 // colmajor[t * rows + i'] = rowmajor[new2old[i'] * k + t]
-__global__ void k_factor_in(const float* __restrict__ rowmajor, const int32_t* __restrict__ new2old,
-                            int64_t rows, int32_t k, float* __restrict__ colmajor) {
+template <class S, class V>
+__global__ void k_factor_in(const S* __restrict__ rowmajor, const int32_t* __restrict__ new2old,
+                            int64_t rows, int32_t k, V* __restrict__ colmajor) {
     const int64_t total = rows * k;
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * kT) {
         const int64_t t = e / rows;
         const int64_t i = e - t * rows;
-        colmajor[e] = rowmajor[(int64_t)new2old[i] * k + t];
+        colmajor[e] = (V)rowmajor[(int64_t)new2old[i] * k + t];
     }
 }
 
 // rowmajor[i * k + t] = colmajor[t * rows + old2new[i]]
-__global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* __restrict__ old2new,
-                             int64_t rows, int32_t k, float* __restrict__ rowmajor) {
+template <class V, class S>
+__global__ void k_factor_out(const V* __restrict__ colmajor, const int32_t* __restrict__ old2new,
+                             int64_t rows, int32_t k, S* __restrict__ rowmajor) {
     const int64_t total = rows * k;
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * kT) {
         const int64_t i = e / k;
         const int64_t t = e - i * k;
-        rowmajor[e] = colmajor[t * rows + old2new[i]];
+        rowmajor[e] = (S)colmajor[t * rows + old2new[i]];
     }
 }
 
@@ -135,17 +140,17 @@ __global__ void k_factor_out(const float* __restrict__ colmajor, const int32_t* 
 // in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
 // unpadded layout order) has its value in slot pos[e]; its segment, and from it the
 // row and the tile, are found by binary search.
-template <class I>
+template <class I, class V>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
                           int32_t P, int32_t T, bool swz, const I* __restrict__ idx,
-                          const int32_t* __restrict__ pos, const float* __restrict__ A,
-                          const float* __restrict__ W, const float* __restrict__ H, int64_t m,
-                          int64_t n, int32_t k, int64_t nnz, float* __restrict__ val) {
+                          const int32_t* __restrict__ pos, const V* __restrict__ A,
+                          const V* __restrict__ W, const V* __restrict__ H, int64_t m,
+                          int64_t n, int32_t k, int64_t nnz, V* __restrict__ val) {
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
          e += (int64_t)gridDim.x * kT) {
         const int64_t f = pos[e];         // value slot
-        const int64_t q = val_entry(f);   // entry position
+        const int64_t q = val_entry<V>(f);   // entry position
         int64_t lo = 0, hi = nseg;  // last s with seg_start[s] <= q
         while (hi - lo > 1) {
             const int64_t mid = (lo + hi) >> 1;
@@ -162,27 +167,33 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
-        val[f] = (float)((double)A[e] - pred);
+        val[f] = (V)((double)A[e] - pred);
     }
 }
 
-__global__ void k_copy_mapped(const float* __restrict__ src, const int32_t* __restrict__ smap,
-                              float* __restrict__ dst, const int32_t* __restrict__ dmap,
+template <class S, class V>
+__global__ void k_copy_mapped(const S* __restrict__ src, const int32_t* __restrict__ smap,
+                              V* __restrict__ dst, const int32_t* __restrict__ dmap,
                               int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
-        dst[dmap ? dmap[i] : i] = src[smap ? smap[i] : i];
+        dst[dmap ? dmap[i] : i] = (V)src[smap ? smap[i] : i];
 }
 
-__global__ void k_consistency(const float* __restrict__ a, const int32_t* __restrict__ amap,
-                              const float* __restrict__ b, const int32_t* __restrict__ bmap,
+// Bitwise comparison of the two copies (as unsigned words of the value's size).
+template <class V>
+__global__ void k_consistency(const V* __restrict__ a, const int32_t* __restrict__ amap,
+                              const V* __restrict__ b, const int32_t* __restrict__ bmap,
                               int64_t n, unsigned long long* count) {
+    using U = typename std::conditional<sizeof(V) == 4, uint32_t, uint64_t>::type;
     for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
-        if (__float_as_uint(a[amap[i]]) != __float_as_uint(b[bmap[i]])) atomicAdd(count, 1ull);
+        if (__builtin_bit_cast(U, a[amap[i]]) != __builtin_bit_cast(U, b[bmap[i]]))
+            atomicAdd(count, 1ull);
 }
 
-__global__ void k_seg_spread(const float* __restrict__ F, int64_t rows,
+template <class V>
+__global__ void k_seg_spread(const V* __restrict__ F, int64_t rows,
                              const int32_t* __restrict__ seg_row, int64_t S, int32_t k,
-                             float* __restrict__ out) {
+                             V* __restrict__ out) {
     const int64_t total = S * k;
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * kT) {
@@ -205,7 +216,8 @@ __device__ __forceinline__ void block_total(double acc, double* out) {
     if (threadIdx.x == 0) *out = s[0];
 }
 
-__global__ void k_sq_sum(const float* __restrict__ v, int64_t n, double* __restrict__ part) {
+template <class V>
+__global__ void k_sq_sum(const V* __restrict__ v, int64_t n, double* __restrict__ part) {
     double acc = 0.0;
     for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT) {
         const double d = v[i];
@@ -214,10 +226,11 @@ __global__ void k_sq_sum(const float* __restrict__ v, int64_t n, double* __restr
     block_total(acc, &part[blockIdx.x]);
 }
 
+template <class V>
 __global__ void k_test_err(const int32_t* __restrict__ row, const int32_t* __restrict__ col,
                            const float* __restrict__ val, int64_t nnz,
                            const int32_t* __restrict__ rnew, const int32_t* __restrict__ cnew,
-                           const float* __restrict__ W, const float* __restrict__ H, int64_t m,
+                           const V* __restrict__ W, const V* __restrict__ H, int64_t m,
                            int64_t n, int32_t k, double* __restrict__ part) {
     double acc = 0.0;
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
@@ -271,17 +284,18 @@ hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hi
     return hipGetLastError();
 }
 
+template <class V>
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
                               int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
-                              void* idx, float* val, int32_t* pos, hipStream_t s) {
+                              void* idx, V* val, int32_t* pos, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
     const uint64_t mask = cbits >= 64 ? ~0ull : ((1ull << cbits) - 1);
     if (idx16)
-        hipLaunchKernelGGL(k_layout_fill<uint16_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
+        hipLaunchKernelGGL((k_layout_fill<uint16_t, V>), grid_for(nnz), dim3(kT), 0, s, keys, perm,
                            val_in, nnz, cbits, mask, seg_off, swz, static_cast<uint16_t*>(idx), val,
                            pos);
     else
-        hipLaunchKernelGGL(k_layout_fill<int32_t>, grid_for(nnz), dim3(kT), 0, s, keys, perm,
+        hipLaunchKernelGGL((k_layout_fill<int32_t, V>), grid_for(nnz), dim3(kT), 0, s, keys, perm,
                            val_in, nnz, cbits, mask, seg_off, swz, static_cast<int32_t*>(idx), val,
                            pos);
     return hipGetLastError();
@@ -311,78 +325,122 @@ hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t
     return hipGetLastError();
 }
 
-hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t s) {
+template <class V>
+hipError_t launch_fill(V* dst, V value, int64_t n, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_fill, grid_for(n), dim3(kT), 0, s, dst, value, n);
+    hipLaunchKernelGGL(k_fill<V>, grid_for(n), dim3(kT), 0, s, dst, value, n);
     return hipGetLastError();
 }
 
-hipError_t launch_scatter_factor_in(const float* rowmajor, const int32_t* new2old, int64_t rows,
-                                    int32_t k, float* colmajor, hipStream_t s) {
-    hipLaunchKernelGGL(k_factor_in, grid_for(rows * k), dim3(kT), 0, s, rowmajor, new2old, rows, k,
-                       colmajor);
+template <class S, class V>
+hipError_t launch_scatter_factor_in(const S* rowmajor, const int32_t* new2old, int64_t rows,
+                                    int32_t k, V* colmajor, hipStream_t s) {
+    hipLaunchKernelGGL((k_factor_in<S, V>), grid_for(rows * k), dim3(kT), 0, s, rowmajor, new2old,
+                       rows, k, colmajor);
     return hipGetLastError();
 }
 
-hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2new, int64_t rows,
-                                    int32_t k, float* rowmajor, hipStream_t s) {
-    hipLaunchKernelGGL(k_factor_out, grid_for(rows * k), dim3(kT), 0, s, colmajor, old2new, rows,
-                       k, rowmajor);
+template <class V, class S>
+hipError_t launch_gather_factor_out(const V* colmajor, const int32_t* old2new, int64_t rows,
+                                    int32_t k, S* rowmajor, hipStream_t s) {
+    hipLaunchKernelGGL((k_factor_out<V, S>), grid_for(rows * k), dim3(kT), 0, s, colmajor, old2new,
+                       rows, k, rowmajor);
     return hipGetLastError();
 }
 
-hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const float* A,
-                                   const float* W, const float* H, int64_t m, int64_t n,
-                                   int32_t k, hipStream_t s) {
+template <class V>
+hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const V* A, const V* W,
+                                   const V* H, int64_t m, int64_t n, int32_t k, hipStream_t s) {
     if (L.nnz == 0) return hipSuccess;
     if (L.idx16)
-        hipLaunchKernelGGL(k_rebuild<uint16_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
+        hipLaunchKernelGGL((k_rebuild<uint16_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
                            static_cast<const uint16_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
-                           L.val);
+                           static_cast<V*>(L.val));
     else
-        hipLaunchKernelGGL(k_rebuild<int32_t>, grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
+        hipLaunchKernelGGL((k_rebuild<int32_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
                            static_cast<const int32_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
-                           L.val);
+                           static_cast<V*>(L.val));
     return hipGetLastError();
 }
 
-hipError_t launch_copy_mapped(const float* src, const int32_t* smap, float* dst,
-                              const int32_t* dmap, int64_t n, hipStream_t s) {
+template <class S, class V>
+hipError_t launch_copy_mapped(const S* src, const int32_t* smap, V* dst, const int32_t* dmap,
+                              int64_t n, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_copy_mapped, grid_for(n), dim3(kT), 0, s, src, smap, dst, dmap, n);
+    hipLaunchKernelGGL((k_copy_mapped<S, V>), grid_for(n), dim3(kT), 0, s, src, smap, dst, dmap, n);
     return hipGetLastError();
 }
 
-hipError_t launch_consistency(const float* a, const int32_t* amap, const float* b,
-                              const int32_t* bmap, int64_t n, unsigned long long* count,
-                              hipStream_t s) {
+template <class V>
+hipError_t launch_consistency(const V* a, const int32_t* amap, const V* b, const int32_t* bmap,
+                              int64_t n, unsigned long long* count, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_consistency, grid_for(n), dim3(kT), 0, s, a, amap, b, bmap, n, count);
+    hipLaunchKernelGGL(k_consistency<V>, grid_for(n), dim3(kT), 0, s, a, amap, b, bmap, n, count);
     return hipGetLastError();
 }
 
-hipError_t launch_seg_spread(const float* F, int64_t rows, const int32_t* seg_row, int64_t S,
-                             int32_t k, float* out, hipStream_t s) {
+template <class V>
+hipError_t launch_seg_spread(const V* F, int64_t rows, const int32_t* seg_row, int64_t S,
+                             int32_t k, V* out, hipStream_t s) {
     if (S == 0 || k == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_seg_spread, grid_for(S * k), dim3(kT), 0, s, F, rows, seg_row, S, k, out);
+    hipLaunchKernelGGL(k_seg_spread<V>, grid_for(S * k), dim3(kT), 0, s, F, rows, seg_row, S, k,
+                       out);
     return hipGetLastError();
 }
 
-hipError_t launch_sq_sum(const float* v, int64_t n, double* part, int32_t nparts, hipStream_t s) {
-    hipLaunchKernelGGL(k_sq_sum, dim3(nparts), dim3(kT), 0, s, v, n, part);
+template <class V>
+hipError_t launch_sq_sum(const V* v, int64_t n, double* part, int32_t nparts, hipStream_t s) {
+    hipLaunchKernelGGL(k_sq_sum<V>, dim3(nparts), dim3(kT), 0, s, v, n, part);
     return hipGetLastError();
 }
 
+template <class V>
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,
-                           const int32_t* rold2new, const int32_t* cold2new, const float* W,
-                           const float* H, int64_t m, int64_t n, int32_t k, double* part,
+                           const int32_t* rold2new, const int32_t* cold2new, const V* W,
+                           const V* H, int64_t m, int64_t n, int32_t k, double* part,
                            int32_t nparts, hipStream_t s) {
-    hipLaunchKernelGGL(k_test_err, dim3(nparts), dim3(kT), 0, s, row, col, val, nnz, rold2new,
+    hipLaunchKernelGGL(k_test_err<V>, dim3(nparts), dim3(kT), 0, s, row, col, val, nnz, rold2new,
                        cold2new, W, H, m, n, k, part);
     return hipGetLastError();
 }
+
+#define CCDK_BUILD_INSTANTIATE(V)                                                               \
+    template hipError_t launch_layout_fill<V>(const uint64_t*, const int32_t*, const float*,    \
+                                              int64_t, int, const int32_t*, bool, bool, void*,  \
+                                              V*, int32_t*, hipStream_t);                       \
+    template hipError_t launch_fill<V>(V*, V, int64_t, hipStream_t);                            \
+    template hipError_t launch_scatter_factor_in<float, V>(const float*, const int32_t*,        \
+                                                           int64_t, int32_t, V*, hipStream_t);  \
+    template hipError_t launch_scatter_factor_in<double, V>(const double*, const int32_t*,      \
+                                                            int64_t, int32_t, V*, hipStream_t); \
+    template hipError_t launch_gather_factor_out<V, float>(const V*, const int32_t*, int64_t,   \
+                                                           int32_t, float*, hipStream_t);       \
+    template hipError_t launch_gather_factor_out<V, double>(const V*, const int32_t*, int64_t,  \
+                                                            int32_t, double*, hipStream_t);     \
+    template hipError_t launch_rebuild_residual<V>(const Layout&, const int32_t*, const V*,     \
+                                                   const V*, const V*, int64_t, int64_t,        \
+                                                   int32_t, hipStream_t);                       \
+    template hipError_t launch_copy_mapped<V, V>(const V*, const int32_t*, V*, const int32_t*,  \
+                                                 int64_t, hipStream_t);                         \
+    template hipError_t launch_consistency<V>(const V*, const int32_t*, const V*,               \
+                                              const int32_t*, int64_t, unsigned long long*,     \
+                                              hipStream_t);                                     \
+    template hipError_t launch_seg_spread<V>(const V*, int64_t, const int32_t*, int64_t,        \
+                                             int32_t, V*, hipStream_t);                         \
+    template hipError_t launch_sq_sum<V>(const V*, int64_t, double*, int32_t, hipStream_t);     \
+    template hipError_t launch_test_err<V>(const int32_t*, const int32_t*, const float*,        \
+                                           int64_t, const int32_t*, const int32_t*, const V*,   \
+                                           const V*, int64_t, int64_t, int32_t, double*,        \
+                                           int32_t, hipStream_t);
+CCDK_BUILD_INSTANTIATE(float)
+CCDK_BUILD_INSTANTIATE(double)
+#undef CCDK_BUILD_INSTANTIATE
+template hipError_t launch_copy_mapped<double, float>(const double*, const int32_t*, float*,
+                                                      const int32_t*, int64_t, hipStream_t);
+template hipError_t launch_copy_mapped<float, double>(const float*, const int32_t*, double*,
+                                                      const int32_t*, int64_t, hipStream_t);
 
 // Radix sort of (key, id) pairs on the low `bits` bits of the key.
 hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, int32_t* vout,

@@ -86,15 +86,25 @@ constexpr int kEntryPad = 64;             // entries of padding after idx and va
 
 __host__ __device__ inline uint32_t lds_swizzle(uint32_t c) { return c ^ ((c >> 5) & 31u); }
 
-// Storage slot of the value of entry p (see above), and its inverse.
+// Storage slot of the value of entry p (see above), and its inverse.  A 128-bit
+// access holds E = 16 / sizeof(V) values; the block of kWin entries is stored as
+// kE / E parts of 64 x E values, lane l's values k (E of them per part) at
+// part k / E, position l * E + k % E.  For float: 4l .. 4l + 3 and
+// kWin/2 + 4l .. kWin/2 + 4l + 3.
 static_assert(kWin == 512 && kE == 8, "val_slot assumes 64 lanes of 8 entries");
+template <class V>
 __host__ __device__ inline int64_t val_slot(int64_t p) {
+    constexpr int64_t E = 16 / sizeof(V);
     const int64_t o = p & (kWin - 1);
-    return (p - o) + ((o & 4) << 6) + ((o >> 3) << 2) + (o & 3);
+    const int64_t l = o >> 3, k = o & 7;
+    return (p - o) + (k / E) * (64 * E) + l * E + (k % E);
 }
+template <class V>
 __host__ __device__ inline int64_t val_entry(int64_t f) {
+    constexpr int64_t E = 16 / sizeof(V);
     const int64_t o = f & (kWin - 1);
-    return (f - o) + (((o & 255) >> 2) << 3) + ((o >> 8) << 2) + (o & 3);
+    const int64_t part = o / (64 * E), r = o % (64 * E);
+    return (f - o) + ((r / E) << 3) + part * E + (r % E);
 }
 
 enum PassMode : int32_t {
@@ -124,35 +134,39 @@ enum GatherMode : int32_t {
     kGatherLds = 2,     // vectors staged in LDS (tiled when they do not fit)
 };
 
+// V is the type of the residual, the factors and the in-window arithmetic:
+// float (the paper's faster variant, Section 8) or double.
+template <class V>
 struct PassArgs {
     const void* idx;            // [npad] uint16 or int32 tile-local column
-    float* val;                 // [npad] residual / R-hat, in val_slot order
+    V* val;                     // [npad] residual / R-hat, in val_slot<V> order
     const int32_t* wg_piece;    // [grid + 1] pieces of each workgroup
     const int32_t* piece_tile;  // [npieces] tile of each piece
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
     const int32_t* piece_seg;   // [npieces * kWaves] segment holding each chunk's first entry
     const int32_t* chunk_flags; // [npieces * kWaves] kChunkMid | kChunkCont
-    const float* x;             // [cols] gathered vector of the update
-    const float* p;             // [S] own factor column, current feature, per segment
-    const float* pp;            // [S] own factor column, previous feature (committed), per segment
-    const float* q;             // [cols] other factor column, current feature
-    const float* qq;            // [cols] other factor column, previous feature (committed)
-    float* y;                   // [rows] coordinates (P == 1)
+    const V* x;                 // [cols] gathered vector of the update
+    const V* p;                 // [S] own factor column, current feature, per segment
+    const V* pp;                // [S] own factor column, previous feature (committed), per segment
+    const V* q;                 // [cols] other factor column, current feature
+    const V* qq;                // [cols] other factor column, previous feature (committed)
+    V* y;                       // [rows] coordinates (P == 1)
     double2* part;              // [S + 2 * chunks] partials: per segment (P > 1), then the
                                 // head and tail slot of every chunk
     double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
     int32_t rows, cols, T, P;
-    int32_t Ts;                 // LDS floats per staged vector slice
+    int32_t Ts;                 // LDS elements per staged vector slice
     int32_t pad;                // index held by padding entries (reads 0)
     int32_t nseg;               // S
     int32_t nseg_ne;            // segments with entries (P == 1: rows before the empty ones)
-    int32_t vec_floats;         // LDS floats taken by staged vectors
+    int32_t vec_elems;          // LDS elements taken by staged vectors
     int32_t x_is_q;             // x and q are the same vector (staged once)
     double lambda;
 };
 
 // Finishes rows from partial slots: row ids[i] (or i when ids is null) adds
 // part[srcs[src_ptr[i] .. src_ptr[i + 1])] in order.
+template <class V>
 struct CombineArgs {
     const int32_t* ids;          // [n] rows, or null
     const int32_t* src_ptr;      // [n + 1]
@@ -160,8 +174,8 @@ struct CombineArgs {
     const int32_t* seg_ptr;      // [n + 1] segments of each row (with yseg)
     const int32_t* segs;
     const double2* part;
-    float* y;
-    float* yseg;                 // optional [S]: y spread over the row's segments
+    V* y;
+    V* yseg;                     // optional [S]: y spread over the row's segments
     int32_t n;
     double lambda;
 };
@@ -172,12 +186,12 @@ struct Layout {
     int64_t npad = 0;                // entries including alignment padding
     int32_t gather = kGatherGlobal;
     int32_t T = 0, P = 1;
-    int32_t Ts = 0;                  // LDS floats per staged slice (swizzled range + zero)
+    int32_t Ts = 0;                  // LDS elements per staged slice (swizzled range + zero)
     int32_t pad = 0;                 // padding index: the zero word (staged) or cols (global)
     bool swz = false;                // indices are swizzled LDS positions (staged layouts)
     bool idx16 = false;
     void* idx = nullptr;             // [npad + kEntryPad]
-    float* val = nullptr;            // [npad + kEntryPad]
+    void* val = nullptr;             // [npad + kEntryPad] of the handle's value type
     int64_t* seg_start = nullptr;    // [S + 1], in padded positions
     int32_t* seg_row = nullptr;
     int32_t* tile_seg = nullptr;     // [P + 1] first segment of each tile
@@ -201,17 +215,20 @@ struct Layout {
     int32_t grid = 0;                // persistent workgroups per pass
 };
 
-// Launchers (sweep.hip).
+// Launchers (sweep.hip), instantiated for V = float and V = double.
 hipError_t sweep_init();  // raise the dynamic-LDS limit of the staged kernels
-hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const float* p,
-                       const float* pp, const float* q, const float* qq, float* y, double lambda,
-                       double* sse_part, hipStream_t s);
-hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda, hipStream_t s);
-hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s);
+template <class V>
+hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, const V* pp,
+                       const V* q, const V* qq, V* y, double lambda, double* sse_part,
+                       hipStream_t s);
+template <class V>
+hipError_t launch_combine(const Layout& L, V* y, V* yseg, double lambda, hipStream_t s);
+template <class V>
+hipError_t launch_copy(const V* src, V* dst, int64_t n, hipStream_t s);
 hipError_t launch_reduce_sum(const double* part, int32_t n, double* out, hipStream_t s);
 int staged_vectors(PassMode mode, bool x_is_q);
 
-// Device build and utilities (build.hip).
+// Device build and utilities (build.hip); V as above, S a host-side element type.
 hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t* count, hipStream_t s);
 hipError_t launch_map(const int32_t* in, const int32_t* table, int64_t n, int32_t* out,
                       hipStream_t s);
@@ -221,35 +238,42 @@ hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32
                            int64_t nnz, int32_t rows, int32_t T, int cbits, uint64_t* keys,
                            int32_t* ids, hipStream_t s);
 hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hipStream_t s);
+template <class V>
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
                               int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
-                              void* idx, float* val, int32_t* pos, hipStream_t s);
+                              void* idx, V* val, int32_t* pos, hipStream_t s);
 hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t* out,
                           hipStream_t s);
-hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t s);
-hipError_t launch_scatter_factor_in(const float* rowmajor, const int32_t* new2old, int64_t rows,
-                                    int32_t k, float* colmajor, hipStream_t s);
-hipError_t launch_gather_factor_out(const float* colmajor, const int32_t* old2new, int64_t rows,
-                                    int32_t k, float* rowmajor, hipStream_t s);
-hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const float* A,
-                                   const float* W, const float* H, int64_t m, int64_t n,
-                                   int32_t k, hipStream_t s);
-// dst[dmap ? dmap[i] : i] = src[smap ? smap[i] : i] for i < n
-hipError_t launch_copy_mapped(const float* src, const int32_t* smap, float* dst,
-                              const int32_t* dmap, int64_t n, hipStream_t s);
-hipError_t launch_consistency(const float* a, const int32_t* amap, const float* b,
-                              const int32_t* bmap, int64_t n, unsigned long long* count,
-                              hipStream_t s);
+template <class V>
+hipError_t launch_fill(V* dst, V value, int64_t n, hipStream_t s);
+template <class S, class V>
+hipError_t launch_scatter_factor_in(const S* rowmajor, const int32_t* new2old, int64_t rows,
+                                    int32_t k, V* colmajor, hipStream_t s);
+template <class V, class S>
+hipError_t launch_gather_factor_out(const V* colmajor, const int32_t* old2new, int64_t rows,
+                                    int32_t k, S* rowmajor, hipStream_t s);
+template <class V>
+hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const V* A, const V* W,
+                                   const V* H, int64_t m, int64_t n, int32_t k, hipStream_t s);
+// dst[dmap ? dmap[i] : i] = src[smap ? smap[i] : i] for i < n (converting between types)
+template <class S, class V>
+hipError_t launch_copy_mapped(const S* src, const int32_t* smap, V* dst, const int32_t* dmap,
+                              int64_t n, hipStream_t s);
+template <class V>
+hipError_t launch_consistency(const V* a, const int32_t* amap, const V* b, const int32_t* bmap,
+                              int64_t n, unsigned long long* count, hipStream_t s);
 // out[t * S + s] = F[t * rows + seg_row[s]] for t < k
-hipError_t launch_seg_spread(const float* F, int64_t rows, const int32_t* seg_row, int64_t S,
-                             int32_t k, float* out, hipStream_t s);
-hipError_t launch_sq_sum(const float* v, int64_t n, double* part, int32_t nparts,
-                         hipStream_t s);
+template <class V>
+hipError_t launch_seg_spread(const V* F, int64_t rows, const int32_t* seg_row, int64_t S,
+                             int32_t k, V* out, hipStream_t s);
+template <class V>
+hipError_t launch_sq_sum(const V* v, int64_t n, double* part, int32_t nparts, hipStream_t s);
+template <class V>
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,
-                           const int32_t* rold2new, const int32_t* cold2new, const float* W,
-                           const float* H, int64_t m, int64_t n, int32_t k, double* part,
+                           const int32_t* rold2new, const int32_t* cold2new, const V* W,
+                           const V* H, int64_t m, int64_t n, int32_t k, double* part,
                            int32_t nparts, hipStream_t s);
 hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, int32_t* vout,
                       int64_t n, int bits, hipStream_t s, void** tmp, size_t* tmp_bytes);

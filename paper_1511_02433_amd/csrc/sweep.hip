@@ -34,7 +34,16 @@ namespace {
 using rsrc_t = __amdgpu_buffer_rsrc_t;
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, gfx9 family
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 128 bits of the value type: four floats or two doubles.
+template <class V> struct Vec16;
+template <> struct Vec16<float> { using type = f32x4; };
+template <> struct Vec16<double> { using type = f64x2; };
+
+__device__ __forceinline__ float fmav(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+__device__ __forceinline__ double fmav(double a, double b, double c) { return __builtin_fma(a, b, c); }
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
     uint32_t lim = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
@@ -44,6 +53,13 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 // Bounded load: offsets past the descriptor's limit read 0.
 __device__ __forceinline__ float ld_f32(rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+// Two 32-bit bounded loads (a 64-bit buffer load is not used, see the toolchain notes).
+__device__ __forceinline__ double ld_f64(rsrc_t r, uint32_t off) {
+    int2 v;
+    v.x = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    v.y = __builtin_amdgcn_raw_buffer_load_b32(r, off + 4u, 0, 0);
+    return __builtin_bit_cast(double, v);
 }
 
 // ---- cross-lane operations ---------------------------------------------------
@@ -66,6 +82,19 @@ __device__ __forceinline__ float dpp_f(float old, float v) {
                                                                  ROWS, 0xF, BC));
 }
 
+template <int CTRL, int ROWS = 0xF, bool BC = false>
+__device__ __forceinline__ double dpp_d(double old, double v) {
+    const int2 o = __builtin_bit_cast(int2, old), x = __builtin_bit_cast(int2, v);
+    int2 r;
+    r.x = __builtin_amdgcn_update_dpp(o.x, x.x, CTRL, ROWS, 0xF, BC);
+    r.y = __builtin_amdgcn_update_dpp(o.y, x.y, CTRL, ROWS, 0xF, BC);
+    return __builtin_bit_cast(double, r);
+}
+template <int CTRL, int ROWS = 0xF, bool BC = false>
+__device__ __forceinline__ float dpp_v(float old, float v) { return dpp_f<CTRL, ROWS, BC>(old, v); }
+template <int CTRL, int ROWS = 0xF, bool BC = false>
+__device__ __forceinline__ double dpp_v(double old, double v) { return dpp_d<CTRL, ROWS, BC>(old, v); }
+
 // 1.0 on the lanes whose bit is set in the wave-uniform mask m, else 0.0.
 __device__ __forceinline__ float lane_factor(uint64_t m) {
     return __builtin_amdgcn_inverse_ballot_w64(m) ? 1.0f : 0.0f;
@@ -74,11 +103,11 @@ __device__ __forceinline__ float lane_factor(uint64_t m) {
 // One step of an inclusive segmented scan over lanes: the lanes set in m add
 // the value of the lane CTRL reads (sources out of range, or in rows outside
 // ROWS, contribute 0).  Every lane takes part, so every source is well defined.
-template <int CTRL, int ROWS = 0xF>
-__device__ __forceinline__ void seg_step(uint64_t m, float& n, float& d) {
-    const float f = lane_factor(m);
-    n = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, n), f, n);
-    d = __builtin_fmaf(dpp_f<CTRL, ROWS, true>(0.0f, d), f, d);
+template <int CTRL, int ROWS = 0xF, class V>
+__device__ __forceinline__ void seg_step(uint64_t m, V& n, V& d) {
+    const V f = (V)lane_factor(m);
+    n = fmav(dpp_v<CTRL, ROWS, true>(V(0), n), f, n);
+    d = fmav(dpp_v<CTRL, ROWS, true>(V(0), d), f, d);
 }
 
 // Lanes below the first set bit of a 16- or 32-lane group (all of them if none).
@@ -97,7 +126,8 @@ __device__ __forceinline__ uint64_t before_first32(uint64_t bits) {
 // broadcasts extend a lane's sum into the previous row (lanes 15 and 47) and the
 // previous half (lane 31) when no segment starts between that row's (or half's)
 // first lane and the lane itself.  The masks are wave-uniform bit arithmetic.
-__device__ __forceinline__ void seg_scan(uint64_t starts, float& n, float& d) {
+template <class V>
+__device__ __forceinline__ void seg_scan(uint64_t starts, V& n, V& d) {
     uint64_t m = ~starts;
     seg_step<kRowShr1>(m, n, d);
     m &= m << 1;
@@ -164,9 +194,10 @@ __device__ __forceinline__ double lane_f64(double v, int src) {
     return __builtin_bit_cast(double, r);
 }
 
-__device__ __forceinline__ float coordinate(double num, double den, double lambda) {
-    double d = lambda + den;
-    return d == 0.0 ? 0.0f : (float)(num / d);
+template <class V>
+__device__ __forceinline__ V coordinate(double num, double den, double lambda) {
+    const double d = lambda + den;
+    return d == 0.0 ? V(0) : (V)(num / d);
 }
 
 template <int MODE> struct Needs {
@@ -179,27 +210,30 @@ template <int MODE> struct Needs {
 };
 
 // Where a pass reads its gathered vectors: LDS slices of the tile, or global.
+template <class V>
 struct Gather {
-    const float* lx;
-    const float* lq;
-    const float* lqq;
+    const V* lx;
+    const V* lq;
+    const V* lqq;
     rsrc_t gx, gq, gqq;
 };
 
-template <bool STAGED>
-__device__ __forceinline__ float gat(const float* lds, rsrc_t g, uint32_t c) {
+template <bool STAGED, class V>
+__device__ __forceinline__ V gat(const V* lds, rsrc_t g, uint32_t c) {
     if constexpr (STAGED)
         return lds[c];
-    else
+    else if constexpr (sizeof(V) == 4)
         return ld_f32(g, c * 4u);
+    else
+        return ld_f64(g, c * 8u);
 }
 
 // Residual bookkeeping of a mode applied to one stored value.
-template <int MODE>
-__device__ __forceinline__ float rhat(float v, float qv, float qqv, float pr, float ppr) {
-    if constexpr (MODE == kModeAdd) return __builtin_fmaf(pr, qv, v);
-    if constexpr (MODE == kModeSubAdd) return __builtin_fmaf(pr, qv, __builtin_fmaf(-ppr, qqv, v));
-    if constexpr (MODE == kModeFlush) return __builtin_fmaf(-ppr, qqv, v);
+template <int MODE, class V>
+__device__ __forceinline__ V rhat(V v, V qv, V qqv, V pr, V ppr) {
+    if constexpr (MODE == kModeAdd) return fmav(pr, qv, v);
+    if constexpr (MODE == kModeSubAdd) return fmav(pr, qv, fmav(-ppr, qqv, v));
+    if constexpr (MODE == kModeFlush) return fmav(-ppr, qqv, v);
     return v;
 }
 
@@ -207,26 +241,27 @@ __device__ __forceinline__ float rhat(float v, float qv, float qqv, float pr, fl
 // Copy the tile's slice of every gathered vector into LDS at the swizzled
 // positions, with a zero at the padding index.  Slots come in the order x, q,
 // qq; x shares q's slot when they are the same vector.
-template <int MODE>
-__device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* lds, Gather& gx) {
+template <int MODE, class V>
+__device__ __forceinline__ void stage_tile(const PassArgs<V>& a, int tile, V* lds, Gather<V>& gx) {
     using N = Needs<MODE>;
     const int T = a.T, Ts = a.Ts;
     const int c0 = tile * T;
     const int len = min(T, a.cols - c0);
     const bool alias = N::x && N::q && a.x_is_q;
     int slot = 0;
-    float* sx = nullptr;
-    float* sq = nullptr;
-    float* sqq = nullptr;
+    V* sx = nullptr;
+    V* sq = nullptr;
+    V* sqq = nullptr;
     if (N::x && !alias) sx = lds + (slot++) * Ts;
     if (N::q) sq = lds + (slot++) * Ts;
     if (alias) sx = sq;
     if (N::qq) sqq = lds + (slot++) * Ts;
-    // Sixteen strided elements per thread per step, loads first, so that a step
-    // costs one memory latency (one or two steps cover a tile).
-    constexpr int kU = 16;
+    // Strided elements per thread per step, loads first, so that a step costs one
+    // memory latency: sixteen floats (one or two steps cover a tile), or four
+    // doubles, which keeps the fused double kernels within their registers.
+    constexpr int kU = sizeof(V) == 4 ? 16 : 4;
     for (int i0 = (int)threadIdx.x; i0 < len; i0 += kU * kWG) {
-        float vx[kU], vq[kU], vqq[kU];
+        V vx[kU], vq[kU], vqq[kU];
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const int i = min(i0 + u * kWG, len - 1);
@@ -246,9 +281,9 @@ __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* l
         }
     }
     if (threadIdx.x == 0) {
-        if (N::x && !alias) sx[a.pad] = 0.0f;
-        if (N::q) sq[a.pad] = 0.0f;
-        if (N::qq) sqq[a.pad] = 0.0f;
+        if (N::x && !alias) sx[a.pad] = V(0);
+        if (N::q) sq[a.pad] = V(0);
+        if (N::qq) sqq[a.pad] = V(0);
     }
     gx.lx = sx;
     gx.lq = sq;
@@ -258,23 +293,26 @@ __device__ __forceinline__ void stage_tile(const PassArgs& a, int tile, float* l
 // What a window needs from memory before its arithmetic: the lane's kE values
 // and indices, and the row scalars of segment sb + lane (the window's segments
 // are sb .. sb + 64, sb being the one open before its first entry).
+template <class V>
 struct Win {
-    f32x4 v0, v1;
+    static constexpr int E = 16 / sizeof(V);  // values per 128-bit access
+    typename Vec16<V>::type vv[kE / E];
     u32x4 c0, c1;  // IDX16: c0 holds the 8 indices packed in pairs
-    float pr, ppr;
+    V pr, ppr;
 };
 
 // Data loads of the window block at b (a multiple of kWin): lane l's values from
 // the two halves of the block (val_slot order), its indices in entry order.
 // Lanes at or past `lim` read lane 0's part instead, so every address stays
 // inside the arrays; a window past the chunk rereads block b.
-template <bool IDX16>
-__device__ __forceinline__ void load_data(const PassArgs& a, int64_t b, int64_t lim, uint32_t le,
-                                          Win& w) {
+template <bool IDX16, class V>
+__device__ __forceinline__ void load_data(const PassArgs<V>& a, int64_t b, int64_t lim, uint32_t le,
+                                          Win<V>& w) {
+    using VV = typename Vec16<V>::type;
     const bool in = b + (int64_t)le < lim;
-    const f32x4* vp = reinterpret_cast<const f32x4*>(a.val + b + (in ? (int64_t)(le >> 1) : 0));
-    w.v0 = __builtin_nontemporal_load(vp);
-    w.v1 = __builtin_nontemporal_load(vp + kWin / 8);
+    const VV* vp = reinterpret_cast<const VV*>(a.val + b) + (in ? (int)(le / kE) : 0);
+#pragma unroll
+    for (int q = 0; q < kE / Win<V>::E; ++q) w.vv[q] = __builtin_nontemporal_load(vp + 64 * q);
     const int64_t eb = b + (in ? (int64_t)le : 0);
     if constexpr (IDX16) {
         w.c0 = __builtin_nontemporal_load(
@@ -286,8 +324,8 @@ __device__ __forceinline__ void load_data(const PassArgs& a, int64_t b, int64_t 
     }
 }
 // Row scalars of segments sb .. sb + 63, one per lane.
-template <int MODE>
-__device__ __forceinline__ void load_slots(const PassArgs& a, int sb, int lane, Win& w) {
+template <int MODE, class V>
+__device__ __forceinline__ void load_slots(const PassArgs<V>& a, int sb, int lane, Win<V>& w) {
     using N = Needs<MODE>;
     if constexpr (N::p || N::pp) {
         const int sj = min(max(sb + lane, 0), a.nseg - 1);
@@ -297,8 +335,8 @@ __device__ __forceinline__ void load_slots(const PassArgs& a, int sb, int lane, 
 }
 
 // Index of entry k of the lane, without the segment start bit.
-template <bool IDX16>
-__device__ __forceinline__ uint32_t col_of(const Win& w, int k) {
+template <bool IDX16, class V>
+__device__ __forceinline__ uint32_t col_of(const Win<V>& w, int k) {
     using B = IndexBits<typename std::conditional<IDX16, uint16_t, int32_t>::type>;
     uint32_t c;
     if constexpr (IDX16) {
@@ -309,17 +347,31 @@ __device__ __forceinline__ uint32_t col_of(const Win& w, int k) {
     }
     return k == 0 ? (c & B::mask) : c;  // only a lane's first entry carries the bit
 }
-template <bool IDX16>
-__device__ __forceinline__ bool starts_segment(const Win& w) {
+template <bool IDX16, class V>
+__device__ __forceinline__ bool starts_segment(const Win<V>& w) {
     using B = IndexBits<typename std::conditional<IDX16, uint16_t, int32_t>::type>;
     return (w.c0[0] & B::start) != 0u;
 }
-__device__ __forceinline__ float val_of(const Win& w, int k) { return k < 4 ? w.v0[k] : w.v1[k - 4]; }
+template <class V>
+__device__ __forceinline__ V val_of(const Win<V>& w, int k) {
+    return w.vv[k / Win<V>::E][k % Win<V>::E];
+}
 
 __device__ __forceinline__ float lane_pick(float v, uint32_t src) {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((int)(src << 2),
                                                                   __builtin_bit_cast(int, v)));
 }
+__device__ __forceinline__ double lane_pick(double v, uint32_t src) {
+    const int2 x = __builtin_bit_cast(int2, v);
+    int2 r;
+    r.x = __builtin_amdgcn_ds_bpermute((int)(src << 2), x.x);
+    r.y = __builtin_amdgcn_ds_bpermute((int)(src << 2), x.y);
+    return __builtin_bit_cast(double, r);
+}
+__device__ __forceinline__ double lane_read(float v, int src) {
+    return (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), src));
+}
+__device__ __forceinline__ double lane_read(double v, int src) { return lane_f64(v, src); }
 
 // State a wave carries from window to window of its chunk.
 struct Walk {
@@ -336,13 +388,13 @@ struct Walk {
 // A segment's sums over this chunk: its coordinate (P == 1: segment s is row s)
 // or partial, or, for a segment that began in an earlier chunk, the chunk's
 // head partial.
-template <bool P1>
-__device__ __forceinline__ void emit(const PassArgs& a, const Walk& wk, int s, double num,
+template <bool P1, class V>
+__device__ __forceinline__ void emit(const PassArgs<V>& a, const Walk& wk, int s, double num,
                                      double den) {
     if (s == wk.mid)
         a.part[wk.head] = make_double2(num, den);
     else if constexpr (P1)
-        a.y[s] = coordinate(num, den, a.lambda);
+        a.y[s] = coordinate<V>(num, den, a.lambda);
     else
         a.part[s] = make_double2(num, den);
 }
@@ -355,9 +407,10 @@ __device__ __forceinline__ void emit(const PassArgs& a, const Walk& wk, int s, d
 // gives every segment's window sum at its last lane, and the lane that starts
 // the next segment emits it.  The data of the window after next is requested
 // first, so two windows' loads are in flight while this one is reduced.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
-__device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk& wk,
-                                       const Win& cur, Win& nxt, Win& nn, int lane, uint32_t le) {
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+__device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx, Walk& wk,
+                                       const Win<V>& cur, Win<V>& nxt, Win<V>& nn, int lane,
+                                       uint32_t le) {
     using N = Needs<MODE>;
     const int64_t b = wk.elo;
     const int64_t we = min(b + (int64_t)kWin, wk.c1);
@@ -366,14 +419,14 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
     {
         const int64_t b2 = we + kWin;
         const bool more = b2 < wk.c1;
-        load_data<IDX16>(a, more ? b2 : b, more ? wk.c1 : b, le, nn);
+        load_data<IDX16, V>(a, more ? b2 : b, more ? wk.c1 : b, le, nn);
     }
     const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
     const bool lv = lane < nl;
-    const bool fl = lv && starts_segment<IDX16>(cur);
+    const bool fl = lv && starts_segment<IDX16, V>(cur);
     const uint64_t starts = __ballot(fl);
     const int sb_n = wk.sb + __builtin_popcountll(starts);
-    load_slots<MODE>(a, sb_n, lane, nxt);  // the next window's row scalars
+    load_slots<MODE, V>(a, sb_n, lane, nxt);  // the next window's row scalars
 
     // Segments started at lanes 0 .. lane: the lane's segment is sb + cl.
     const uint64_t sh = starts >> 1;
@@ -382,7 +435,7 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
 
     // Row scalars of the lane's segment, from the window's slots; with 64 starts the
     // last lane's segment is sb + 64, past the slots.
-    float pr = 0.0f, ppr = 0.0f;
+    V pr = V(0), ppr = V(0);
     if constexpr (N::p) pr = lane_pick(cur.pr, cl);
     if constexpr (N::pp) ppr = lane_pick(cur.ppr, cl);
     if constexpr (N::p || N::pp) {
@@ -393,45 +446,52 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
     }
 
     // Gathers, residual bookkeeping, and the lane's sums.
-    float r[kE];
-    float an = 0.0f, ad = 0.0f;
+    V r[kE];
+    V an = V(0), ad = V(0);
 #pragma unroll
     for (int k = 0; k < kE; ++k) {
-        const uint32_t c = col_of<IDX16>(cur, k);
-        const float qv = N::q ? gat<STAGED>(gx.lq, gx.gq, c) : 0.0f;
-        const float qqv = N::qq ? gat<STAGED>(gx.lqq, gx.gqq, c) : 0.0f;
-        r[k] = rhat<MODE>(val_of(cur, k), qv, qqv, pr, ppr);
+        const uint32_t c = col_of<IDX16, V>(cur, k);
+        const V qv = N::q ? gat<STAGED, V>(gx.lq, gx.gq, c) : V(0);
+        const V qqv = N::qq ? gat<STAGED, V>(gx.lqq, gx.gqq, c) : V(0);
+        r[k] = rhat<MODE, V>(val_of<V>(cur, k), qv, qqv, pr, ppr);
         if constexpr (N::x) {
-            const float xv = XQ ? qv : gat<STAGED>(gx.lx, gx.gx, c);
-            an = __builtin_fmaf(r[k], xv, an);
-            ad = __builtin_fmaf(xv, xv, ad);
+            const V xv = XQ ? qv : gat<STAGED, V>(gx.lx, gx.gx, c);
+            an = fmav(r[k], xv, an);
+            ad = fmav(xv, xv, ad);
         }
     }
     if constexpr (N::store) {
         // R-hat back to the lane's two value groups: each store instruction of the
         // wave covers 1 KB of contiguous memory.
         if (lv) {
-            f32x4* wp = reinterpret_cast<f32x4*>(a.val + b + (le >> 1));
-            __builtin_nontemporal_store(f32x4{r[0], r[1], r[2], r[3]}, wp);
-            __builtin_nontemporal_store(f32x4{r[4], r[5], r[6], r[7]}, wp + kWin / 8);
+            using VV = typename Vec16<V>::type;
+            constexpr int E = Win<V>::E;
+            VV* wp = reinterpret_cast<VV*>(a.val + b) + (int)(le / kE);
+#pragma unroll
+            for (int q = 0; q < kE / E; ++q) {
+                VV w;
+#pragma unroll
+                for (int e = 0; e < E; ++e) w[e] = r[q * E + e];
+                __builtin_nontemporal_store(w, wp + 64 * q);
+            }
         }
     }
     if constexpr (MODE == kModeFlush) {
-        float s2 = 0.0f;
+        V s2 = V(0);
 #pragma unroll
-        for (int k = 0; k < kE; ++k) s2 = __builtin_fmaf(r[k], r[k], s2);
+        for (int k = 0; k < kE; ++k) s2 = fmav(r[k], r[k], s2);
         if (lv) wk.sse += (double)s2;
     } else {
         if (!lv) {
-            an = 0.0f;
-            ad = 0.0f;
+            an = V(0);
+            ad = V(0);
         }
         seg_scan(starts, an, ad);
         // A lane that starts a segment emits the previous one: its sum over the
         // earlier lanes of the window (the scan at the lane before), plus the sums
         // from earlier windows when it is the window's first segment.
-        const float pn = dpp_f<kWaveShr1, 0xF, true>(0.0f, an);
-        const float pd = dpp_f<kWaveShr1, 0xF, true>(0.0f, ad);
+        const V pn = dpp_v<kWaveShr1, 0xF, true>(V(0), an);
+        const V pd = dpp_v<kWaveShr1, 0xF, true>(V(0), ad);
         if (fl) {
             const bool first = lane == (int)__builtin_ctzll(starts);
             double en = (double)pn, ed = (double)pd;
@@ -439,12 +499,12 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
                 en += wk.cn;
                 ed += wk.cd;
             }
-            if (wk.open || lane > 0) emit<P1>(a, wk, wk.sb + (int)cl - 1, en, ed);
+            if (wk.open || lane > 0) emit<P1, V>(a, wk, wk.sb + (int)cl - 1, en, ed);
         }
         // The segment of the window's last lane stays open.
         const int ll = nl - 1;
-        const double ln = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, an), ll));
-        const double ld = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ad), ll));
+        const double ln = lane_read(an, ll);
+        const double ld = lane_read(ad, ll);
         if (starts == 0ull) {
             wk.cn += ln;
             wk.cd += ld;
@@ -464,31 +524,31 @@ __device__ __forceinline__ void window(const PassArgs& a, const Gather& gx, Walk
 // with the staging of the tile.  s0 is the segment holding entry
 // c0; it began in an earlier chunk when the chunk's first lane does not start it
 // (flag kChunkMid).
-template <int MODE, bool IDX16>
-__device__ __forceinline__ void begin_chunk(const PassArgs& a, int64_t c0, int64_t c1, int s0,
-                                            int flags, int lane, Win& wa, Win& wb) {
+template <int MODE, bool IDX16, class V>
+__device__ __forceinline__ void begin_chunk(const PassArgs<V>& a, int64_t c0, int64_t c1, int s0,
+                                            int flags, int lane, Win<V>& wa, Win<V>& wb) {
     const uint32_t le = (uint32_t)lane * kE;
-    load_data<IDX16>(a, c0, c1, le, wa);
-    load_slots<MODE>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
+    load_data<IDX16, V>(a, c0, c1, le, wa);
+    load_slots<MODE, V>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
     const bool more = c0 + kWin < c1;
-    load_data<IDX16>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
+    load_data<IDX16, V>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
 }
 
 // wa and wb hold the requests of begin_chunk.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
-__device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, int64_t c0,
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+__device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>& gx, int64_t c0,
                                           int64_t c1, int s0, int flags, int gc, int lane,
-                                          Win& wa, Win& wb, double& sse) {
+                                          Win<V>& wa, Win<V>& wb, double& sse) {
     const uint32_t le = (uint32_t)lane * kE;
     const bool mid = flags & kChunkMid;
     Walk wk{c0, c1, mid ? s0 : s0 - 1, mid, 0.0, 0.0, sse, mid ? s0 : -1, a.nseg + 2 * gc};
-    Win wc;
+    Win<V> wc;
     while (true) {
-        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wa, wb, wc, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wa, wb, wc, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wb, wc, wa, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wb, wc, wa, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, XQ>(a, gx, wk, wc, wa, wb, lane, le);
+        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wc, wa, wb, lane, le);
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
@@ -498,7 +558,7 @@ __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, i
             if (flags & kChunkCont)
                 a.part[wk.head + (wk.sb == wk.mid ? 0 : 1)] = make_double2(wk.cn, wk.cd);
             else
-                emit<P1>(a, wk, wk.sb, wk.cn, wk.cd);
+                emit<P1, V>(a, wk, wk.sb, wk.cn, wk.cd);
         }
     }
     sse = wk.sse;
@@ -507,15 +567,16 @@ __device__ __forceinline__ void run_chunk(const PassArgs& a, const Gather& gx, i
 // One pass: the workgroup's pieces in order, each staging its tile (when it
 // differs from the one staged) and then giving every wave its chunk.  XQ: the
 // update gathers the same vector as the add-back (x == q), read once per entry.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ>
-__device__ __forceinline__ void pass_main(const PassArgs& a) {
+template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+__device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     using N = Needs<MODE>;
-    extern __shared__ float lds[];
+    extern __shared__ f32x4 lds_raw[];  // 16-byte aligned
+    V* lds = reinterpret_cast<V*>(lds_raw);
     const int wg = blockIdx.x;
 
-    Gather gx{};
+    Gather<V> gx{};
     if constexpr (!STAGED) {
-        const uint64_t vb = (uint64_t)a.cols * 4u;
+        const uint64_t vb = (uint64_t)a.cols * sizeof(V);
         if (N::x) gx.gx = make_rsrc(a.x, vb);
         if (N::q) gx.gq = make_rsrc(a.q, vb);
         if (N::qq) gx.gqq = make_rsrc(a.qq, vb);
@@ -526,7 +587,7 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
     if constexpr (MODE != kModeFlush && P1) {
         // The rows after the last non-empty one have no entries: coordinate 0.
         for (int i = wg * kWG + (int)threadIdx.x; i < a.rows - a.nseg_ne; i += gridDim.x * kWG)
-            a.y[a.nseg_ne + i] = coordinate(0.0, 0.0, a.lambda);
+            a.y[a.nseg_ne + i] = coordinate<V>(0.0, 0.0, a.lambda);
     }
 
     double sse = 0.0;
@@ -538,19 +599,19 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
         const int s0 = a.piece_seg[gc], flags = a.chunk_flags[gc];
         // The chunk's first windows are requested before the staging, which they do
         // not depend on.
-        Win wa, wb;
-        if (c0 < c1) begin_chunk<MODE, IDX16>(a, c0, c1, s0, flags, lane, wa, wb);
+        Win<V> wa, wb;
+        if (c0 < c1) begin_chunk<MODE, IDX16, V>(a, c0, c1, s0, flags, lane, wa, wb);
         if constexpr (STAGED) {
             const int tile = a.piece_tile[pc];
             if (tile != staged) {
                 if (staged >= 0) __syncthreads();  // every wave is done with the old slice
-                stage_tile<MODE>(a, tile, lds, gx);
+                stage_tile<MODE, V>(a, tile, lds, gx);
                 __syncthreads();
                 staged = tile;
             }
         }
         if (c0 < c1)
-            run_chunk<MODE, STAGED, IDX16, P1, XQ>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
+            run_chunk<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -561,29 +622,29 @@ __device__ __forceinline__ void pass_main(const PassArgs& a) {
 }  // namespace
 
 // Distinct kernel names per pass kind, so that profiles separate them.  The
-// template arguments select LDS staging, the index width and whether segments
-// are rows (P == 1).
-template <bool STAGED, bool IDX16, bool P1>
-__global__ __launch_bounds__(kWG) void ccd_pass(PassArgs a) {
-    pass_main<kModePlain, STAGED, IDX16, P1, false>(a);
+// template arguments select LDS staging, the index width, whether segments are
+// rows (P == 1) and the value type.
+template <bool STAGED, bool IDX16, bool P1, class V>
+__global__ __launch_bounds__(kWG) void ccd_pass(PassArgs<V> a) {
+    pass_main<kModePlain, STAGED, IDX16, P1, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1>
-__global__ __launch_bounds__(kWG) void ccd_pass_fused_first(PassArgs a) {
+template <bool STAGED, bool IDX16, bool P1, class V>
+__global__ __launch_bounds__(kWG) void ccd_pass_fused_first(PassArgs<V> a) {
     if (a.x_is_q)
-        pass_main<kModeAdd, STAGED, IDX16, P1, true>(a);
+        pass_main<kModeAdd, STAGED, IDX16, P1, true, V>(a);
     else
-        pass_main<kModeAdd, STAGED, IDX16, P1, false>(a);
+        pass_main<kModeAdd, STAGED, IDX16, P1, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1>
-__global__ __launch_bounds__(kWG) void ccd_pass_fused(PassArgs a) {
+template <bool STAGED, bool IDX16, bool P1, class V>
+__global__ __launch_bounds__(kWG) void ccd_pass_fused(PassArgs<V> a) {
     if (a.x_is_q)
-        pass_main<kModeSubAdd, STAGED, IDX16, P1, true>(a);
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, true, V>(a);
     else
-        pass_main<kModeSubAdd, STAGED, IDX16, P1, false>(a);
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1>
-__global__ __launch_bounds__(kWG) void ccd_flush(PassArgs a) {
-    pass_main<kModeFlush, STAGED, IDX16, P1, false>(a);
+template <bool STAGED, bool IDX16, bool P1, class V>
+__global__ __launch_bounds__(kWG) void ccd_flush(PassArgs<V> a) {
+    pass_main<kModeFlush, STAGED, IDX16, P1, false, V>(a);
 }
 
 // x summed over the 16 lanes of a DPP row; every lane of the row gets the same
@@ -601,7 +662,8 @@ __device__ __forceinline__ double row16_sum(double x) {
 // tree over the 16 lanes.  With yseg, the coordinate is also written to every
 // segment of the row.
 constexpr int kCombineLanes = 16;
-__global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
+template <class V>
+__global__ __launch_bounds__(256) void ccd_combine(CombineArgs<V> c) {
     const int l = (int)(threadIdx.x & (kCombineLanes - 1));
     const int i = blockIdx.x * (256 / kCombineLanes) + (int)(threadIdx.x / kCombineLanes);
     if (i >= c.n) return;  // whole 16-lane rows leave together
@@ -615,14 +677,15 @@ __global__ __launch_bounds__(256) void ccd_combine(CombineArgs c) {
     }
     num = row16_sum(num);
     den = row16_sum(den);
-    const float yr = coordinate(num, den, c.lambda);
+    const V yr = coordinate<V>(num, den, c.lambda);
     if (l == 0) c.y[c.ids ? c.ids[i] : i] = yr;
     if (c.yseg)
         for (int k = c.seg_ptr[i] + l; k < c.seg_ptr[i + 1]; k += kCombineLanes) c.yseg[c.segs[k]] = yr;
 }
 
-__global__ __launch_bounds__(256) void ccd_copy(const float* __restrict__ src,
-                                                float* __restrict__ dst, int64_t n) {
+template <class V>
+__global__ __launch_bounds__(256) void ccd_copy(const V* __restrict__ src, V* __restrict__ dst,
+                                                int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < n) dst[i] = src[i];
 }
@@ -654,10 +717,10 @@ int staged_vectors(PassMode mode, bool x_is_q) {
 }
 
 namespace {
-template <bool S, bool I, bool P1>
+template <bool S, bool I, bool P1, class V>
 hipError_t raise_lds() {
-    const void* ks[] = {(const void*)ccd_pass<S, I, P1>, (const void*)ccd_pass_fused_first<S, I, P1>,
-                        (const void*)ccd_pass_fused<S, I, P1>, (const void*)ccd_flush<S, I, P1>};
+    const void* ks[] = {(const void*)ccd_pass<S, I, P1, V>, (const void*)ccd_pass_fused_first<S, I, P1, V>,
+                        (const void*)ccd_pass_fused<S, I, P1, V>, (const void*)ccd_flush<S, I, P1, V>};
     for (const void* k : ks) {
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
         if (e != hipSuccess) return e;
@@ -665,43 +728,51 @@ hipError_t raise_lds() {
     return hipSuccess;
 }
 
-template <bool S, bool I, bool P1>
-void launch_mode(PassMode mode, dim3 grid, size_t lds, hipStream_t s, const PassArgs& a) {
+template <bool S, bool I, bool P1, class V>
+void launch_mode(PassMode mode, dim3 grid, size_t lds, hipStream_t s, const PassArgs<V>& a) {
     switch (mode) {
         case kModePlain:
-            hipLaunchKernelGGL((ccd_pass<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeAdd:
-            hipLaunchKernelGGL((ccd_pass_fused_first<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass_fused_first<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeSubAdd:
-            hipLaunchKernelGGL((ccd_pass_fused<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass_fused<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeFlush:
-            hipLaunchKernelGGL((ccd_flush<S, I, P1>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_flush<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
             break;
     }
+}
+
+template <class V>
+hipError_t raise_lds_all() {
+    hipError_t e = raise_lds<true, true, true, V>();
+    if (e == hipSuccess) e = raise_lds<true, true, false, V>();
+    if (e == hipSuccess) e = raise_lds<false, true, true, V>();
+    if (e == hipSuccess) e = raise_lds<false, false, true, V>();
+    return e;
 }
 }  // namespace
 
 hipError_t sweep_init() {
-    hipError_t e = raise_lds<true, true, true>();
-    if (e == hipSuccess) e = raise_lds<true, true, false>();
-    if (e == hipSuccess) e = raise_lds<false, true, true>();
-    if (e == hipSuccess) e = raise_lds<false, false, true>();
+    hipError_t e = raise_lds_all<float>();
+    if (e == hipSuccess) e = raise_lds_all<double>();
     return e;
 }
 
-hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const float* p,
-                       const float* pp, const float* q, const float* qq, float* y, double lambda,
-                       double* sse_part, hipStream_t s) {
+template <class V>
+hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, const V* pp,
+                       const V* q, const V* qq, V* y, double lambda, double* sse_part,
+                       hipStream_t s) {
     if (L.grid == 0) return hipSuccess;
     const bool staged = L.gather == kGatherLds;
     // Kernel variants: LDS staging uses 16-bit indices; global gathers have P == 1.
     if (staged ? !L.idx16 : L.P != 1) return hipErrorInvalidValue;
-    PassArgs a{};
+    PassArgs<V> a{};
     a.idx = L.idx;
-    a.val = L.val;
+    a.val = static_cast<V*>(L.val);
     a.wg_piece = L.wg_piece;
     a.piece_tile = L.piece_tile;
     a.piece_chunk = L.piece_chunk;
@@ -725,27 +796,28 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const float* x, const flo
     a.nseg_ne = (int32_t)L.nseg_ne;
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
     a.lambda = lambda;
-    a.vec_floats = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
-    const size_t lds = (size_t)a.vec_floats * sizeof(float);
+    a.vec_elems = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
+    const size_t lds = (size_t)a.vec_elems * sizeof(V);
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     const dim3 grid(L.grid);
     if (staged) {
         if (L.P == 1)
-            launch_mode<true, true, true>(mode, grid, lds, s, a);
+            launch_mode<true, true, true, V>(mode, grid, lds, s, a);
         else
-            launch_mode<true, true, false>(mode, grid, lds, s, a);
+            launch_mode<true, true, false, V>(mode, grid, lds, s, a);
     } else if (L.idx16) {
-        launch_mode<false, true, true>(mode, grid, lds, s, a);
+        launch_mode<false, true, true, V>(mode, grid, lds, s, a);
     } else {
-        launch_mode<false, false, true>(mode, grid, lds, s, a);
+        launch_mode<false, false, true, V>(mode, grid, lds, s, a);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda, hipStream_t s) {
+template <class V>
+hipError_t launch_combine(const Layout& L, V* y, V* yseg, double lambda, hipStream_t s) {
     if (L.ncomb == 0) return hipSuccess;
     if (yseg && !L.row_seg_ptr) return hipErrorInvalidValue;
-    CombineArgs c{};
+    CombineArgs<V> c{};
     c.ids = L.comb_rows;
     c.src_ptr = L.src_ptr;
     c.srcs = L.srcs;
@@ -757,14 +829,15 @@ hipError_t launch_combine(const Layout& L, float* y, float* yseg, double lambda,
     c.n = L.ncomb;
     c.lambda = lambda;
     constexpr int rows_per_block = 256 / kCombineLanes;
-    hipLaunchKernelGGL(ccd_combine, dim3((unsigned)((L.ncomb + rows_per_block - 1) / rows_per_block)),
+    hipLaunchKernelGGL(ccd_combine<V>, dim3((unsigned)((L.ncomb + rows_per_block - 1) / rows_per_block)),
                        dim3(256), 0, s, c);
     return hipGetLastError();
 }
 
-hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s) {
+template <class V>
+hipError_t launch_copy(const V* src, V* dst, int64_t n, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(ccd_copy, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
+    hipLaunchKernelGGL(ccd_copy<V>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
     return hipGetLastError();
 }
 
@@ -772,5 +845,14 @@ hipError_t launch_reduce_sum(const double* part, int32_t n, double* out, hipStre
     hipLaunchKernelGGL(ccd_reduce_sum, dim3(1), dim3(256), 0, s, part, n, out);
     return hipGetLastError();
 }
+
+#define CCDK_SWEEP_INSTANTIATE(V)                                                              \
+    template hipError_t launch_pass<V>(const Layout&, PassMode, const V*, const V*, const V*,  \
+                                       const V*, const V*, V*, double, double*, hipStream_t); \
+    template hipError_t launch_combine<V>(const Layout&, V*, V*, double, hipStream_t);        \
+    template hipError_t launch_copy<V>(const V*, V*, int64_t, hipStream_t);
+CCDK_SWEEP_INSTANTIATE(float)
+CCDK_SWEEP_INSTANTIATE(double)
+#undef CCDK_SWEEP_INSTANTIATE
 
 }  // namespace ccdk
