@@ -14,7 +14,10 @@ by re-typing the oracle's own formulas.
 * results do not depend on the thread count;
 * the open outer loop equals single outer iterations, its history equals eq. 1
   and the RMSEs evaluated from the factors, and it stops at the first
-  iteration whose relative decrease of eq. 1 is within the tolerance.
+  iteration whose relative decrease of eq. 1 is within the tolerance;
+* element-wise CCD (Algorithm 2) at k > 1 converges to a point where every
+  single coordinate minimises eq. 1 (golden-section search), never increases
+  eq. 1 and keeps R = A - W H^T.
 """
 import os
 from fractions import Fraction
@@ -244,6 +247,54 @@ def test_train_rmse_matches_prediction_error_on_training_set():
     o = Oracle(m, n, k, lam, row, col, val, H0)
     o.run(2, 2)
     assert abs(o.train_rmse() - o.test_rmse(row, col, val)) < 1e-12
+
+
+def _coordinate_minimum(A_terms, lam):
+    """argmin_z sum (a - z b)^2 + lam z^2 for pairs (a, b), by golden-section search."""
+    return _golden_min(lambda z: sum((a - z * b) ** 2 for a, b in A_terms) + lam * z * z, -50.0, 50.0)
+
+
+def test_elementwise_ccd_converges_to_a_coordinatewise_minimum():
+    # Algorithm 2 at k = 3 (where it differs from CCD++): at its fixed point every
+    # single coordinate w_it and h_jt minimises eq. 1 with all others held, which is
+    # checked by golden-section search on eq. 1 evaluated from A and the factors.
+    m, n, k, nnz, lam = 12, 9, 3, 60, 0.3
+    row, col, val, H0 = synth.small_random(m, n, nnz, k, seed=21)
+    row, col, val = np.asarray(row), np.asarray(col), np.asarray(val, np.float64)
+    o = Oracle(m, n, k, lam, row, col, val, H0)
+    o.ccd_run(400)
+    W, H = o.factors()
+    o.ccd_run(1)
+    W2, H2 = o.factors()
+    assert np.max(np.abs(W2 - W)) < 1e-9 and np.max(np.abs(H2 - H)) < 1e-9  # converged
+    for i in range(m):
+        e = np.nonzero(row == i)[0]
+        for t in range(k):
+            others = val[e] - (W[i] @ H[col[e]].T) + W[i, t] * H[col[e], t]
+            z = _coordinate_minimum(list(zip(others, H[col[e], t])), lam)
+            assert abs(z - W[i, t]) <= 1e-6 * max(1.0, abs(z)), (i, t)
+    for j in range(n):
+        e = np.nonzero(col == j)[0]
+        for t in range(k):
+            others = val[e] - np.einsum("ij,j->i", W[row[e]], H[j]) + W[row[e], t] * H[j, t]
+            z = _coordinate_minimum(list(zip(others, W[row[e], t])), lam)
+            assert abs(z - H[j, t]) <= 1e-6 * max(1.0, abs(z)), (j, t)
+
+
+def test_elementwise_ccd_objective_monotone_and_residual_invariant():
+    m, n, k, nnz, lam = 50, 40, 4, 600, 0.1
+    row, col, val, H0 = synth.small_random(m, n, nnz, k, seed=22)
+    row, col, val = np.asarray(row), np.asarray(col), np.asarray(val, np.float64)
+    o = Oracle(m, n, k, lam, row, col, val, H0)
+    fs = []
+    for _ in range(6):
+        o.ccd_run(1)
+        W, H = o.factors()
+        pred = np.einsum("ij,ij->i", W[row], H[col])
+        np.testing.assert_allclose(o.residual(), val - pred, rtol=0, atol=1e-12)
+        fs.append(float(np.sum((val - pred) ** 2) + lam * (np.sum(W * W) + np.sum(H * H))))
+    assert all(b <= a * (1 + 1e-12) for a, b in zip(fs, fs[1:])), fs
+    assert fs[-1] < 0.9 * fs[0]
 
 
 def _numpy_objective_and_rmse(W, H, lam, row, col, val, trow, tcol, tval):
