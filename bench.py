@@ -76,13 +76,23 @@ def stored_traffic(key: str, workload: str, precision: str = "f32"):
     return None if k is None else k.get("bytes_per_launch")
 
 
-def cpu_baseline(ds, k, inner, budget_s, threads):
+def cpu_baseline(ds, k, inner, budget_s, threads, algorithm="ccdpp"):
     import numpy as np
     from oracle import Oracle
 
     w = ds.workload
     log(f"cpu baseline: building the oracle on {w.name} ({threads} threads)")
     o = Oracle(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val, ds.h0(k), threads=threads)
+    if algorithm == "ccd":
+        # One whole outer iteration of Algorithm 2 (it cannot be cut per feature).
+        t0 = time.perf_counter()
+        o.ccd_run(1)
+        dt = time.perf_counter() - t0
+        o.close()
+        log(f"cpu baseline: one element-wise CCD outer iteration in {dt:.2f}s")
+        return {"value": 2.0 * k * w.nnz / dt / 1e9, "unit": "Gnnz/s", "cores": threads,
+                "kind": "oracle", "sample": f"one outer iteration of element-wise CCD on the full "
+                                            f"{w.name} matrix, fp64 oracle, {dt:.1f} s"}
     done = 0
     t0 = time.perf_counter()
     while done < k:
@@ -109,6 +119,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--algorithm", default="ccdpp", choices=["ccdpp", "ccd"],
+                    help="ccdpp: Algorithm 3 (the headline); ccd: element-wise CCD, Algorithm 2")
     ap.add_argument("--precision", default="f32", choices=["f32", "f64"],
                     help="value type of the residual, factors and sweep arithmetic")
     ap.add_argument("--no-open-loop", action="store_true",
@@ -171,11 +183,17 @@ def main():
                         "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
         return kinds, per_layout
 
+    def step():
+        if args.algorithm == "ccd":
+            g.ccd_run(1)
+        else:
+            g.run(1, inner)
+
     def timed(steps):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(steps):
-            g.run(1, inner)
+            step()
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) * 1e3 / steps
 
@@ -186,7 +204,7 @@ def main():
         last = i + 1 == args.warmup and not args.no_prof
         if last:
             g.profile(True)
-        g.run(1, inner)
+        step()
         if last:
             torch.cuda.synchronize()
             kinds, per_layout = read_kernels()
@@ -215,7 +233,9 @@ def main():
         g.profile_only(-1, -1)
         g.profile(False)
     ms_plain = timed(max(2, args.steps // 2)) if prof else ms
-    visits = 2.0 * inner * k * w.nnz
+    # Nonzero visits per step: CCD++ visits every entry 2 * inner times per feature;
+    # element-wise CCD visits it once per feature in each of its two phases.
+    visits = (2.0 if args.algorithm == "ccd" else 2.0 * inner) * k * w.nnz
     value = visits / (ms * 1e-3) / 1e9
     log(f"{ms:.3f} ms/step (events on the dominant kernel), {ms_plain:.3f} ms/step without; "
         f"{value:.1f} Gnnz/s")
@@ -238,7 +258,7 @@ def main():
     # the objective of eq. 1 and the training and held-out RMSE (the held-out triplets
     # are copied to the device once per call, inside this time).
     open_loop = None
-    if not args.no_open_loop:
+    if not args.no_open_loop and args.algorithm == "ccdpp":
         test = (ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -258,7 +278,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         threads = min(16, os.cpu_count() or 1)
-        cpu = cpu_baseline(synth.load(args.workload), k, inner, args.cpu_budget, threads)
+        cpu = cpu_baseline(synth.load(args.workload), k, inner, args.cpu_budget, threads,
+                           args.algorithm)
 
     out = {
         "metric": "CCD++ nonzeros/sec (G/s) + achieved HBM GB/s vs peak; s per outer iter",
@@ -275,8 +296,10 @@ def main():
         "dtype": args.precision,
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.m}x{w.n}, nnz={w.nnz}, k={k}, lambda={w.lam}, "
-                               f"inner={inner}; step = 1 outer iteration",
-                   "m": w.m, "n": w.n, "nnz": w.nnz, "k": k, "inner_iters": inner},
+                               + (f"inner={inner}; step = 1 outer iteration" if args.algorithm == "ccdpp"
+                                  else "element-wise CCD (Algorithm 2); step = 1 outer iteration"),
+                   "m": w.m, "n": w.n, "nnz": w.nnz, "k": k, "inner_iters": inner,
+                   "algorithm": args.algorithm},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "model_bytes_per_step": model_bytes,

@@ -121,6 +121,13 @@ int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  */
 int ccdpp_run(ccdpp_t *h, int32_t outer_iters, int32_t inner_iters);
 
+/* Algorithm 2, element-wise CCD (Section 3.2.1): outer_iters iterations of,
+ * for every row i and feature t in order, w_it from eq. 5 with the residual
+ * update of eq. 6-7, then for every column j and feature t, h_jt from eq. 8
+ * with eq. 9-10.  Same state as ccdpp_run (the two may be mixed), the same
+ * float or double arithmetic.  outer_iters >= 0.  Blocking. */
+int ccdpp_ccd_run(ccdpp_t *h, int32_t outer_iters);
+
 /* Algorithm 3 with its outer loop left open (Section 3.2.2: iterate until
  * convergence or a bound on the iterations): outer iterations of
  * ccdpp_run(h, 1, inner_iters), each followed by the objective f of eq. 1

@@ -66,6 +66,7 @@ def lib() -> ctypes.CDLL:
             "ccdpp_create_ex": ([i64, i64, i32, dbl, i64, P, P, P, u64, ctypes.POINTER(Options),
                                  ctypes.POINTER(P)], ctypes.c_int),
             "ccdpp_run": ([P, i32, i32], ctypes.c_int),
+            "ccdpp_ccd_run": ([P, i32], ctypes.c_int),
             "ccdpp_run_until": ([P, i32, i32, dbl, i64, P, P, P, P, ctypes.POINTER(i32)],
                                 ctypes.c_int),
             "ccdpp_get_factors": ([P, P, P], ctypes.c_int),
@@ -136,6 +137,10 @@ def ccdpp_create_ex(m, n, k, lam, row, col, val, seed=0, opts=None):
 
 def ccdpp_run(h, outer_iters, inner_iters):
     _check(h, lib().ccdpp_run(h, int(outer_iters), int(inner_iters)))
+
+
+def ccdpp_ccd_run(h, outer_iters):
+    _check(h, lib().ccdpp_ccd_run(h, int(outer_iters)))
 
 
 def ccdpp_run_until(h, max_outer, inner_iters, rel_tol, test=None):
@@ -284,6 +289,10 @@ class CCDPP:
 
     def run(self, outer_iters, inner_iters):
         ccdpp_run(self._h, outer_iters, inner_iters)
+
+    def ccd_run(self, outer_iters):
+        """Algorithm 2 (element-wise CCD)."""
+        ccdpp_ccd_run(self._h, outer_iters)
 
     def run_until(self, max_outer, inner_iters, rel_tol, test=None):
         return ccdpp_run_until(self._h, max_outer, inner_iters, rel_tol, test)

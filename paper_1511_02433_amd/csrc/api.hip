@@ -856,6 +856,62 @@ int launch_test_err_any(ccdpp* h, const int32_t* dr, const int32_t* dc, const fl
     });
 }
 
+// Algorithm 2 (element-wise CCD): per outer iteration, every row's k coordinates
+// in order (eq. 5, then the residual update of eq. 6-7), then every column's (eq.
+// 8, eq. 9-10).  Rows are independent within the W phase, so the row loop and the
+// feature loop are exchanged: pass t over the user-major copy computes w_.t for
+// every row from R-hat = R + w_.t h_.t (the same pass as CCD++'s first u-pass), and
+// the residual update of feature t is folded, as a pending subtract, into pass
+// t + 1 (and a final flush).  The H phase does the same on the item-major copy.
+// After each phase the other copy is refreshed from the updated one through the
+// entry maps, so both copies hold the same residual again.
+template <class V>
+int ccd_impl(ccdpp* h, int32_t outer) {
+    using namespace ccdk;
+    const int64_t m = h->m, n = h->n;
+    for (int32_t it = 0; it < outer; ++it) {
+        for (int li = 0; li < 2; ++li) {
+            V* own = as<V>(li == 0 ? h->W : h->H);
+            V* other = as<V>(li == 0 ? h->H : h->W);
+            V* tmp = as<V>(li == 0 ? h->u : h->v);
+            const int64_t rows = li == 0 ? m : n, cols = li == 0 ? n : m;
+            for (int32_t t = 0; t < h->k; ++t) {
+                V* ot = other + (int64_t)t * cols;
+                const V* op = t > 0 ? other + (int64_t)(t - 1) * cols : nullptr;
+                // R-hat = R + own_t other_t (minus the pending feature t - 1), own_t from
+                // eq. 5 / eq. 8 into tmp; a tiled copy's combine also writes own_t per segment.
+                RCK(pass<V>(h, li, t > 0 ? kModeSubAdd : kModeAdd, ot, t, t - 1, ot, op, tmp, t,
+                            t > 0 ? 2 : 1));
+                Timed tm(h, CCDPP_K_COMMIT, li, 2.0 * sizeof(V) * rows);
+                HIPCK(h, launch_copy<V>(tmp, own + (int64_t)t * rows, rows, h->stream));
+                tm.done();
+            }
+            // The pending update of feature k - 1, and for the item-major copy the
+            // training sum of squares.
+            RCK(pass<V>(h, li, kModeFlush, nullptr, -1, h->k - 1, nullptr,
+                        other + (int64_t)(h->k - 1) * cols, nullptr, -1, 1));
+            if (li == 1)
+                HIPCK(h, launch_reduce_sum(h->sse_part, h->L[1].grid * kWaves, h->d_scalar, h->stream));
+            if (li == 0)
+                HIPCK(h, (launch_copy_mapped<V, V>(as<V>(h->L[0].val), h->pos0, as<V>(h->L[1].val),
+                                                   h->map01, h->nnz, h->stream)));
+            else
+                HIPCK(h, (launch_copy_mapped<V, V>(as<V>(h->L[1].val), h->map01, as<V>(h->L[0].val),
+                                                   h->pos0, h->nnz, h->stream)));
+        }
+    }
+    if (outer > 0) {
+        double sse = 0.0;
+        HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
+        HIPCK(h, hipStreamSynchronize(h->stream));
+        h->train_sse = h->L[1].grid ? sse : 0.0;
+        h->train_sse_valid = true;
+    }
+    HIPCK(h, hipStreamSynchronize(h->stream));
+    if (h->prof) collect_profile(h);
+    return CCDPP_OK;
+}
+
 template <class V>
 int run_impl(ccdpp* h, int32_t outer, int32_t inner) {
     using namespace ccdk;
@@ -1023,6 +1079,13 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
     if (outer < 0 || inner < 1)
         return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0 and inner_iters >= 1");
     return h->dbl ? run_impl<double>(h, outer, inner) : run_impl<float>(h, outer, inner);
+}
+
+int ccdpp_ccd_run(ccdpp_t* h, int32_t outer) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (outer < 0) return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0");
+    if (h->pending >= 0) return fail(h, CCDPP_ESTATE, "internal: a subtract is pending");
+    return h->dbl ? ccd_impl<double>(h, outer) : ccd_impl<float>(h, outer);
 }
 
 int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol,

@@ -70,6 +70,7 @@ def test_null_pointers_and_handles():
     assert rc == C.CCDPP_EINVAL
     # every call on a NULL handle answers ESTATE; destroy accepts NULL
     assert L.ccdpp_run(None, 1, 1) == C.CCDPP_ESTATE
+    assert L.ccdpp_ccd_run(None, 1) == C.CCDPP_ESTATE
     done = ctypes.c_int32()
     assert L.ccdpp_run_until(None, 1, 1, 0.0, 0, None, None, None, None,
                              ctypes.byref(done)) == C.CCDPP_ESTATE
