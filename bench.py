@@ -119,6 +119,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--event-every", type=int, default=4,
+                    help="bracket every n-th launch of the dominant kernel with HIP events")
     ap.add_argument("--algorithm", default="ccdpp", choices=["ccdpp", "ccd"],
                     help="ccdpp: Algorithm 3 (the headline); ccd: element-wise CCD, Algorithm 2")
     ap.add_argument("--precision", default="f32", choices=["f32", "f64"],
@@ -218,6 +220,7 @@ def main():
         g.profile(True)
         if dom:
             g.profile_only(per_layout[dom]["kind"], per_layout[dom]["layout"])
+            g.profile_every(args.event_every)
     ms = timed(args.steps)
     if prof:
         if dom:
@@ -231,6 +234,7 @@ def main():
             dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"])
             live = per_layout[dom]
         g.profile_only(-1, -1)
+        g.profile_every(1)
         g.profile(False)
     ms_plain = timed(max(2, args.steps // 2)) if prof else ms
     # Nonzero visits per step: CCD++ visits every entry 2 * inner times per feature;

@@ -206,6 +206,10 @@ int ccdpp_profile(ccdpp_t *h, int32_t enable);
  * copy (0 or 1); -1 for either means all.  Fewer events disturb the stream
  * less.  The selection persists until changed; the default is all. */
 int ccdpp_profile_only(ccdpp_t *h, int32_t kind, int32_t layout);
+/* Time only every `every`-th launch that the selection matches (the first, then
+ * every `every`-th after it); fewer events, less disturbance, the same means.
+ * every >= 1; the default is 1.  Persists until changed. */
+int ccdpp_profile_every(ccdpp_t *h, int32_t every);
 int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launches,
                        double *total_ms, double *algo_bytes);
 

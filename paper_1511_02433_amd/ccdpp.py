@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
             "ccdpp_set_stream": ([P, P], ctypes.c_int),
             "ccdpp_profile": ([P, i32], ctypes.c_int),
             "ccdpp_profile_only": ([P, i32, i32], ctypes.c_int),
+            "ccdpp_profile_every": ([P, i32], ctypes.c_int),
             "ccdpp_profile_read": ([P, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(dbl),
                                     ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_info": ([P, ctypes.POINTER(i64), i32], ctypes.c_int),
@@ -234,6 +235,10 @@ def ccdpp_profile_only(h, kind=-1, layout=-1):
     _check(h, lib().ccdpp_profile_only(h, int(kind), int(layout)))
 
 
+def ccdpp_profile_every(h, every):
+    _check(h, lib().ccdpp_profile_every(h, int(every)))
+
+
 def ccdpp_profile_read(h, kind, layout=-1):
     n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
     _check(h, lib().ccdpp_profile_read(h, int(kind), int(layout), ctypes.byref(n),
@@ -337,6 +342,9 @@ class CCDPP:
 
     def profile_only(self, kind=-1, layout=-1):
         ccdpp_profile_only(self._h, kind, layout)
+
+    def profile_every(self, every):
+        ccdpp_profile_every(self._h, every)
 
     def profile_read(self, kind, layout=-1):
         return ccdpp_profile_read(self._h, kind, layout)

@@ -78,6 +78,8 @@ struct ccdpp {
     // kernel timing
     bool prof = false;
     int32_t prof_kind = -1, prof_layout = -1;  // restrict timing to one kind / copy (-1: all)
+    int32_t prof_every = 1;        // time every n-th launch that the selection matches
+    int64_t prof_seen = 0;         // matching launches since the selection was set
     std::vector<ProfEvent> prof_pending;
     std::vector<hipEvent_t> event_pool;
     int64_t prof_launch[CCDPP_K_COUNT][2] = {};
@@ -698,7 +700,8 @@ struct Timed {
     Timed(ccdpp* h_, int kind_, int layout_, double bytes_)
         : h(h_), kind(kind_), layout(layout_), bytes(bytes_) {
         if (h->prof && (h->prof_kind < 0 || h->prof_kind == kind) &&
-            (h->prof_layout < 0 || h->prof_layout == layout)) {
+            (h->prof_layout < 0 || h->prof_layout == layout) &&
+            h->prof_seen++ % h->prof_every == 0) {
             a = take_event(h);
             if (a) (void)hipEventRecord(a, h->stream);
         }
@@ -1266,6 +1269,15 @@ int ccdpp_profile_only(ccdpp_t* h, int32_t kind, int32_t layout) {
     if (layout < -1 || layout > 1) return fail(h, CCDPP_EINVAL, "bad layout");
     h->prof_kind = kind;
     h->prof_layout = layout;
+    h->prof_seen = 0;
+    return CCDPP_OK;
+}
+
+int ccdpp_profile_every(ccdpp_t* h, int32_t every) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (every < 1) return fail(h, CCDPP_EINVAL, "every must be >= 1");
+    h->prof_every = every;
+    h->prof_seen = 0;
     return CCDPP_OK;
 }
 

@@ -80,6 +80,7 @@ def test_null_pointers_and_handles():
     assert L.ccdpp_check_consistency(None, None) == C.CCDPP_ESTATE
     assert L.ccdpp_profile(None, 1) == C.CCDPP_ESTATE
     assert L.ccdpp_profile_only(None, 0, 0) == C.CCDPP_ESTATE
+    assert L.ccdpp_profile_every(None, 4) == C.CCDPP_ESTATE
     buf = (ctypes.c_int64 * 4)()
     assert L.ccdpp_info(None, buf, 4) == C.CCDPP_ESTATE
     L.ccdpp_destroy(None)
