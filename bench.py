@@ -41,8 +41,9 @@ def kernel_symbol(kind: int, info: dict, layout: int) -> str:
     if kind == 3:
         return f"void ccdk::ccd_copy<{v}>({v} const*, {v}*, long)"
     pre = "u" if layout == 0 else "v"
-    staged = info[f"{pre}_gather"] == 2
-    idx16 = staged or info[f"{pre}_tile_width"] < 32768
+    gather = info[f"{pre}_gather"]
+    staged = gather in (2, 3)  # tiled, or hot (leading columns staged)
+    idx16 = gather == 2 or (gather == 1 and info[f"{pre}_tile_width"] < 32768)
     p1 = info[f"{pre}_tiles"] == 1
     name = KERNEL_NAMES[kind]
     b = lambda x: "true" if x else "false"

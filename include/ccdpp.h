@@ -84,11 +84,19 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  * eq. 16.
  *   gather_mode : 0 automatic; 1 gather the other side's coordinates from
  *                 global memory; 2 stage them in LDS, cut into tiles of
- *                 tile_width columns when they do not fit
+ *                 tile_width columns when they do not fit; 3 (hot) stage
+ *                 the leading tile_width columns, the most frequent ones,
+ *                 and gather the others from global memory (automatic
+ *                 mode takes it when tiles would hold too few entries per
+ *                 row)
  *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
- *                 163840 / (4 * v) - 64, rounded down to a multiple of 64,
- *                 where v = 2 for index 0 and 3 for index 1 (the vectors the
- *                 first pass of a feature stages)
+ *                 163840 / (b * v) - 64, rounded down to a multiple of 64,
+ *                 where b is the bytes per value (4, or 8 with precision 1)
+ *                 and v = 2 for index 0 and 3 for index 1 (the vectors the
+ *                 first pass of a feature stages).  With gather_mode 3, the
+ *                 hot width: a multiple of 32, at most 163840 / b - 64
+ *                 rounded down to a multiple of 64 (0: that maximum); each
+ *                 pass stages as much of it as its vectors leave room for
  *   workgroups  : persistent workgroups per pass (0: two per compute unit)
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 4;
@@ -215,8 +223,8 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
 
 /* Sizes and schedule of the handle: fills up to `len` int64 values of
  *   [0] m, [1] n, [2] nnz, [3] k, [4] device build time in microseconds,
- *   [5] user-major copy gather mode (1 global memory, 2 LDS-staged),
- *   [6] its number of tiles P, [7] tile width T, [8] persistent workgroups per
+ *   [5] user-major copy gather mode (1 global memory, 2 LDS-staged, 3 hot),
+ *   [6] its number of tiles P, [7] tile width T (hot: the hot width), [8] persistent workgroups per
  *   pass, [9] row segments, [10..14] the same five for the item-major copy,
  *   [15] device bytes held, [16] bytes per value (4: float, 8: double).
  * Returns the number of values written. */

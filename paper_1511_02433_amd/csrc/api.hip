@@ -218,25 +218,31 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // is the zero the padding entries read.
     const int64_t vbytes = h->dbl ? 8 : 4;
     const int64_t tmax = ((int64_t)kLdsVecBytes / (vbytes * nvec) - 64) / 64 * 64;
+    const int64_t hmax = ((int64_t)kLdsVecBytes / vbytes - 64) / 64 * 64;  // one vector
     const int forced = opt ? opt->gather_mode[side] : 0;
     const int64_t forced_T = opt ? opt->tile_width[side] : 0;
-    if (forced_T > tmax)
+    if (forced == kGatherHot) {
+        if (forced_T > hmax || forced_T % 32 != 0)
+            return fail(h, CCDPP_EINVAL, "hot tile_width must be a multiple of 32, at most %lld",
+                        (long long)hmax);
+    } else if (forced_T > tmax) {
         return fail(h, CCDPP_EINVAL, "tile_width must be at most %lld", (long long)tmax);
+    }
 
     // Tile width: whole vector if it fits, else balanced tiles of at most tmax.
     int64_t T = cols, P = 1;
-    bool lds = forced != kGatherGlobal;
-    if (forced_T > 0) {
+    int mode = forced == kGatherGlobal || forced == kGatherHot ? forced : kGatherLds;
+    if (forced_T > 0 && mode == kGatherLds) {
         T = forced_T;
     } else if (cols > tmax) {
         P = (cols + tmax - 1) / tmax;
         T = ((cols + P - 1) / P + 63) / 64 * 64;
     }
-    if (!lds) T = cols;
+    if (mode != kGatherLds) T = cols;
     P = (cols + T - 1) / T;
     if ((uint64_t)P * (uint64_t)rows > (uint64_t)INT32_MAX) {
         if (forced == kGatherLds) return fail(h, CCDPP_EINVAL, "too many (tile, row) pairs");
-        lds = false;
+        mode = kGatherHot;
         T = cols;
         P = 1;
     }
@@ -254,22 +260,36 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
                                 s));
         HIPCK(h, hipStreamSynchronize(s));
         if (P == 1 || forced == kGatherLds) break;
-        // Tiling pays only when segments are long enough; otherwise gather through L2.
+        // Tiling pays only when segments are long enough; otherwise stage the leading
+        // columns and gather the others through L2.
         int64_t nonempty = 0;
         for (int32_t c : cnt) nonempty += c > 0;
         if (nonempty > 0 && N / nonempty >= kMinTiledSeg) break;
-        lds = false;
+        mode = kGatherHot;
         T = cols;
         P = 1;
     }
-    L.gather = lds ? kGatherLds : kGatherGlobal;
+    // A hot layout stages whole groups of 32 leading columns; with fewer columns than
+    // that it gathers everything from global memory.
+    if (mode == kGatherHot && cols < 32) mode = kGatherGlobal;
+    const bool lds = mode == kGatherLds;
+    L.gather = mode;
     L.T = (int32_t)T;
     L.P = (int32_t)P;
-    L.swz = lds;
     L.pad = lds ? (int32_t)((T + 31) / 32 * 32) : (int32_t)T;
     L.Ts = lds ? L.pad + 32 : (int32_t)T + 1;
-    // Every index, the padding one included, fits 15 bits (the 16th is the start bit).
-    L.idx16 = L.pad < (int32_t)IndexBits<uint16_t>::start;
+    if (mode == kGatherHot) {
+        // Hot width: the widest one-vector slice, never past the last whole group of
+        // 32 columns (so the padding index cols stays outside the swizzled range).
+        L.hot = (int32_t)std::min<int64_t>(forced_T > 0 ? forced_T : hmax, cols / 32 * 32);
+        L.swz_lim = (uint32_t)L.hot;
+    } else {
+        L.hot = 0;
+        L.swz_lim = lds ? 0xFFFFFFFFu : 0u;
+    }
+    // Every index, the padding one included, fits 15 bits (the 16th is the start bit);
+    // hot layouts always take 32-bit indices.
+    L.idx16 = mode != kGatherHot && L.pad < (int32_t)IndexBits<uint16_t>::start;
 
     // Segments.  P == 1: segment r is row r (rows are relabelled by decreasing
     // length, so the empty ones come last).  P > 1: the non-empty rows of each
@@ -519,7 +539,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         }
         RCK(with_value_type(h, [&](auto z) -> int {
             using V = decltype(z);
-            HIPCK(h, launch_layout_fill<V>(k1, perm, val_in, N, cbits, d_off, L.swz, L.idx16, L.idx,
+            HIPCK(h, launch_layout_fill<V>(k1, perm, val_in, N, cbits, d_off, L.swz_lim, L.idx16, L.idx,
                                            as<V>(L.val), epos, s));
             return CCDPP_OK;
         }));
@@ -801,9 +821,11 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
         return fail(nullptr, CCDPP_EINVAL, "row, col and val must be non-NULL when nnz > 0");
     if (opts) {
         for (int i = 0; i < 2; ++i) {
-            if (opts->gather_mode[i] < 0 || opts->gather_mode[i] > 2)
-                return fail(nullptr, CCDPP_EINVAL, "gather_mode must be 0, 1 or 2");
+            if (opts->gather_mode[i] < 0 || opts->gather_mode[i] > 3)
+                return fail(nullptr, CCDPP_EINVAL, "gather_mode must be 0, 1, 2 or 3");
             if (opts->tile_width[i] < 0) return fail(nullptr, CCDPP_EINVAL, "tile_width < 0");
+            if (opts->gather_mode[i] == ccdk::kGatherHot && opts->tile_width[i] % 32 != 0)
+                return fail(nullptr, CCDPP_EINVAL, "a hot tile_width must be a multiple of 32");
         }
         if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
         if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
@@ -1303,10 +1325,13 @@ int ccdpp_profile_read(ccdpp_t* h, int32_t kind, int32_t layout, int64_t* launch
 int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     if (!h) return CCDPP_ESTATE;
     if (!out || len < 0) return fail(h, CCDPP_EINVAL, "bad output buffer");
+    auto width = [](const ccdk::Layout& L) -> int64_t {
+        return L.gather == ccdk::kGatherHot ? L.hot : L.T;
+    };
     const int64_t v[17] = {h->m,         h->n,         h->nnz,       h->k,
-                           h->build_us,  h->L[0].gather, h->L[0].P,  h->L[0].T,
+                           h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
-                           h->L[1].T,    h->L[1].grid, h->L[1].nseg, h->bytes_held,
+                           width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
                            h->dbl ? 8 : 4};
     int32_t w = std::min<int32_t>(len, 17);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];

@@ -71,7 +71,7 @@ __global__ void k_dup_check(const uint64_t* __restrict__ keys, int64_t nnz, int3
 template <class I, class V>
 __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* __restrict__ perm,
                               const float* __restrict__ val_in, int64_t nnz, int cbits,
-                              uint64_t mask, const int32_t* __restrict__ seg_off, bool swz,
+                              uint64_t mask, const int32_t* __restrict__ seg_off, uint32_t swz_lim,
                               I* __restrict__ idx, V* __restrict__ val,
                               int32_t* __restrict__ pos) {
     for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < nnz;
@@ -80,7 +80,7 @@ __global__ void k_layout_fill(const uint64_t* __restrict__ keys, const int32_t* 
         const int64_t p = q + seg_off[key >> cbits];
         const uint32_t c = (uint32_t)(key & mask);
         const bool first = q == 0 || (keys[q - 1] >> cbits) != (key >> cbits);
-        idx[p] = (I)((swz ? lds_swizzle(c) : c) | (first ? IndexBits<I>::start : 0u));
+        idx[p] = (I)((c < swz_lim ? lds_swizzle(c) : c) | (first ? IndexBits<I>::start : 0u));
         const int64_t f = val_slot<V>(p);
         val[f] = (V)val_in[perm[q]];
         pos[q] = (int32_t)f;
@@ -143,7 +143,7 @@ __global__ void k_factor_out(const V* __restrict__ colmajor, const int32_t* __re
 template <class I, class V>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
-                          int32_t P, int32_t T, bool swz, const I* __restrict__ idx,
+                          int32_t P, int32_t T, uint32_t swz_lim, const I* __restrict__ idx,
                           const int32_t* __restrict__ pos, const V* __restrict__ A,
                           const V* __restrict__ W, const V* __restrict__ H, int64_t m,
                           int64_t n, int32_t k, int64_t nnz, V* __restrict__ val) {
@@ -163,7 +163,7 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
         }
         const int64_t i = seg_row[lo];
         const uint32_t c = (uint32_t)idx[q] & IndexBits<I>::mask;
-        const int64_t j = (int64_t)plo * T + (int64_t)(swz ? lds_swizzle(c) : c);
+        const int64_t j = (int64_t)plo * T + (int64_t)(c < swz_lim ? lds_swizzle(c) : c);
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
@@ -286,17 +286,17 @@ hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hi
 
 template <class V>
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
+                              int64_t nnz, int cbits, const int32_t* seg_off, uint32_t swz_lim, bool idx16,
                               void* idx, V* val, int32_t* pos, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
     const uint64_t mask = cbits >= 64 ? ~0ull : ((1ull << cbits) - 1);
     if (idx16)
         hipLaunchKernelGGL((k_layout_fill<uint16_t, V>), grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, cbits, mask, seg_off, swz, static_cast<uint16_t*>(idx), val,
+                           val_in, nnz, cbits, mask, seg_off, swz_lim, static_cast<uint16_t*>(idx), val,
                            pos);
     else
         hipLaunchKernelGGL((k_layout_fill<int32_t, V>), grid_for(nnz), dim3(kT), 0, s, keys, perm,
-                           val_in, nnz, cbits, mask, seg_off, swz, static_cast<int32_t*>(idx), val,
+                           val_in, nnz, cbits, mask, seg_off, swz_lim, static_cast<int32_t*>(idx), val,
                            pos);
     return hipGetLastError();
 }
@@ -354,12 +354,12 @@ hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const V*
     if (L.nnz == 0) return hipSuccess;
     if (L.idx16)
         hipLaunchKernelGGL((k_rebuild<uint16_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
-                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz_lim,
                            static_cast<const uint16_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
                            static_cast<V*>(L.val));
     else
         hipLaunchKernelGGL((k_rebuild<int32_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
-                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz,
+                           L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz_lim,
                            static_cast<const int32_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
                            static_cast<V*>(L.val));
     return hipGetLastError();
@@ -408,7 +408,7 @@ hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* 
 
 #define CCDK_BUILD_INSTANTIATE(V)                                                               \
     template hipError_t launch_layout_fill<V>(const uint64_t*, const int32_t*, const float*,    \
-                                              int64_t, int, const int32_t*, bool, bool, void*,  \
+                                              int64_t, int, const int32_t*, uint32_t, bool, void*, \
                                               V*, int32_t*, hipStream_t);                       \
     template hipError_t launch_fill<V>(V*, V, int64_t, hipStream_t);                            \
     template hipError_t launch_scatter_factor_in<float, V>(const float*, const int32_t*,        \

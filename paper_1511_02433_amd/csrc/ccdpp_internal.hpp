@@ -65,6 +65,14 @@ namespace ccdk {
 // multiple of 32 at or above T, a word outside the swizzled range that staging
 // sets to zero.
 //
+// A hot layout (P == 1, 32-bit indices) is for a gathered side too long to stage
+// and too sparse to tile: its columns are relabelled by decreasing count, so the
+// first ones take most of the gathers.  Each pass stages as many leading columns
+// as its vectors leave room for (a multiple of 32, at most the layout's hot
+// width tsw) and gathers the others from global memory.  Indices below tsw are
+// swizzled positions, the rest plain columns; the padding index is cols, which
+// the bounded global load turns into 0.
+//
 // The per-row scalars a pass reads (the own factor column of the current and
 // the previous feature) are addressed by segment: with P == 1 segment s is row
 // s and the factor column itself serves; with P > 1 the library keeps a copy of
@@ -132,6 +140,7 @@ enum GatherMode : int32_t {
     kGatherAuto = 0,
     kGatherGlobal = 1,  // P == 1, gathers from global memory
     kGatherLds = 2,     // vectors staged in LDS (tiled when they do not fit)
+    kGatherHot = 3,     // P == 1, the leading columns staged in LDS, the rest from global
 };
 
 // V is the type of the residual, the factors and the in-window arithmetic:
@@ -154,7 +163,8 @@ struct PassArgs {
     double2* part;              // [S + 2 * chunks] partials: per segment (P > 1), then the
                                 // head and tail slot of every chunk
     double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
-    int32_t rows, cols, T, P;
+    int32_t rows, cols, T, P;   // hot layouts: T is the pass's staged width
+    int32_t tsw;                // hot layouts: indices below tsw are swizzled positions
     int32_t Ts;                 // LDS elements per staged vector slice
     int32_t pad;                // index held by padding entries (reads 0)
     int32_t nseg;               // S
@@ -187,8 +197,10 @@ struct Layout {
     int32_t gather = kGatherGlobal;
     int32_t T = 0, P = 1;
     int32_t Ts = 0;                  // LDS elements per staged slice (swizzled range + zero)
-    int32_t pad = 0;                 // padding index: the zero word (staged) or cols (global)
-    bool swz = false;                // indices are swizzled LDS positions (staged layouts)
+    int32_t pad = 0;                 // padding index: the zero word (staged) or cols (global, hot)
+    int32_t hot = 0;                 // hot layouts: the hot width tsw
+    uint32_t swz_lim = 0;            // indices below it are swizzled LDS positions: all of
+                                     // them (tiled), the hot width (hot), none (global)
     bool idx16 = false;
     void* idx = nullptr;             // [npad + kEntryPad]
     void* val = nullptr;             // [npad + kEntryPad] of the handle's value type
@@ -240,7 +252,7 @@ hipError_t launch_seg_keys(const int32_t* lrow, const int32_t* lcol, const int32
 hipError_t launch_dup_check(const uint64_t* keys, int64_t nnz, int32_t* flag, hipStream_t s);
 template <class V>
 hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const float* val_in,
-                              int64_t nnz, int cbits, const int32_t* seg_off, bool swz, bool idx16,
+                              int64_t nnz, int cbits, const int32_t* seg_off, uint32_t swz_lim, bool idx16,
                               void* idx, V* val, int32_t* pos, hipStream_t s);
 hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);

@@ -15,8 +15,14 @@
 // (each entry is touched once per pass), the next window's loads in flight
 // while the current window is reduced.  The vectors a pass gathers from are
 // staged tile by tile in LDS by persistent workgroups (see ccdpp_internal.hpp),
-// so a random gather costs an LDS read; layouts too sparse for tiling gather
-// through L2 with bounded buffer loads instead.
+// so a random gather costs an LDS read; layouts too sparse for tiling stage
+// only their leading (most frequent) columns and gather the others through L2
+// with bounded buffer loads, issued before the next windows' data so that
+// waiting for them does not wait for that data too.
+//
+// Kernel variants: STAGED with 16-bit indices is a tiled layout, STAGED with
+// 32-bit indices a hot layout (P == 1, the leading columns staged), !STAGED a
+// layout that gathers everything from global memory.
 //
 // Arithmetic: R-hat in fp32 FMA.  Inside a window (at most 512 entries) the
 // sums of R-hat*x and x^2 are fp32 segmented scans; a segment's window sums are
@@ -24,6 +30,7 @@
 // identical run to run.  The coordinate num / (lambda + den) is an IEEE fp64
 // division rounded once to fp32; a coordinate whose denominator is exactly zero
 // (lambda = 0 and an empty row) is set to zero.
+#include <algorithm>
 #include <type_traits>
 
 #include "ccdpp_internal.hpp"
@@ -216,13 +223,14 @@ struct Gather {
     const V* lq;
     const V* lqq;
     rsrc_t gx, gq, gqq;
+    uint32_t th;   // hot layouts: indices below th are staged
+    uint32_t tsw;  // hot layouts: indices below tsw are swizzled positions
+    uint32_t gpad; // a column past the vectors (reads 0)
 };
 
-template <bool STAGED, class V>
-__device__ __forceinline__ V gat(const V* lds, rsrc_t g, uint32_t c) {
-    if constexpr (STAGED)
-        return lds[c];
-    else if constexpr (sizeof(V) == 4)
+template <class V>
+__device__ __forceinline__ V gload(rsrc_t g, uint32_t c) {
+    if constexpr (sizeof(V) == 4)
         return ld_f32(g, c * 4u);
     else
         return ld_f64(g, c * 8u);
@@ -240,8 +248,9 @@ __device__ __forceinline__ V rhat(V v, V qv, V qqv, V pr, V ppr) {
 
 // Copy the tile's slice of every gathered vector into LDS at the swizzled
 // positions, with a zero at the padding index.  Slots come in the order x, q,
-// qq; x shares q's slot when they are the same vector.
-template <int MODE, class V>
+// qq; x shares q's slot when they are the same vector.  A hot layout stages its
+// leading T columns as tile 0.
+template <int MODE, bool HOT, class V>
 __device__ __forceinline__ void stage_tile(const PassArgs<V>& a, int tile, V* lds, Gather<V>& gx) {
     using N = Needs<MODE>;
     const int T = a.T, Ts = a.Ts;
@@ -280,7 +289,7 @@ __device__ __forceinline__ void stage_tile(const PassArgs<V>& a, int tile, V* ld
             }
         }
     }
-    if (threadIdx.x == 0) {
+    if (!HOT && threadIdx.x == 0) {  // hot layouts pad with a global column
         if (N::x && !alias) sx[a.pad] = V(0);
         if (N::q) sq[a.pad] = V(0);
         if (N::qq) sqq[a.pad] = V(0);
@@ -412,8 +421,28 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
                                        const Win<V>& cur, Win<V>& nxt, Win<V>& nn, int lane,
                                        uint32_t le) {
     using N = Needs<MODE>;
+    constexpr bool HOT = STAGED && !IDX16;
+    constexpr bool GLOBAL = !STAGED || HOT;  // some gathers read global memory
+    // Float gathers are issued before the loads of the window after next; double
+    // ones after them, inside the entry loop, where the registers allow.
+    constexpr bool EARLY = GLOBAL && sizeof(V) == 4;
     const int64_t b = wk.elo;
     const int64_t we = min(b + (int64_t)kWin, wk.c1);
+    // Gathers from global memory: in a hot layout, the entries past the staged
+    // columns (the others read the padding column, which costs no memory access).
+    V gq[kE], gqq[kE], gxx[kE];
+    auto fetch = [&](int k, uint32_t c) {
+        uint32_t g = c;
+        if constexpr (HOT) g = c < gx.th ? gx.gpad : (c < gx.tsw ? lds_swizzle(c) : c);
+        if constexpr (N::q) gq[k] = gload<V>(gx.gq, g);
+        if constexpr (N::qq) gqq[k] = gload<V>(gx.gqq, g);
+        if constexpr (N::x && !XQ) gxx[k] = gload<V>(gx.gx, g);
+    };
+    if constexpr (EARLY) {
+#pragma unroll
+        for (int k = 0; k < kE; ++k) fetch(k, col_of<IDX16, V>(cur, k));
+        __builtin_amdgcn_sched_barrier(0);
+    }
     // Data of the window after next, before anything waits on this one (a harmless
     // reload of b past the chunk's end).
     {
@@ -451,11 +480,27 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
 #pragma unroll
     for (int k = 0; k < kE; ++k) {
         const uint32_t c = col_of<IDX16, V>(cur, k);
-        const V qv = N::q ? gat<STAGED, V>(gx.lq, gx.gq, c) : V(0);
-        const V qqv = N::qq ? gat<STAGED, V>(gx.lqq, gx.gqq, c) : V(0);
+        if constexpr (GLOBAL && !EARLY) fetch(k, c);
+        V qv = V(0), qqv = V(0), xg = V(0);
+        if constexpr (!STAGED) {
+            if constexpr (N::q) qv = gq[k];
+            if constexpr (N::qq) qqv = gqq[k];
+            if constexpr (N::x && !XQ) xg = gxx[k];
+        } else {
+            const bool hot = !HOT || c < gx.th;
+            const uint32_t lc = hot ? c : 0u;
+            if constexpr (N::q) qv = gx.lq[lc];
+            if constexpr (N::qq) qqv = gx.lqq[lc];
+            if constexpr (N::x && !XQ) xg = gx.lx[lc];
+            if constexpr (HOT) {
+                if constexpr (N::q) qv = hot ? qv : gq[k];
+                if constexpr (N::qq) qqv = hot ? qqv : gqq[k];
+                if constexpr (N::x && !XQ) xg = hot ? xg : gxx[k];
+            }
+        }
         r[k] = rhat<MODE, V>(val_of<V>(cur, k), qv, qqv, pr, ppr);
         if constexpr (N::x) {
-            const V xv = XQ ? qv : gat<STAGED, V>(gx.lx, gx.gx, c);
+            const V xv = XQ ? qv : xg;
             an = fmav(r[k], xv, an);
             ad = fmav(xv, xv, ad);
         }
@@ -574,12 +619,16 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     V* lds = reinterpret_cast<V*>(lds_raw);
     const int wg = blockIdx.x;
 
+    constexpr bool HOT = STAGED && !IDX16;
     Gather<V> gx{};
-    if constexpr (!STAGED) {
+    if constexpr (!STAGED || HOT) {
         const uint64_t vb = (uint64_t)a.cols * sizeof(V);
         if (N::x) gx.gx = make_rsrc(a.x, vb);
         if (N::q) gx.gq = make_rsrc(a.q, vb);
         if (N::qq) gx.gqq = make_rsrc(a.qq, vb);
+        gx.th = (uint32_t)a.T;
+        gx.tsw = (uint32_t)a.tsw;
+        gx.gpad = (uint32_t)a.cols;
     }
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = (int)(threadIdx.x & 63u);
@@ -605,7 +654,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
             const int tile = a.piece_tile[pc];
             if (tile != staged) {
                 if (staged >= 0) __syncthreads();  // every wave is done with the old slice
-                stage_tile<MODE, V>(a, tile, lds, gx);
+                stage_tile<MODE, HOT, V>(a, tile, lds, gx);
                 __syncthreads();
                 staged = tile;
             }
@@ -750,6 +799,7 @@ template <class V>
 hipError_t raise_lds_all() {
     hipError_t e = raise_lds<true, true, true, V>();
     if (e == hipSuccess) e = raise_lds<true, true, false, V>();
+    if (e == hipSuccess) e = raise_lds<true, false, true, V>();
     if (e == hipSuccess) e = raise_lds<false, true, true, V>();
     if (e == hipSuccess) e = raise_lds<false, false, true, V>();
     return e;
@@ -768,8 +818,11 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
                        hipStream_t s) {
     if (L.grid == 0) return hipSuccess;
     const bool staged = L.gather == kGatherLds;
-    // Kernel variants: LDS staging uses 16-bit indices; global gathers have P == 1.
+    const bool hot = L.gather == kGatherHot;
+    // Kernel variants: tiles use 16-bit indices, hot layouts 32-bit ones; global
+    // gathers and hot layouts have P == 1.
     if (staged ? !L.idx16 : L.P != 1) return hipErrorInvalidValue;
+    if (hot && L.idx16) return hipErrorInvalidValue;
     PassArgs<V> a{};
     a.idx = L.idx;
     a.val = static_cast<V*>(L.val);
@@ -796,7 +849,17 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     a.nseg_ne = (int32_t)L.nseg_ne;
     a.x_is_q = (x != nullptr && x == q) ? 1 : 0;
     a.lambda = lambda;
-    a.vec_elems = staged ? staged_vectors(mode, a.x_is_q) * a.Ts : 0;
+    const int nv = staged_vectors(mode, a.x_is_q);
+    a.tsw = 0;
+    a.vec_elems = staged ? nv * a.Ts : 0;
+    if (hot) {
+        // As many leading columns as the pass's vectors leave room for.
+        const int64_t fit = ((int64_t)kLdsVecBytes / ((int64_t)sizeof(V) * nv) - 64) / 64 * 64;
+        a.T = (int32_t)std::min<int64_t>(L.hot, fit);
+        a.Ts = a.T;
+        a.tsw = L.hot;
+        a.vec_elems = nv * a.Ts;
+    }
     const size_t lds = (size_t)a.vec_elems * sizeof(V);
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     const dim3 grid(L.grid);
@@ -805,6 +868,8 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
             launch_mode<true, true, true, V>(mode, grid, lds, s, a);
         else
             launch_mode<true, true, false, V>(mode, grid, lds, s, a);
+    } else if (hot) {
+        launch_mode<true, false, true, V>(mode, grid, lds, s, a);
     } else if (L.idx16) {
         launch_mode<false, true, true, V>(mode, grid, lds, s, a);
     } else {

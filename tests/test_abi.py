@@ -51,11 +51,19 @@ def test_create_rejects_bad_arguments_on_the_host(kw, msg):
     assert msg in str(ei.value)
 
 
-def test_create_rejects_bad_options():
+@pytest.mark.parametrize("kw, msg", [
+    (dict(gather_mode=(7, 0)), "gather_mode"),
+    (dict(gather_mode=(0, 4)), "gather_mode"),
+    (dict(gather_mode=(3, 0), tile_width=(100, 0)), "multiple of 32"),
+    (dict(tile_width=(0, -1)), "tile_width"),
+    (dict(precision=2), "precision"),
+])
+def test_create_rejects_bad_options(kw, msg):
     _lib_or_skip()
     with pytest.raises(C.CCDPPError) as ei:
-        _create(opts=C.make_options(gather_mode=(7, 0)))
+        _create(opts=C.make_options(**kw))
     assert ei.value.code == C.CCDPP_EINVAL
+    assert msg in str(ei.value)
 
 
 def test_null_pointers_and_handles():

@@ -74,6 +74,7 @@ LAYOUTS = {
     "global": dict(gather_mode=(1, 1)),
     "tiled": dict(gather_mode=(2, 2), tile_width=(192, 128)),
     "tiled_odd": dict(gather_mode=(2, 2), tile_width=(100, 333), workgroups=3),
+    "hot": dict(gather_mode=(3, 3), tile_width=(64, 96)),
 }
 
 

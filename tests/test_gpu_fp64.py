@@ -88,6 +88,7 @@ LAYOUTS = {
     "global": dict(gather_mode=(1, 1)),
     "tiled": dict(gather_mode=(2, 2), tile_width=(192, 128)),
     "tiled_odd": dict(gather_mode=(2, 2), tile_width=(100, 333), workgroups=3),
+    "hot": dict(gather_mode=(3, 3), tile_width=(64, 96)),
 }
 
 
@@ -114,7 +115,7 @@ def test_short_segments_and_32bit_indices(transpose):
         row, col = col, row
         m, n = n, m
         H0 = (np.random.default_rng(53).standard_normal((n, 3)) * 0.1).astype(np.float32)
-    for opts in (_opts(), _opts(gather_mode=(1, 1))):
+    for opts in (_opts(), _opts(gather_mode=(1, 1)), _opts(gather_mode=(3, 3), tile_width=(4096, 4096))):
         g, o = _pair(m, n, 3, 0.1, row, col, val, H0, opts=opts)
         g.run(1, 2)
         o.run(1, 2)

@@ -171,6 +171,12 @@ LAYOUTS = {
     "tiled": dict(gather_mode=(2, 2), tile_width=(192, 128)),
     "tiled_odd": dict(gather_mode=(2, 2), tile_width=(100, 333), workgroups=3),
     "mixed": dict(gather_mode=(1, 2), tile_width=(0, 64), workgroups=1),
+    # Hot layouts: a few leading columns staged, the rest gathered from global memory
+    # (widths 64 and 96 of 900 and 1500), and the widest hot width, which stages all
+    # but the last partial group of 32 columns.
+    "hot": dict(gather_mode=(3, 3), tile_width=(64, 96)),
+    "hot_wide": dict(gather_mode=(3, 3), workgroups=3),
+    "hot_mixed": dict(gather_mode=(2, 3), tile_width=(128, 32), workgroups=1),
 }
 
 
@@ -203,14 +209,20 @@ def test_layout_strategies_match_oracle(name):
         assert info["u_tiles"] > 1 and info["v_tiles"] > 1
     if name == "global":
         assert info["u_gather"] == 1 and info["v_gather"] == 1
+    if name.startswith("hot"):
+        assert info["v_gather"] == 3
 
 
-@pytest.mark.parametrize("layout", ["auto", "global"])
+@pytest.mark.parametrize("layout", ["auto", "global", "hot"])
 @pytest.mark.parametrize("transpose", [False, True])
 def test_short_segments_fill_windows(layout, transpose):
     # Rows of 1..8 entries: every segment fills one lane after alignment padding, so
     # full windows hold 64 segment starts (the last lane's segment lies past the
-    # window's row-scalar slots).  40,000 columns need 32-bit indices in global mode.
+    # window's row-scalar slots).  40,000 columns need 32-bit indices outside tiles.
+    # Tiles of them would hold about one entry per row, so the automatic layout of
+    # that side is hot: the plain passes stage all 40,000 columns, the first passes
+    # (two or three vectors) the leading 20,416 or 13,568, and gather the rest,
+    # swizzled indices included, from global memory.  "hot" stages only 4,096.
     from paper_1511_02433_amd.ccdpp import make_options
     lens = list(np.random.default_rng(51).integers(1, 9, 6000))
     row, col, val, H0 = synth.lengths_problem(lens, 40_000, 3, seed=52)
@@ -221,9 +233,14 @@ def test_short_segments_fill_windows(layout, transpose):
         H0 = (np.random.default_rng(53).standard_normal((n, 3)) * 0.1).astype(np.float32)
     print(f"case: short segments layout={layout} transpose={transpose} nnz={row.size}",
           flush=True)
-    opts = make_options(gather_mode=(1, 1)) if layout == "global" else make_options()
+    opts = {"global": make_options(gather_mode=(1, 1)),
+            "hot": make_options(gather_mode=(3, 3), tile_width=(4096, 4096)),
+            "auto": make_options()}[layout]
     g = CCDPP(m, n, 3, 0.1, row, col, val, opts=opts)
-    print({k: v for k, v in g.info().items() if k.startswith(("u_", "v_"))})
+    info = g.info()
+    print({k: v for k, v in info.items() if k.startswith(("u_", "v_"))})
+    wide = "v" if transpose else "u"  # the side that gathers over 40,000 columns
+    assert info[f"{wide}_gather"] == {"global": 1, "hot": 3, "auto": 3}[layout]
     g.set_factors(np.zeros((m, 3), np.float32), H0)
     o = Oracle(m, n, 3, 0.1, row, col, val, H0)
     g.run(1, 2)
