@@ -474,6 +474,11 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         HIPCK(h, dalloc(h, &L.part, nslots));
         L.nslots = nslots;
     }
+    if (!lds && !h->dbl) {
+        float* pk;
+        HIPCK(h, dalloc(h, &pk, 4 * cols));
+        L.pk = pk;
+    }
     RCK(upload(h, &L.seg_start, seg_start));
     RCK(upload(h, &L.seg_row, seg_row));
     RCK(upload(h, &L.tile_seg, tile_seg));

@@ -159,6 +159,8 @@ struct PassArgs {
     const V* pp;                // [S] own factor column, previous feature (committed), per segment
     const V* q;                 // [cols] other factor column, current feature
     const V* qq;                // [cols] other factor column, previous feature (committed)
+    const V* pk;                // [4 * cols] float hot or global first passes: (x, q, qq, 0)
+                                // of every column, so that a gather reads one 16-byte record
     V* y;                       // [rows] coordinates (P == 1)
     double2* part;              // [S + 2 * chunks] partials: per segment (P > 1), then the
                                 // head and tail slot of every chunk
@@ -221,6 +223,7 @@ struct Layout {
     int32_t* row_seg_ptr = nullptr;  // P > 1: segments of each row in tile order
     int32_t* row_segs = nullptr;
     double2* part = nullptr;         // [nslots]
+    void* pk = nullptr;              // float hot or global layouts: [4 * cols] packed gathers
     int64_t nslots = 0;
     int64_t nseg = 0;
     int64_t nseg_ne = 0;

@@ -61,6 +61,9 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 __device__ __forceinline__ float ld_f32(rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
+__device__ __forceinline__ f32x4 ld_f32x4(rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 // Two 32-bit bounded loads (a 64-bit buffer load is not used, see the toolchain notes).
 __device__ __forceinline__ double ld_f64(rsrc_t r, uint32_t off) {
     int2 v;
@@ -223,6 +226,7 @@ struct Gather {
     const V* lq;
     const V* lqq;
     rsrc_t gx, gq, gqq;
+    rsrc_t gpk;    // packed (x, q, qq, 0) records (float first passes)
     uint32_t th;   // hot layouts: indices below th are staged
     uint32_t tsw;  // hot layouts: indices below tsw are swizzled positions
     uint32_t gpad; // a column past the vectors (reads 0)
@@ -426,6 +430,8 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     // Float gathers are issued before the loads of the window after next; double
     // ones after them, inside the entry loop, where the registers allow.
     constexpr bool EARLY = GLOBAL && sizeof(V) == 4;
+    // A float first pass gathers its two or three vectors as one 16-byte record.
+    constexpr bool PACK = EARLY && N::q && (N::qq || (N::x && !XQ));
     const int64_t b = wk.elo;
     const int64_t we = min(b + (int64_t)kWin, wk.c1);
     // Gathers from global memory: in a hot layout, the entries past the staged
@@ -434,9 +440,16 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     auto fetch = [&](int k, uint32_t c) {
         uint32_t g = c;
         if constexpr (HOT) g = c < gx.th ? gx.gpad : (c < gx.tsw ? lds_swizzle(c) : c);
-        if constexpr (N::q) gq[k] = gload<V>(gx.gq, g);
-        if constexpr (N::qq) gqq[k] = gload<V>(gx.gqq, g);
-        if constexpr (N::x && !XQ) gxx[k] = gload<V>(gx.gx, g);
+        if constexpr (PACK) {
+            const f32x4 w = ld_f32x4(gx.gpk, g * 16u);
+            gxx[k] = w.x;
+            gq[k] = w.y;
+            gqq[k] = w.z;
+        } else {
+            if constexpr (N::q) gq[k] = gload<V>(gx.gq, g);
+            if constexpr (N::qq) gqq[k] = gload<V>(gx.gqq, g);
+            if constexpr (N::x && !XQ) gxx[k] = gload<V>(gx.gx, g);
+        }
     };
     if constexpr (EARLY) {
 #pragma unroll
@@ -626,6 +639,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
         if (N::x) gx.gx = make_rsrc(a.x, vb);
         if (N::q) gx.gq = make_rsrc(a.q, vb);
         if (N::qq) gx.gqq = make_rsrc(a.qq, vb);
+        gx.gpk = make_rsrc(a.pk, a.pk ? (uint64_t)a.cols * 16u : 0u);
         gx.th = (uint32_t)a.T;
         gx.tsw = (uint32_t)a.tsw;
         gx.gpad = (uint32_t)a.cols;
@@ -737,6 +751,22 @@ __global__ __launch_bounds__(256) void ccd_copy(const V* __restrict__ src, V* __
                                                 int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < n) dst[i] = src[i];
+}
+
+// The packed gather records of a float first pass: (x, q, qq, 0) per column,
+// a null vector giving zeros.
+__global__ __launch_bounds__(256) void ccd_pack(const float* __restrict__ x,
+                                                const float* __restrict__ q,
+                                                const float* __restrict__ qq,
+                                                f32x4* __restrict__ pk, int32_t n) {
+    const int32_t i = (int32_t)blockIdx.x * 256 + (int32_t)threadIdx.x;
+    if (i >= n) return;
+    f32x4 w;
+    w.x = x ? x[i] : 0.0f;
+    w.y = q ? q[i] : 0.0f;
+    w.z = qq ? qq[i] : 0.0f;
+    w.w = 0.0f;
+    pk[i] = w;
 }
 
 // Single-workgroup fixed-order sum: thread t sums part[t], part[t+256], ... in
@@ -862,6 +892,16 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     }
     const size_t lds = (size_t)a.vec_elems * sizeof(V);
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
+    if (!staged && sizeof(V) == 4 && nv >= 2) {
+        // Float first passes that gather two or three vectors from global memory read
+        // them as packed records.
+        if (!L.pk) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(ccd_pack, dim3((unsigned)((L.cols + 255) / 256)), dim3(256), 0, s,
+                           reinterpret_cast<const float*>(x), reinterpret_cast<const float*>(q),
+                           reinterpret_cast<const float*>(qq), static_cast<f32x4*>(L.pk),
+                           (int32_t)L.cols);
+        a.pk = static_cast<const V*>(L.pk);
+    }
     const dim3 grid(L.grid);
     if (staged) {
         if (L.P == 1)
