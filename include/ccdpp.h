@@ -226,7 +226,10 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   [5] user-major copy gather mode (1 global memory, 2 LDS-staged, 3 hot),
  *   [6] its number of tiles P, [7] tile width T (hot: the hot width), [8] persistent workgroups per
  *   pass, [9] row segments, [10..14] the same five for the item-major copy,
- *   [15] device bytes held, [16] bytes per value (4: float, 8: double).
+ *   [15] device bytes held, [16] bytes per value (4: float, 8: double),
+ *   [17] user-major rows that the workgroups of a pass finish themselves (cut
+ *   between the waves of one workgroup), [18] rows the combine kernel finishes
+ *   after each pass, [19..20] the same two for the item-major copy.
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

@@ -248,7 +248,8 @@ def ccdpp_profile_read(h, kind, layout=-1):
 
 INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_width",
                "u_workgroups", "u_segments", "v_gather", "v_tiles", "v_tile_width", "v_workgroups",
-               "v_segments", "device_bytes", "value_bytes")
+               "v_segments", "device_bytes", "value_bytes", "u_rows_finished_in_pass",
+               "u_rows_combined", "v_rows_finished_in_pass", "v_rows_combined")
 
 
 def ccdpp_info(h):

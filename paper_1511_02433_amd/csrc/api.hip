@@ -319,32 +319,33 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     while (S_ne > 0 && seg_start[S_ne] == seg_start[S_ne - 1]) --S_ne;
     L.nseg_ne = S_ne;
 
-    // Alignment padding: every segment starts at a multiple of kE, every tile at a
-    // multiple of kAlign; the entries skipped over are padding at the end of the
-    // previous segment.
+    // Alignment padding: every segment starts at a multiple of kE; the first segment
+    // of a tile, and a segment that begins a workgroup's share (below), at a multiple
+    // of kAlign.  The entries skipped over are padding at the end of the previous
+    // segment.
     const int64_t S_work = P == 1 ? S_ne : S;  // segments that hold entries
+    const std::vector<int64_t> seg_start0 = seg_start;  // unpadded
     std::vector<int32_t> seg_off((size_t)S, 0);
-    std::vector<int64_t> pstart((size_t)S + 1);
-    {
-        std::vector<char> tile_first((size_t)S + 1, 0);
-        for (int64_t p = 0; p < P; ++p) tile_first[tile_seg[p]] = 1;
+    std::vector<char> align_first((size_t)S + 1, 0);
+    for (int64_t p = 0; p < P; ++p) align_first[tile_seg[p]] = 1;
+    int64_t NP = 0;
+    auto pad_layout = [&]() -> int {
         int64_t off = 0;
         for (int64_t sg = 0; sg < S_work; ++sg) {
-            const int64_t al = tile_first[sg] ? kAlign : kE;
-            off += (al - (seg_start[sg] + off) % al) % al;
-            if (seg_start[sg] + off > (int64_t)INT32_MAX - kEntryPad)
+            const int64_t al = align_first[sg] ? kAlign : kE;
+            off += (al - (seg_start0[sg] + off) % al) % al;
+            if (seg_start0[sg] + off > (int64_t)INT32_MAX - kEntryPad)
                 return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
             seg_off[sg] = (int32_t)off;
-            pstart[sg] = seg_start[sg] + off;
+            seg_start[sg] = seg_start0[sg] + off;  // from here on, padded positions
         }
-        const int64_t NP = (N + off + kAlign - 1) / kAlign * kAlign;
+        NP = (N + off + kAlign - 1) / kAlign * kAlign;
         if (NP > (int64_t)INT32_MAX - kEntryPad)
             return fail(h, CCDPP_EINVAL, "too many entries after alignment padding");
-        for (int64_t sg = S_work; sg <= S; ++sg) pstart[sg] = NP;
-        L.npad = NP;
-    }
-    const int64_t NP = L.npad;
-    seg_start.swap(pstart);  // from here on, segment starts are padded positions
+        for (int64_t sg = S_work; sg <= S; ++sg) seg_start[sg] = NP;
+        return CCDPP_OK;
+    };
+    RCK(pad_layout());
 
     // Persistent workgroups own equal shares of the work, cut at multiples of kAlign; a
     // share is processed as one piece per tile it touches, and every piece is cut
@@ -354,13 +355,20 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // bounds ignore segment bounds: a segment cut by one or more chunk bounds leaves,
     // in every chunk it meets, a partial (num, den) in a slot of its own (the chunk's
     // head slot if the segment began before the chunk, else its tail slot), and the
-    // combine adds a row's partials in entry order.
-    // Two shares per compute unit: a workgroup holds a whole CU's LDS, so the second
-    // round of workgroups goes to whichever CUs finish first, which evens out the
-    // remaining differences in speed between shares.
-    int64_t G = opt && opt->workgroups > 0 ? opt->workgroups : 2 * (int64_t)h->cus;
-    if (!(opt && opt->workgroups > 0))
+    // partials of a row are added in entry order.
+    // Two shares per compute unit when every wave still gets several windows: a
+    // workgroup holds a whole CU's LDS, so the second round of workgroups goes to
+    // whichever CUs finish first, which evens out the remaining differences in speed
+    // between shares.  Smaller layouts take one share per compute unit, which halves
+    // the per-workgroup staging and start-up.
+    int64_t G;
+    if (opt && opt->workgroups > 0) {
+        G = opt->workgroups;
+    } else {
+        const int64_t two = 2 * (int64_t)h->cus;
+        G = NP >= two * kWaves * kWin * 8 ? two : (int64_t)h->cus;
         G = std::max<int64_t>(1, std::min<int64_t>(G, (NP + kWaves * kWin - 1) / (kWaves * kWin)));
+    }
     const int64_t wseg = !opt || opt->seg_weight == 0 ? kSegWeight
                          : std::max<int64_t>(0, opt->seg_weight);
     auto upa = [](int64_t v) { return (v + kAlign - 1) / kAlign * kAlign; };
@@ -384,14 +392,44 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         }
         return lo;
     };
+    auto target = [&](int64_t wt, int64_t g) { return wt / G * g + wt % G * g / G; };
+    // With P == 1 (float) every share boundary moves to the start of the nearest row,
+    // when none of them changes its shares by more than an eighth: rows are then
+    // cut only between the waves of one workgroup, which finishes them at the end of
+    // the pass, and no combine kernel runs.  Otherwise the shares stay balanced and
+    // the combine kernel finishes every cut row.
+    std::vector<int64_t> snap((size_t)G + 1, -1);
+    bool snapped = false;
+    if (P == 1 && G > 1 && S_work > 0 && !h->dbl) {
+        const int64_t wt = work_at(NP);
+        snapped = true;
+        for (int64_t g = 1; g < G && snapped; ++g) {
+            const int64_t t = target(wt, g);
+            const int64_t sg = std::min<int64_t>(seg_of(0, pos_at(t)), S_work - 1);
+            int64_t best = sg;
+            auto miss = [&](int64_t x) { return std::llabs(work_at(seg_start[x]) - t); };
+            if (sg + 1 < S_work && miss(sg + 1) < miss(sg)) best = sg + 1;
+            snap[g] = best;
+            snapped = miss(best) <= wt / G / 8;
+        }
+        if (snapped) {
+            for (int64_t g = 1; g < G; ++g) align_first[snap[g]] = 1;
+            RCK(pad_layout());
+        } else {
+            std::fill(snap.begin(), snap.end(), -1);
+        }
+    }
+    L.npad = NP;
     const int64_t work_total = work_at(NP);
     std::vector<int32_t> wg_piece(1, 0), piece_tile, piece_seg, chunk_flags;
     std::vector<int64_t> piece_chunk;
     std::vector<std::vector<int32_t>> src_of((size_t)S);  // partial slots of each cut segment
     std::vector<int64_t> gb((size_t)G + 1);
-    for (int64_t g = 0; g <= G; ++g)
-        gb[g] = g == 0 ? 0 : g == G ? NP : std::min(NP, upa(pos_at(work_total / G * g +
-                                                                    work_total % G * g / G)));
+    for (int64_t g = 0; g <= G; ++g) {
+        gb[g] = g == 0 ? 0 : g == G ? NP
+                : snap[g] >= 0 ? seg_start[snap[g]] : std::min(NP, upa(pos_at(target(work_total, g))));
+        if (g > 0) gb[g] = std::max(gb[g], gb[g - 1]);
+    }
     for (int64_t g = 0; g < G; ++g) {
         const int64_t lo = gb[g], hi = std::max(gb[g], gb[g + 1]);
         for (int64_t p = 0; p < P; ++p) {
@@ -430,9 +468,54 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     if (nslots > INT32_MAX) return fail(h, CCDPP_EINVAL, "too many partial slots");
 
     // Combine lists.  P == 1: only the rows whose segment was cut, each from its
-    // partial slots.  P > 1: every row, from its segments in tile order (a cut
+    // partial slots; a row cut only between the waves of one workgroup is finished
+    // by that workgroup at the end of the pass (its wg_cut list), the others by the
+    // combine kernel.  P > 1: every row, from its segments in tile order (a cut
     // segment by its partial slots), plus the segment list for the per-segment
     // copy of the committed coordinate.
+    if (P == 1) {
+        std::vector<int32_t> piece_wg((size_t)L.npieces);
+        for (int64_t g = 0; g < G; ++g)
+            for (int32_t pc = wg_piece[g]; pc < wg_piece[g + 1]; ++pc) piece_wg[pc] = (int32_t)g;
+        auto slot_wg = [&](int32_t slot) { return piece_wg[(slot - S) / 2 / kWaves]; };
+        std::vector<int32_t> wcut(1, 0), crow;
+        std::vector<uint64_t> cdesc;
+        std::vector<std::vector<int64_t>> local((size_t)G);
+        for (int64_t sg = 0; snapped && sg < S; ++sg) {
+            const auto& sl = src_of[sg];
+            if (sl.empty() || (int)sl.size() > kCutMaxSlots) continue;
+            const int32_t g0 = slot_wg(sl[0]);
+            bool one = true;
+            for (int32_t x : sl) one = one && slot_wg(x) == g0;
+            if (!one) continue;
+            // Local slot 2w (head) or 2w + 1 (tail) of wave w: the workgroup has one piece.
+            uint64_t d = (uint64_t)(sl.size() - 1);
+            for (size_t i = 0; i < sl.size(); ++i)
+                d |= (uint64_t)((sl[i] - S) % (2 * kWaves)) << (4 + 5 * i);
+            if (local[g0].size() >= 64) return fail(h, CCDPP_EDEVICE, "internal: too many cut rows");
+            local[g0].push_back(sg);
+            cdesc.push_back(d);
+            src_of[sg].insert(src_of[sg].begin(), -1);  // finished in the pass
+        }
+        std::vector<uint64_t> cdesc_sorted;
+        {
+            // cdesc follows segment order, which is also workgroup order.
+            size_t k = 0;
+            for (int64_t g = 0; g < G; ++g) {
+                for (int64_t sg : local[g]) {
+                    crow.push_back((int32_t)sg);
+                    cdesc_sorted.push_back(cdesc[k++]);
+                }
+                wcut.push_back((int32_t)crow.size());
+            }
+        }
+        RCK(upload(h, &L.wg_cut, wcut));
+        if (!crow.empty()) {
+            RCK(upload(h, &L.cut_row, crow));
+            RCK(upload(h, &L.cut_desc, cdesc_sorted));
+        }
+        L.ncut = (int32_t)crow.size();
+    }
     {
         std::vector<int32_t> ids, sptr(1, 0), srcs, gptr, gsegs;
         auto add_seg = [&](int64_t sg) {
@@ -443,7 +526,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         };
         if (P == 1) {
             for (int64_t sg = 0; sg < S; ++sg)
-                if (!src_of[sg].empty()) {
+                if (!src_of[sg].empty() && src_of[sg][0] >= 0) {
                     ids.push_back((int32_t)sg);
                     add_seg(sg);
                     sptr.push_back((int32_t)srcs.size());
@@ -1333,12 +1416,13 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     auto width = [](const ccdk::Layout& L) -> int64_t {
         return L.gather == ccdk::kGatherHot ? L.hot : L.T;
     };
-    const int64_t v[17] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[21] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
-                           h->dbl ? 8 : 4};
-    int32_t w = std::min<int32_t>(len, 17);
+                           h->dbl ? 8 : 4, h->L[0].ncut, h->L[0].ncomb, h->L[1].ncut,
+                           h->L[1].ncomb};
+    int32_t w = std::min<int32_t>(len, 21);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

@@ -85,7 +85,9 @@ constexpr int kWin = 64 * kE;             // entries per window
 constexpr int kAlign = kWin;              // tile, share and chunk starts: whole window blocks
 
 constexpr int kLdsBytes = 160 * 1024;     // LDS per workgroup
-constexpr int kLdsVecBytes = kLdsBytes;   // all of it holds staged vectors
+constexpr int kCutSlotBytes = 2 * 16 * 16;  // per-wave head and tail partials (P == 1)
+constexpr int kLdsVecBytes = kLdsBytes - kCutSlotBytes;  // the rest holds staged vectors
+constexpr int kCutMaxSlots = 12;          // slots of a row a workgroup finishes itself
 constexpr int kMinTiledSeg = 32;          // mean entries per segment for tiling to pay
 constexpr int kSegWeight = 4;             // default work of one segment, in entries
 constexpr int kChunkMid = 1;              // chunk flag: its first segment began in an earlier chunk
@@ -154,6 +156,11 @@ struct PassArgs {
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
     const int32_t* piece_seg;   // [npieces * kWaves] segment holding each chunk's first entry
     const int32_t* chunk_flags; // [npieces * kWaves] kChunkMid | kChunkCont
+    const int32_t* wg_cut;      // P == 1: [grid + 1] rows cut between the workgroup's waves,
+    const int32_t* cut_row;     //   which it finishes at the end of the pass from the
+    const uint64_t* cut_desc;   //   head (2w) and tail (2w + 1) partials of its waves w:
+                                //   bits 0-3 the slot count - 1, then 5 bits per slot
+    int32_t slot_lds;           // byte offset of those partials in LDS
     const V* x;                 // [cols] gathered vector of the update
     const V* p;                 // [S] own factor column, current feature, per segment
     const V* pp;                // [S] own factor column, previous feature (committed), per segment
@@ -215,11 +222,16 @@ struct Layout {
     int32_t* piece_seg = nullptr;
     int32_t* chunk_flags = nullptr;
     int32_t npieces = 0;
-    int32_t ncomb = 0;               // rows the combine finishes (P == 1: the cut ones)
+    int32_t ncomb = 0;               // rows the combine finishes (P == 1: those cut
+                                     // between workgroups)
     int32_t* comb_rows = nullptr;    // P == 1: their ids
     int32_t* src_ptr = nullptr;      // [ncomb + 1] partial slots of each combined row
     int32_t* srcs = nullptr;
     int64_t nsrc = 0;
+    int32_t* wg_cut = nullptr;       // P == 1: [grid + 1] rows each workgroup finishes,
+    int32_t* cut_row = nullptr;      //   those rows
+    uint64_t* cut_desc = nullptr;    //   and their wave partials in entry order
+    int32_t ncut = 0;
     int32_t* row_seg_ptr = nullptr;  // P > 1: segments of each row in tile order
     int32_t* row_segs = nullptr;
     double2* part = nullptr;         // [nslots]

@@ -398,15 +398,29 @@ struct Walk {
     int head;     // the chunk's head partial slot (its tail slot follows)
 };
 
+extern __shared__ f32x4 lds_raw[];  // dynamic LDS, 16-byte aligned
+
+// P == 1: the head (2w) and tail (2w + 1) partials of every wave w in LDS, after the
+// staged vectors, from which the workgroup finishes the rows cut between its waves.
+template <class V>
+__device__ __forceinline__ double2* cut_slots(const PassArgs<V>& a) {
+    return reinterpret_cast<double2*>(reinterpret_cast<char*>(lds_raw) + a.slot_lds);
+}
+template <class V>
+__device__ __forceinline__ double2* wave_slots(const PassArgs<V>& a) {
+    return cut_slots(a) + 2 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 // A segment's sums over this chunk: its coordinate (P == 1: segment s is row s)
 // or partial, or, for a segment that began in an earlier chunk, the chunk's
 // head partial.
 template <bool P1, class V>
 __device__ __forceinline__ void emit(const PassArgs<V>& a, const Walk& wk, int s, double num,
                                      double den) {
-    if (s == wk.mid)
+    if (s == wk.mid) {
         a.part[wk.head] = make_double2(num, den);
-    else if constexpr (P1)
+        if constexpr (P1 && sizeof(V) == 4) wave_slots(a)[0] = make_double2(num, den);
+    } else if constexpr (P1)
         a.y[s] = coordinate<V>(num, den, a.lambda);
     else
         a.part[s] = make_double2(num, den);
@@ -613,9 +627,11 @@ __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>&
         // The last segment: finished, or going on past the chunk (a partial in the head
         // slot when it is also the segment that began earlier, else in the tail slot).
         if (lane == 0) {
-            if (flags & kChunkCont)
-                a.part[wk.head + (wk.sb == wk.mid ? 0 : 1)] = make_double2(wk.cn, wk.cd);
-            else
+            if (flags & kChunkCont) {
+                const int t = wk.sb == wk.mid ? 0 : 1;
+                a.part[wk.head + t] = make_double2(wk.cn, wk.cd);
+                if constexpr (P1 && sizeof(V) == 4) wave_slots(a)[t] = make_double2(wk.cn, wk.cd);
+            } else
                 emit<P1, V>(a, wk, wk.sb, wk.cn, wk.cd);
         }
     }
@@ -628,7 +644,6 @@ __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>&
 template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
 __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     using N = Needs<MODE>;
-    extern __shared__ f32x4 lds_raw[];  // 16-byte aligned
     V* lds = reinterpret_cast<V*>(lds_raw);
     const int wg = blockIdx.x;
 
@@ -647,6 +662,24 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = (int)(threadIdx.x & 63u);
 
+    // P == 1, float: the rows cut between this workgroup's waves (at most 15), one per
+    // lane of wave 0, requested now and finished at the end from the waves' LDS
+    // partials.  (The double kernels are short of registers for it: their layouts
+    // leave every cut row to the combine kernel.)
+    constexpr bool CUT = MODE != kModeFlush && P1 && sizeof(V) == 4;
+    constexpr bool CUT_EARLY = CUT;
+    int cut0 = 0, ncut = 0, crow = 0;
+    uint64_t cdesc = 0;
+    if constexpr (CUT) {
+        cut0 = a.wg_cut[wg];
+        ncut = a.wg_cut[wg + 1] - cut0;
+    }
+    if constexpr (CUT_EARLY) {
+        if (wave == 0 && lane < ncut) {
+            crow = a.cut_row[cut0 + lane];
+            cdesc = a.cut_desc[cut0 + lane];
+        }
+    }
     if constexpr (MODE != kModeFlush && P1) {
         // The rows after the last non-empty one have no entries: coordinate 0.
         for (int i = wg * kWG + (int)threadIdx.x; i < a.rows - a.nseg_ne; i += gridDim.x * kWG)
@@ -679,6 +712,25 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
         if (lane == 0) a.sse_part[wg * kWaves + wave] = t;
+    } else if constexpr (P1) {
+        // Rows cut between this workgroup's waves: their partials, in entry order.
+        if (ncut > 0) {       // the same for every thread of the workgroup
+            __syncthreads();  // every wave's partials are in LDS
+            if (wave == 0 && lane < ncut) {
+                if constexpr (!CUT_EARLY) {
+                    crow = a.cut_row[cut0 + lane];
+                    cdesc = a.cut_desc[cut0 + lane];
+                }
+                const int n = (int)(cdesc & 15u) + 1;
+                double num = 0.0, den = 0.0;
+                for (int i = 0; i < n; ++i) {
+                    const double2 pv = cut_slots(a)[(int)((cdesc >> (4 + 5 * i)) & 31u)];
+                    num += pv.x;
+                    den += pv.y;
+                }
+                a.y[crow] = coordinate<V>(num, den, a.lambda);
+            }
+        }
     }
 }
 
@@ -861,6 +913,10 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     a.piece_chunk = L.piece_chunk;
     a.piece_seg = L.piece_seg;
     a.chunk_flags = L.chunk_flags;
+    a.wg_cut = L.wg_cut;
+    a.cut_row = L.cut_row;
+    a.cut_desc = L.cut_desc;
+    if (L.P == 1 && !L.wg_cut) return hipErrorInvalidValue;
     a.x = x;
     a.p = p;
     a.pp = pp;
@@ -890,7 +946,8 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
         a.tsw = L.hot;
         a.vec_elems = nv * a.Ts;
     }
-    const size_t lds = (size_t)a.vec_elems * sizeof(V);
+    a.slot_lds = (int32_t)(((size_t)a.vec_elems * sizeof(V) + 15) / 16 * 16);
+    const size_t lds = (size_t)a.slot_lds + (L.P == 1 ? (size_t)kCutSlotBytes : 0);
     if (lds > (size_t)kLdsBytes) return hipErrorInvalidValue;
     if (!staged && sizeof(V) == 4 && nv >= 2) {
         // Float first passes that gather two or three vectors from global memory read

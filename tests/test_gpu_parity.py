@@ -211,6 +211,11 @@ def test_layout_strategies_match_oracle(name):
         assert info["u_gather"] == 1 and info["v_gather"] == 1
     if name.startswith("hot"):
         assert info["v_gather"] == 3
+    if name == "auto":
+        # Short rows at every share boundary: the workgroups finish the rows cut between
+        # their waves themselves, and no combine kernel runs on either side.
+        for side in "uv":
+            assert info[f"{side}_rows_finished_in_pass"] > 0 and info[f"{side}_rows_combined"] == 0
 
 
 @pytest.mark.parametrize("layout", ["auto", "global", "hot"])
@@ -258,7 +263,9 @@ def test_short_segments_fill_windows(layout, transpose):
 
 def test_heavy_rows_in_tiles_and_layout_equivalence():
     # Rows far longer than kGroupMaxLen inside tiles, plus the same problem under two
-    # layouts: results agree to summation-order rounding.
+    # layouts: results agree to summation-order rounding.  With one tile per side,
+    # rows cut between the waves of a workgroup are finished by the pass itself, and
+    # rows too long to keep inside one workgroup's share by the combine kernel.
     from paper_1511_02433_amd.ccdpp import make_options
     lens = [5000, 3000, 2049, 1025, 1024, 513, 200, 64, 9, 1, 0] * 3
     row, col, val, H0 = synth.lengths_problem(lens, 6000, 3, seed=41)
@@ -267,6 +274,12 @@ def test_heavy_rows_in_tiles_and_layout_equivalence():
     res = []
     for opts in (make_options(), make_options(gather_mode=(2, 2), tile_width=(512, 16))):
         g = CCDPP(m, 6000, 3, 0.05, row, col, val, opts=opts)
+        info = g.info()
+        print({k: v for k, v in info.items() if k.startswith(("u_", "v_"))})
+        if info["u_tiles"] == 1:
+            # Rows of 5000 entries in shares of about 8000: the shares stay balanced and
+            # the combine kernel finishes every cut row.
+            assert info["u_rows_finished_in_pass"] == 0 and info["u_rows_combined"] > 0
         g.set_factors(np.zeros((m, 3), np.float32), H0)
         g.run(1, 3)
         res.append(g.factors())
