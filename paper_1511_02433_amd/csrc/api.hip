@@ -400,7 +400,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // the combine kernel finishes every cut row.
     std::vector<int64_t> snap((size_t)G + 1, -1);
     bool snapped = false;
-    if (P == 1 && G > 1 && S_work > 0 && !h->dbl) {
+    if (P == 1 && S_work > 0 && !h->dbl) {  // (one workgroup: nothing to move)
         const int64_t wt = work_at(NP);
         snapped = true;
         for (int64_t g = 1; g < G && snapped; ++g) {
