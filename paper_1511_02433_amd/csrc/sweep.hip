@@ -316,22 +316,23 @@ struct Win {
 
 // Data loads of the window block at b (a multiple of kWin): lane l's values from
 // the two halves of the block (val_slot order), its indices in entry order.
-// Lanes at or past `lim` read lane 0's part instead, so every address stays
-// inside the arrays; a window past the chunk rereads block b.
+// Chunks start and end at multiples of kWin, so every block a chunk reads lies
+// whole inside the arrays.  A window past the chunk's end (own == false) rereads
+// lane 0's part of block b on every lane: one line, never used.  Positions fit
+// 31 bits (the layout build checks), so they are 32-bit here.
 template <bool IDX16, class V>
-__device__ __forceinline__ void load_data(const PassArgs<V>& a, int64_t b, int64_t lim, uint32_t le,
+__device__ __forceinline__ void load_data(const PassArgs<V>& a, int32_t b, bool own, uint32_t le,
                                           Win<V>& w) {
     using VV = typename Vec16<V>::type;
-    const bool in = b + (int64_t)le < lim;
-    const VV* vp = reinterpret_cast<const VV*>(a.val + b) + (in ? (int)(le / kE) : 0);
+    const uint32_t lo = own ? le : 0u;
+    const VV* vp = reinterpret_cast<const VV*>(a.val + b) + (int)(lo / kE);
 #pragma unroll
     for (int q = 0; q < kE / Win<V>::E; ++q) w.vv[q] = __builtin_nontemporal_load(vp + 64 * q);
-    const int64_t eb = b + (in ? (int64_t)le : 0);
     if constexpr (IDX16) {
         w.c0 = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + eb));
+            reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + b + lo));
     } else {
-        const u32x4* ip = reinterpret_cast<const u32x4*>(static_cast<const int32_t*>(a.idx) + eb);
+        const u32x4* ip = reinterpret_cast<const u32x4*>(static_cast<const int32_t*>(a.idx) + b + lo);
         w.c0 = __builtin_nontemporal_load(ip);
         w.c1 = __builtin_nontemporal_load(ip + 1);
     }
@@ -388,8 +389,8 @@ __device__ __forceinline__ double lane_read(double v, int src) { return lane_f64
 
 // State a wave carries from window to window of its chunk.
 struct Walk {
-    int64_t elo;  // first entry of the next window (a multiple of kE)
-    int64_t c1;   // end of the chunk (a multiple of kE)
+    int32_t elo;  // first entry of the next window (a multiple of kWin)
+    int32_t c1;   // end of the chunk (a multiple of kWin)
     int sb;       // segment of the entry before elo (the open one, when `open`)
     bool open;    // a segment is open: it has entries before elo in this chunk
     double cn, cd;  // sums of the open segment so far
@@ -446,8 +447,8 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     constexpr bool EARLY = GLOBAL && sizeof(V) == 4;
     // A float first pass gathers its two or three vectors as one 16-byte record.
     constexpr bool PACK = EARLY && N::q && (N::qq || (N::x && !XQ));
-    const int64_t b = wk.elo;
-    const int64_t we = min(b + (int64_t)kWin, wk.c1);
+    const int32_t b = wk.elo;
+    const int32_t we = min(b + kWin, wk.c1);
     // Gathers from global memory: in a hot layout, the entries past the staged
     // columns (the others read the padding column, which costs no memory access).
     V gq[kE], gqq[kE], gxx[kE];
@@ -473,9 +474,9 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     // Data of the window after next, before anything waits on this one (a harmless
     // reload of b past the chunk's end).
     {
-        const int64_t b2 = we + kWin;
+        const int32_t b2 = we + kWin;
         const bool more = b2 < wk.c1;
-        load_data<IDX16, V>(a, more ? b2 : b, more ? wk.c1 : b, le, nn);
+        load_data<IDX16, V>(a, more ? b2 : b, more, le, nn);
     }
     const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
     const bool lv = lane < nl;
@@ -597,19 +598,19 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
 // c0; it began in an earlier chunk when the chunk's first lane does not start it
 // (flag kChunkMid).
 template <int MODE, bool IDX16, class V>
-__device__ __forceinline__ void begin_chunk(const PassArgs<V>& a, int64_t c0, int64_t c1, int s0,
+__device__ __forceinline__ void begin_chunk(const PassArgs<V>& a, int32_t c0, int32_t c1, int s0,
                                             int flags, int lane, Win<V>& wa, Win<V>& wb) {
     const uint32_t le = (uint32_t)lane * kE;
-    load_data<IDX16, V>(a, c0, c1, le, wa);
+    load_data<IDX16, V>(a, c0, true, le, wa);
     load_slots<MODE, V>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
     const bool more = c0 + kWin < c1;
-    load_data<IDX16, V>(a, more ? c0 + kWin : c0, more ? c1 : c0, le, wb);
+    load_data<IDX16, V>(a, more ? c0 + kWin : c0, more, le, wb);
 }
 
 // wa and wb hold the requests of begin_chunk.
 template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
-__device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>& gx, int64_t c0,
-                                          int64_t c1, int s0, int flags, int gc, int lane,
+__device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>& gx, int32_t c0,
+                                          int32_t c1, int s0, int flags, int gc, int lane,
                                           Win<V>& wa, Win<V>& wb, double& sse) {
     const uint32_t le = (uint32_t)lane * kE;
     const bool mid = flags & kChunkMid;
@@ -689,8 +690,8 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     double sse = 0.0;
     int staged = -1;
     for (int pc = a.wg_piece[wg]; pc < a.wg_piece[wg + 1]; ++pc) {
-        const int64_t c0 = a.piece_chunk[pc * (kWaves + 1) + wave];
-        const int64_t c1 = a.piece_chunk[pc * (kWaves + 1) + wave + 1];
+        const int32_t c0 = (int32_t)a.piece_chunk[pc * (kWaves + 1) + wave];
+        const int32_t c1 = (int32_t)a.piece_chunk[pc * (kWaves + 1) + wave + 1];
         const int gc = pc * kWaves + wave;
         const int s0 = a.piece_seg[gc], flags = a.chunk_flags[gc];
         // The chunk's first windows are requested before the staging, which they do
