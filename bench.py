@@ -36,8 +36,8 @@ def kernel_symbol(kind: int, info: dict, layout: int) -> str:
     """The kernel's name as a trace shows it (the sweep kernels are templated on
     LDS staging, 16-bit indices, P == 1 and the value type)."""
     v = "double" if info.get("value_bytes", 4) == 8 else "float"
-    if kind == 2:
-        return f"void ccdk::ccd_combine<{v}>(ccdk::CombineArgs<{v}>)"
+    if kind == 2:  # (4 lanes per row instead of 16 on layouts whose rows have few partials)
+        return f"void ccdk::ccd_combine<16, {v}>(ccdk::CombineArgs<{v}>)"
     if kind == 3:
         return f"void ccdk::ccd_copy<{v}>({v} const*, {v}*, long)"
     pre = "u" if layout == 0 else "v"

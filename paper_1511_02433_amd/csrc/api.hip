@@ -554,6 +554,8 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             RCK(upload(h, &L.srcs, srcs));
         }
         L.nsrc = (int64_t)srcs.size();
+        // A quad per row when rows have fewer than 12 partials on average.
+        L.comb_lanes = L.ncomb > 0 && L.nsrc < 12 * (int64_t)L.ncomb ? 4 : 16;
         HIPCK(h, dalloc(h, &L.part, nslots));
         L.nslots = nslots;
     }

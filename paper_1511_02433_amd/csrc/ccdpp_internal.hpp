@@ -222,6 +222,7 @@ struct Layout {
     int32_t* piece_seg = nullptr;
     int32_t* chunk_flags = nullptr;
     int32_t npieces = 0;
+    int32_t comb_lanes = 16;         // lanes per row of the combine (4 when rows have few partials)
     int32_t ncomb = 0;               // rows the combine finishes (P == 1: those cut
                                      // between workgroups)
     int32_t* comb_rows = nullptr;    // P == 1: their ids

@@ -773,30 +773,41 @@ __device__ __forceinline__ double row16_sum(double x) {
     return x;
 }
 
-// Fixed-order combine of a row's partials: 16 lanes (one DPP row) per row; lane
-// l adds the row's partial slots l, l + 16, ... in entry order, then a fixed
-// tree over the 16 lanes.  With yseg, the coordinate is also written to every
-// segment of the row.
-constexpr int kCombineLanes = 16;
-template <class V>
+// x summed over the 4 lanes of a quad, every lane getting the same bits.
+__device__ __forceinline__ double quad_sum(double x) {
+    x += dppq_d<0xB1>(x);  // lane ^ 1
+    x += dppq_d<0x4E>(x);  // lane ^ 2
+    return x;
+}
+
+// Fixed-order combine of a row's partials: L lanes per row (16, one DPP row, or
+// 4, a quad, for layouts whose rows have few partials); lane l adds the row's
+// partial slots l, l + L, ... in entry order, then a fixed tree over the L
+// lanes.  With yseg, the coordinate is also written to every segment of the row.
+template <int L, class V>
 __global__ __launch_bounds__(256) void ccd_combine(CombineArgs<V> c) {
-    const int l = (int)(threadIdx.x & (kCombineLanes - 1));
-    const int i = blockIdx.x * (256 / kCombineLanes) + (int)(threadIdx.x / kCombineLanes);
-    if (i >= c.n) return;  // whole 16-lane rows leave together
+    const int l = (int)(threadIdx.x & (L - 1));
+    const int i = blockIdx.x * (256 / L) + (int)(threadIdx.x / L);
+    if (i >= c.n) return;  // whole rows of lanes leave together
     const int b = c.src_ptr[i];
     const int e = c.src_ptr[i + 1];
     double num = 0.0, den = 0.0;
-    for (int k = b + l; k < e; k += kCombineLanes) {
+    for (int k = b + l; k < e; k += L) {
         const double2 pv = c.part[c.srcs[k]];
         num += pv.x;
         den += pv.y;
     }
-    num = row16_sum(num);
-    den = row16_sum(den);
+    if constexpr (L == 16) {
+        num = row16_sum(num);
+        den = row16_sum(den);
+    } else {
+        num = quad_sum(num);
+        den = quad_sum(den);
+    }
     const V yr = coordinate<V>(num, den, c.lambda);
     if (l == 0) c.y[c.ids ? c.ids[i] : i] = yr;
     if (c.yseg)
-        for (int k = c.seg_ptr[i] + l; k < c.seg_ptr[i + 1]; k += kCombineLanes) c.yseg[c.segs[k]] = yr;
+        for (int k = c.seg_ptr[i] + l; k < c.seg_ptr[i + 1]; k += L) c.yseg[c.segs[k]] = yr;
 }
 
 template <class V>
@@ -991,9 +1002,10 @@ hipError_t launch_combine(const Layout& L, V* y, V* yseg, double lambda, hipStre
     c.yseg = yseg;
     c.n = L.ncomb;
     c.lambda = lambda;
-    constexpr int rows_per_block = 256 / kCombineLanes;
-    hipLaunchKernelGGL(ccd_combine<V>, dim3((unsigned)((L.ncomb + rows_per_block - 1) / rows_per_block)),
-                       dim3(256), 0, s, c);
+    if (L.comb_lanes == 4)
+        hipLaunchKernelGGL((ccd_combine<4, V>), dim3((unsigned)((L.ncomb + 63) / 64)), dim3(256), 0, s, c);
+    else
+        hipLaunchKernelGGL((ccd_combine<16, V>), dim3((unsigned)((L.ncomb + 15) / 16)), dim3(256), 0, s, c);
     return hipGetLastError();
 }
 
