@@ -90,14 +90,15 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 mode takes it when tiles would hold too few entries per
  *                 row)
  *   tile_width  : columns per LDS tile (0: as wide as LDS allows); at most
- *                 163840 / (b * v) - 64, rounded down to a multiple of 64,
+ *                 (163840 - 512) / (b * v) - 64, rounded down to a multiple of 64,
  *                 where b is the bytes per value (4, or 8 with precision 1)
  *                 and v = 2 for index 0 and 3 for index 1 (the vectors the
  *                 first pass of a feature stages).  With gather_mode 3, the
- *                 hot width: a multiple of 32, at most 163840 / b - 64
+ *                 hot width: a multiple of 32, at most (163840 - 512) / b - 64
  *                 rounded down to a multiple of 64 (0: that maximum); each
  *                 pass stages as much of it as its vectors leave room for
- *   workgroups  : persistent workgroups per pass (0: two per compute unit)
+ *   workgroups  : persistent workgroups per pass (0: two per compute unit,
+ *                 one for copies of fewer than about 33.5M entries)
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 4;
  *                 -1: shares by entries alone)

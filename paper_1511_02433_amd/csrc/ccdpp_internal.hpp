@@ -29,10 +29,15 @@ namespace ccdk {
 // writes the coordinate directly; with P > 1 every segment yields a partial
 // (numerator, denominator) and a combine kernel adds a row's partials in tile
 // order.  A layout whose tiles would hold too few entries per segment keeps
-// P == 1 and gathers from global memory instead ("global" mode).
+// P == 1 and becomes a hot layout (below); a forced "global" layout gathers
+// everything from global memory.
 //
 // Persistent workgroups of kWG threads each own an equal, contiguous share of
-// the layout's (tile-major) entries.  A share that crosses tile boundaries is
+// the layout's (tile-major) entries (two shares per CU when every wave still
+// gets several windows, else one).  With P == 1 (float) the share bounds sit on
+// row starts when that keeps the shares within an eighth of equal; rows are then
+// cut only between the waves of one workgroup, which finishes them at the end of
+// the pass from partials its waves leave in LDS, and no combine kernel runs.  A share that crosses tile boundaries is
 // processed as one "piece" per tile, restaging LDS between pieces; inside a
 // piece each of the 16 waves owns one of 16 equal contiguous chunks.  Chunk
 // bounds do not follow segment bounds, so every wave streams the same number
