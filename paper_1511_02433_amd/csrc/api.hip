@@ -54,6 +54,8 @@ struct ccdpp {
     int32_t* perm0 = nullptr;      // e -> input triplet index
     int32_t* pos0 = nullptr;       // e -> value slot in the user-major copy
     int32_t* map01 = nullptr;      // e -> value slot in the item-major copy
+    int32_t* slot01 = nullptr;     // element-wise CCD: user-major slot -> item-major slot (or -1)
+    int32_t* slot10 = nullptr;     //   and back; built on the first ccdpp_ccd_run
     // Value type of the residual, the factors and the sweep arithmetic: float, or
     // double with options.precision = 1.  The arrays below hold that type.
     bool dbl = false;
@@ -984,22 +986,33 @@ template <class V>
 int ccd_impl(ccdpp* h, int32_t outer) {
     using namespace ccdk;
     const int64_t m = h->m, n = h->n;
+    if (outer > 0 && !h->slot01) {
+        // Slot-to-slot maps between the copies, for the residual refresh after each phase.
+        int32_t *s01, *s10;
+        HIPCK(h, dalloc(h, &s01, h->L[0].npad));
+        HIPCK(h, dalloc(h, &s10, h->L[1].npad));
+        HIPCK(h, hipMemsetAsync(s01, 0xFF, (size_t)h->L[0].npad * 4, h->stream));
+        HIPCK(h, hipMemsetAsync(s10, 0xFF, (size_t)h->L[1].npad * 4, h->stream));
+        HIPCK(h, launch_slot_map(h->pos0, h->map01, h->nnz, s01, h->stream));
+        HIPCK(h, launch_slot_map(h->map01, h->pos0, h->nnz, s10, h->stream));
+        h->slot01 = s01;
+        h->slot10 = s10;
+    }
     for (int32_t it = 0; it < outer; ++it) {
         for (int li = 0; li < 2; ++li) {
             V* own = as<V>(li == 0 ? h->W : h->H);
             V* other = as<V>(li == 0 ? h->H : h->W);
-            V* tmp = as<V>(li == 0 ? h->u : h->v);
             const int64_t rows = li == 0 ? m : n, cols = li == 0 ? n : m;
             for (int32_t t = 0; t < h->k; ++t) {
                 V* ot = other + (int64_t)t * cols;
                 const V* op = t > 0 ? other + (int64_t)(t - 1) * cols : nullptr;
                 // R-hat = R + own_t other_t (minus the pending feature t - 1), own_t from
-                // eq. 5 / eq. 8 into tmp; a tiled copy's combine also writes own_t per segment.
-                RCK(pass<V>(h, li, t > 0 ? kModeSubAdd : kModeAdd, ot, t, t - 1, ot, op, tmp, t,
-                            t > 0 ? 2 : 1));
-                Timed tm(h, CCDPP_K_COMMIT, li, 2.0 * sizeof(V) * rows);
-                HIPCK(h, launch_copy<V>(tmp, own + (int64_t)t * rows, rows, h->stream));
-                tm.done();
+                // eq. 5 / eq. 8 written in place: a segment's old own_t is read before the
+                // segment's new value is written, and a row cut between chunks is written
+                // only after every chunk (by the workgroup at the end, or by the combine,
+                // which for a tiled copy also writes own_t per segment).
+                RCK(pass<V>(h, li, t > 0 ? kModeSubAdd : kModeAdd, ot, t, t - 1, ot, op,
+                            own + (int64_t)t * rows, t, t > 0 ? 2 : 1));
             }
             // The pending update of feature k - 1, and for the item-major copy the
             // training sum of squares.
@@ -1008,11 +1021,11 @@ int ccd_impl(ccdpp* h, int32_t outer) {
             if (li == 1)
                 HIPCK(h, launch_reduce_sum(h->sse_part, h->L[1].grid * kWaves, h->d_scalar, h->stream));
             if (li == 0)
-                HIPCK(h, (launch_copy_mapped<V, V>(as<V>(h->L[0].val), h->pos0, as<V>(h->L[1].val),
-                                                   h->map01, h->nnz, h->stream)));
+                HIPCK(h, (launch_copy_slots<V>(as<V>(h->L[0].val), h->slot01, as<V>(h->L[1].val),
+                                               h->L[0].npad, h->stream)));
             else
-                HIPCK(h, (launch_copy_mapped<V, V>(as<V>(h->L[1].val), h->map01, as<V>(h->L[0].val),
-                                                   h->pos0, h->nnz, h->stream)));
+                HIPCK(h, (launch_copy_slots<V>(as<V>(h->L[1].val), h->slot10, as<V>(h->L[0].val),
+                                               h->L[1].npad, h->stream)));
         }
     }
     if (outer > 0) {

@@ -104,6 +104,24 @@ __global__ void k_compose(const int32_t* __restrict__ a, const int32_t* __restri
         out[q] = a[b[q]];
 }
 
+// out[from[e]] = to[e]: a map between value slots of the two copies.
+__global__ void k_slot_map(const int32_t* __restrict__ from, const int32_t* __restrict__ to,
+                           int64_t n, int32_t* __restrict__ out) {
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < n; q += (int64_t)gridDim.x * kT)
+        out[from[q]] = to[q];
+}
+
+// dst[map[f]] = src[f] over the source copy's value slots in order (slots of
+// padding entries map to -1): sequential reads, one scattered write per entry.
+template <class V>
+__global__ void k_copy_slots(const V* __restrict__ src, const int32_t* __restrict__ map,
+                             V* __restrict__ dst, int64_t n) {
+    for (int64_t f = (int64_t)blockIdx.x * kT + threadIdx.x; f < n; f += (int64_t)gridDim.x * kT) {
+        const int32_t g = map[f];
+        if (g >= 0) dst[g] = src[f];
+    }
+}
+
 template <class V>
 __global__ void k_fill(V* __restrict__ dst, V value, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < n; i += (int64_t)gridDim.x * kT)
@@ -325,6 +343,20 @@ hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t
     return hipGetLastError();
 }
 
+hipError_t launch_slot_map(const int32_t* from, const int32_t* to, int64_t n, int32_t* out,
+                          hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_slot_map, grid_for(n), dim3(kT), 0, s, from, to, n, out);
+    return hipGetLastError();
+}
+
+template <class V>
+hipError_t launch_copy_slots(const V* src, const int32_t* map, V* dst, int64_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_copy_slots<V>), grid_for(n), dim3(kT), 0, s, src, map, dst, n);
+    return hipGetLastError();
+}
+
 template <class V>
 hipError_t launch_fill(V* dst, V value, int64_t n, hipStream_t s) {
     if (n == 0) return hipSuccess;
@@ -411,6 +443,7 @@ hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* 
                                               int64_t, int, const int32_t*, uint32_t, bool, void*, \
                                               V*, int32_t*, hipStream_t);                       \
     template hipError_t launch_fill<V>(V*, V, int64_t, hipStream_t);                            \
+    template hipError_t launch_copy_slots<V>(const V*, const int32_t*, V*, int64_t, hipStream_t); \
     template hipError_t launch_scatter_factor_in<float, V>(const float*, const int32_t*,        \
                                                            int64_t, int32_t, V*, hipStream_t);  \
     template hipError_t launch_scatter_factor_in<double, V>(const double*, const int32_t*,      \

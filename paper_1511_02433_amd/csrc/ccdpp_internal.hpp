@@ -277,6 +277,10 @@ hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const f
                               void* idx, V* val, int32_t* pos, hipStream_t s);
 hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
+hipError_t launch_slot_map(const int32_t* from, const int32_t* to, int64_t n, int32_t* out,
+                          hipStream_t s);
+template <class V>
+hipError_t launch_copy_slots(const V* src, const int32_t* map, V* dst, int64_t n, hipStream_t s);
 hipError_t launch_compose(const int32_t* a, const int32_t* b, int64_t n, int32_t* out,
                           hipStream_t s);
 template <class V>
