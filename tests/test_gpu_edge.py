@@ -80,6 +80,20 @@ def test_one_dense_row_or_column(transpose):
     _compare(m, n, 1, 0.1, row, col, val, H0, outer=2, inner=3)
 
 
+def test_row_across_every_wave_of_a_workgroup():
+    # One row of 20,000 entries with a few short rows after it, in one workgroup: the long row
+    # is cut between all 16 waves, more partials than a workgroup finishes itself, so the
+    # combine kernel finishes it (any short row cut between waves the workgroup finishes).
+    lens = [20_000] + list(np.random.default_rng(66).integers(1, 30, 20))
+    row, col, val, H0 = synth.lengths_problem(lens, 20_000, 1, seed=67)
+    print(f"case: one row across all waves nnz={row.size}", flush=True)
+    g = _compare(len(lens), 20_000, 1, 0.1, row, col, val, H0, outer=2, inner=2,
+                 opts=make_options(workgroups=1))
+    info = g.info()
+    print({k: v for k, v in info.items() if k.startswith("u_")})
+    assert info["u_rows_combined"] == 1
+
+
 def test_rows_at_window_and_chunk_boundaries():
     # Lengths around multiples of the 8-entry lane group and the 512-entry window.
     lens = [511, 512, 513, 1023, 1024, 1025, 7, 8, 9, 63, 64, 65, 255, 256, 257] * 4
