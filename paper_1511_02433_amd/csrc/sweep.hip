@@ -272,7 +272,28 @@ __device__ __forceinline__ void stage_tile(const PassArgs<V>& a, int tile, V* ld
     // Strided elements per thread per step, loads first, so that a step costs one
     // memory latency: sixteen floats (one or two steps cover a tile), or four
     // doubles, which keeps the fused double kernels within their registers.
-    constexpr int kU = sizeof(V) == 4 ? 16 : 4;
+    if constexpr (sizeof(V) == 4) {
+        // Float slices go straight from memory into LDS: wave w fills the 64-word blocks
+        // w, w + 16, ... of every slot, lane l loading the column whose swizzled position
+        // is the block's word l (the swizzle stays inside 32-word groups, so the loads
+        // stay coalesced).  Columns at or past len read 0 through the bounded descriptor;
+        // a slot holds at least len rounded up to 64 words (Ts).
+        const int wave = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63u);
+        const int words = (len + 63) / 64 * 64;
+        auto fill = [&](const V* src, V* dst) {
+            const rsrc_t r = make_rsrc(src + c0, (uint64_t)len * sizeof(V));
+            for (int b = wave * 64; b < words; b += kWG) {
+                const uint32_t c = lds_swizzle((uint32_t)(b + lane));
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    r, (__attribute__((address_space(3))) void*)(dst + b), 4, c * 4u, 0, 0, 0);
+            }
+        };
+        if (N::x && !alias) fill(a.x, sx);
+        if (N::q) fill(a.q, sq);
+        if (N::qq) fill(a.qq, sqq);
+        __builtin_amdgcn_s_waitcnt(0);  // the loads into LDS are done
+    } else {
+    constexpr int kU = 4;
     for (int i0 = (int)threadIdx.x; i0 < len; i0 += kU * kWG) {
         V vx[kU], vq[kU], vqq[kU];
 #pragma unroll
@@ -292,6 +313,7 @@ __device__ __forceinline__ void stage_tile(const PassArgs<V>& a, int tile, V* ld
                 if (N::qq) sqq[li] = vqq[u];
             }
         }
+    }
     }
     if (!HOT && threadIdx.x == 0) {  // hot layouts pad with a global column
         if (N::x && !alias) sx[a.pad] = V(0);
@@ -954,7 +976,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
         // As many leading columns as the pass's vectors leave room for.
         const int64_t fit = ((int64_t)kLdsVecBytes / ((int64_t)sizeof(V) * nv) - 64) / 64 * 64;
         a.T = (int32_t)std::min<int64_t>(L.hot, fit);
-        a.Ts = a.T;
+        a.Ts = (a.T + 63) / 64 * 64;  // whole 64-word blocks (at most fit)
         a.tsw = L.hot;
         a.vec_elems = nv * a.Ts;
     }
