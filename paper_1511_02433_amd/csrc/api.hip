@@ -558,7 +558,12 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         L.nsrc = (int64_t)srcs.size();
         // A quad per row when rows have fewer than 12 partials on average.
         L.comb_lanes = L.ncomb > 0 && L.nsrc < 12 * (int64_t)L.ncomb ? 4 : 16;
-        HIPCK(h, dalloc(h, &L.part, nslots));
+        RCK(with_value_type(h, [&](auto z) -> int {
+            part_t<decltype(z)>* pp;
+            HIPCK(h, dalloc(h, &pp, nslots));
+            L.part = pp;
+            return CCDPP_OK;
+        }));
         L.nslots = nslots;
     }
     if (!lds && !h->dbl) {
@@ -736,8 +741,8 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
     HIPCK(h, dalloc(h, &h->d_count, 1));
     for (int li = 0; li < 2; ++li)  // partials are written before they are read: start them as NaN
-        HIPCK(h, launch_fill<float>(reinterpret_cast<float*>(h->L[li].part), __builtin_nanf(""),
-                                    4 * h->L[li].nslots, s));
+        HIPCK(h, launch_fill<float>(static_cast<float*>(h->L[li].part), __builtin_nanf(""),
+                                    (h->dbl ? 4 : 2) * h->L[li].nslots, s));
     RCK(with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
         V *A, *W, *H, *u, *v;
@@ -853,7 +858,7 @@ double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors, do
     const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
     double b = (L.idx16 ? 2.0 : 4.0) * nnz + vb * nnz;
     if (mode != kModePlain) b += vb * nnz;
-    if (mode != kModeFlush) b += L.P == 1 ? vb * S : 16.0 * S;
+    if (mode != kModeFlush) b += L.P == 1 ? vb * S : 2.0 * vb * S;  // coordinate or partial
     if (mode == kModeAdd || mode == kModeSubAdd) b += vb * S;
     if (mode == kModeSubAdd || mode == kModeFlush) b += vb * S;
     b += vb * cols * gathered_vectors;
@@ -888,10 +893,10 @@ int pass(ccdpp* h, int li, ccdk::PassMode mode, const V* x, int32_t pcol, int32_
     }
     if (mode != ccdk::kModeFlush && L.ncomb > 0) {
         V* yseg = commit >= 0 && L.P > 1 ? seg_col<V>(h, li, commit) : nullptr;
-        // Partial slots read (16 B) and listed (4 B), per row a list bound, an id and y;
+        // Partial slots read (two values) and listed (4 B), per row a list bound, an id and y;
         // with yseg the segment list and the per-segment copy.
         Timed tc(h, CCDPP_K_COMBINE, li,
-                 20.0 * L.nsrc + (8.0 + vb) * L.ncomb + (yseg ? (4.0 + vb) * L.nseg : 0.0));
+                 (2.0 * vb + 4.0) * L.nsrc + (8.0 + vb) * L.ncomb + (yseg ? (4.0 + vb) * L.nseg : 0.0));
         HIPCK(h, ccdk::launch_combine<V>(L, y, yseg, h->lambda, h->stream));
         tc.done();
     }

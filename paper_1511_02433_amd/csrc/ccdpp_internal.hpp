@@ -150,6 +150,13 @@ enum GatherMode : int32_t {
     kGatherHot = 3,     // P == 1, the leading columns staged in LDS, the rest from global
 };
 
+// A segment's partial (numerator, denominator): summed in fp64 across windows and
+// stored at the value type's precision (rounded once to fp32 for float values).
+template <class V> struct PartOf;
+template <> struct PartOf<float> { using type = float2; };
+template <> struct PartOf<double> { using type = double2; };
+template <class V> using part_t = typename PartOf<V>::type;
+
 // V is the type of the residual, the factors and the in-window arithmetic:
 // float (the paper's faster variant, Section 8) or double.
 template <class V>
@@ -174,7 +181,7 @@ struct PassArgs {
     const V* pk;                // [4 * cols] float hot or global first passes: (x, q, qq, 0)
                                 // of every column, so that a gather reads one 16-byte record
     V* y;                       // [rows] coordinates (P == 1)
-    double2* part;              // [S + 2 * chunks] partials: per segment (P > 1), then the
+    part_t<V>* part;            // [S + 2 * chunks] partials: per segment (P > 1), then the
                                 // head and tail slot of every chunk
     double* sse_part;           // [grid * kWaves] flush: per-wave sum of squares
     int32_t rows, cols, T, P;   // hot layouts: T is the pass's staged width
@@ -197,7 +204,7 @@ struct CombineArgs {
     const int32_t* srcs;
     const int32_t* seg_ptr;      // [n + 1] segments of each row (with yseg)
     const int32_t* segs;
-    const double2* part;
+    const part_t<V>* part;
     V* y;
     V* yseg;                     // optional [S]: y spread over the row's segments
     int32_t n;
@@ -240,7 +247,7 @@ struct Layout {
     int32_t ncut = 0;
     int32_t* row_seg_ptr = nullptr;  // P > 1: segments of each row in tile order
     int32_t* row_segs = nullptr;
-    double2* part = nullptr;         // [nslots]
+    void* part = nullptr;            // [nslots] part_t of the value type
     void* pk = nullptr;              // float hot or global layouts: [4 * cols] packed gathers
     int64_t nslots = 0;
     int64_t nseg = 0;

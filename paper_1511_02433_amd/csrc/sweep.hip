@@ -27,7 +27,9 @@
 // Arithmetic: R-hat in fp32 FMA.  Inside a window (at most 512 entries) the
 // sums of R-hat*x and x^2 are fp32 segmented scans; a segment's window sums are
 // added in fp64, across windows too, in a fixed order, so results are
-// identical run to run.  The coordinate num / (lambda + den) is an IEEE fp64
+// identical run to run.  A tiled copy stores each segment's sums as a partial
+// of the value type (one fp32 rounding for float values), which the combine
+// adds in fp64.  The coordinate num / (lambda + den) is an IEEE fp64
 // division rounded once to fp32; a coordinate whose denominator is exactly zero
 // (lambda = 0 and an empty row) is set to zero.
 #include <algorithm>
@@ -434,6 +436,11 @@ __device__ __forceinline__ double2* wave_slots(const PassArgs<V>& a) {
     return cut_slots(a) + 2 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 }
 
+__device__ __forceinline__ float2 make_part(float, double n, double d) {
+    return make_float2((float)n, (float)d);
+}
+__device__ __forceinline__ double2 make_part(double, double n, double d) { return make_double2(n, d); }
+
 // A segment's sums over this chunk: its coordinate (P == 1: segment s is row s)
 // or partial, or, for a segment that began in an earlier chunk, the chunk's
 // head partial.
@@ -441,12 +448,12 @@ template <bool P1, class V>
 __device__ __forceinline__ void emit(const PassArgs<V>& a, const Walk& wk, int s, double num,
                                      double den) {
     if (s == wk.mid) {
-        a.part[wk.head] = make_double2(num, den);
+        a.part[wk.head] = make_part(V(0), num, den);
         if constexpr (P1 && sizeof(V) == 4) wave_slots(a)[0] = make_double2(num, den);
     } else if constexpr (P1)
         a.y[s] = coordinate<V>(num, den, a.lambda);
     else
-        a.part[s] = make_double2(num, den);
+        a.part[s] = make_part(V(0), num, den);
 }
 
 // One window [elo, we) of a wave's chunk: up to 64 lanes of kE entries, lane l
@@ -652,7 +659,7 @@ __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>&
         if (lane == 0) {
             if (flags & kChunkCont) {
                 const int t = wk.sb == wk.mid ? 0 : 1;
-                a.part[wk.head + t] = make_double2(wk.cn, wk.cd);
+                a.part[wk.head + t] = make_part(V(0), wk.cn, wk.cd);
                 if constexpr (P1 && sizeof(V) == 4) wave_slots(a)[t] = make_double2(wk.cn, wk.cd);
             } else
                 emit<P1, V>(a, wk, wk.sb, wk.cn, wk.cd);
@@ -815,9 +822,9 @@ __global__ __launch_bounds__(256) void ccd_combine(CombineArgs<V> c) {
     const int e = c.src_ptr[i + 1];
     double num = 0.0, den = 0.0;
     for (int k = b + l; k < e; k += L) {
-        const double2 pv = c.part[c.srcs[k]];
-        num += pv.x;
-        den += pv.y;
+        const part_t<V> pv = c.part[c.srcs[k]];
+        num += (double)pv.x;
+        den += (double)pv.y;
     }
     if constexpr (L == 16) {
         num = row16_sum(num);
@@ -957,7 +964,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     a.q = q;
     a.qq = qq;
     a.y = y;
-    a.part = L.part;
+    a.part = static_cast<part_t<V>*>(L.part);
     a.sse_part = sse_part;
     a.rows = (int32_t)L.rows;
     a.cols = (int32_t)L.cols;
@@ -1019,7 +1026,7 @@ hipError_t launch_combine(const Layout& L, V* y, V* yseg, double lambda, hipStre
     c.srcs = L.srcs;
     c.seg_ptr = L.row_seg_ptr;
     c.segs = L.row_segs;
-    c.part = L.part;
+    c.part = static_cast<const part_t<V>*>(L.part);
     c.y = y;
     c.yseg = yseg;
     c.n = L.ncomb;
