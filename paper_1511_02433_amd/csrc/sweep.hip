@@ -500,8 +500,8 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
         for (int k = 0; k < kE; ++k) fetch(k, col_of<IDX16, V>(cur, k));
         __builtin_amdgcn_sched_barrier(0);
     }
-    // Data of the window after next, before anything waits on this one (a harmless
-    // reload of b past the chunk's end).
+    // Data of the window after next, before anything waits on this one (past the
+    // chunk's end, a reload of lane 0's part of block b that nothing reads).
     {
         const int32_t b2 = we + kWin;
         const bool more = b2 < wk.c1;
