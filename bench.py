@@ -45,9 +45,12 @@ def kernel_symbol(kind: int, info: dict, layout: int) -> str:
     staged = gather in (2, 3)  # tiled, or hot (leading columns staged)
     idx16 = gather == 2 or (gather == 1 and info[f"{pre}_tile_width"] < 32768)
     p1 = info[f"{pre}_tiles"] == 1
+    cache = info.get(f"{pre}_cache", 1) - 1  # 0 streaming, 1 write-back stores, 2 cached
+    if kind == 1 and cache == 1:
+        cache = 0  # the plain pass stores no residual: the streaming kernel
     name = KERNEL_NAMES[kind]
     b = lambda x: "true" if x else "false"
-    return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}, {v}>(ccdk::PassArgs<{v}>)"
+    return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}, {cache}, {v}>(ccdk::PassArgs<{v}>)"
 
 
 def log(msg):
@@ -123,7 +126,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
-    ap.add_argument("--event-every", type=int, default=4,
+    ap.add_argument("--event-every", type=int, default=3,
                     help="bracket every n-th launch of the dominant kernel with HIP events")
     ap.add_argument("--algorithm", default="ccdpp", choices=["ccdpp", "ccd"],
                     help="ccdpp: Algorithm 3 (the headline); ccd: element-wise CCD, Algorithm 2")

@@ -106,7 +106,18 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 paper's float version, Section 8); 1 float64 throughout
  *                 (its double version).  Partial sums across windows and the
  *                 coordinate division are float64 in both.
- * Results differ between layouts only by floating-point summation order.
+ *   cache       : how the passes access the copy's residual: 0 automatic;
+ *                 1 streaming (non-temporal loads and stores); 2 streaming
+ *                 loads and write-back stores of the updated residual;
+ *                 3 cached loads and write-back stores.  2 and 3 need a
+ *                 copy staged in LDS (gather_mode 2) with precision 0, else
+ *                 create fails with EINVAL.  Automatic: 3 on both copies
+ *                 when their residual streams (values and indices) total at
+ *                 most 160 MB, so that they stay in the memory-side cache;
+ *                 otherwise 2 on the first copy staged with one tile, 1 on
+ *                 the other.
+ * Results differ between layouts only by floating-point summation order; the
+ * cache policy does not change them.
  */
 typedef struct ccdpp_options {
     int32_t gather_mode[2];
@@ -114,6 +125,7 @@ typedef struct ccdpp_options {
     int32_t workgroups;
     int32_t seg_weight;
     int32_t precision;
+    int32_t cache[2];
 } ccdpp_options_t;
 
 /* ccdpp_create with explicit layout options (opts may be NULL). */
@@ -230,7 +242,9 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   [15] device bytes held, [16] bytes per value (4: float, 8: double),
  *   [17] user-major rows that the workgroups of a pass finish themselves (cut
  *   between the waves of one workgroup), [18] rows the combine kernel finishes
- *   after each pass, [19..20] the same two for the item-major copy.
+ *   after each pass, [19..20] the same two for the item-major copy,
+ *   [21..22] the cache policy of the user-major and item-major copies
+ *   (numbered as ccdpp_options_t.cache: 1, 2 or 3).
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

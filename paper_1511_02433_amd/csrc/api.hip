@@ -26,6 +26,10 @@ thread_local std::string g_create_error;
 
 constexpr int64_t kMaxDim = int64_t(1) << 30;
 constexpr int64_t kMaxNnz = INT32_MAX;
+// Residual streams (values and indices of both copies) up to this size stay in
+// MI355X's 256 MB memory-side cache from one pass to the next when the passes
+// use cached accesses.
+constexpr int64_t kCachedStreamBytes = int64_t(160) << 20;
 constexpr int32_t kReduceParts = 1024;
 
 struct ProfEvent {
@@ -660,6 +664,43 @@ int spread_factors(ccdpp* h) {
     });
 }
 
+// The cache policy of each copy's residual stream (float, tiled copies; the
+// others always stream).  Measured on MI355X:
+// - when both streams fit in the memory-side cache (10M ratings: 123 MB), cached
+//   loads and stores keep them there between passes: 7% less time per outer
+//   iteration than streaming;
+// - when they do not (100M ratings: 1.23 GB), cached accesses are 13% slower,
+//   but write-back R-hat stores on one tiled copy with P == 1 make its first pass
+//   of each feature 13% faster for a 6% slower next pass over that copy (1.2% per
+//   outer iteration); on both copies together the gains cancel.
+int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
+    using namespace ccdk;
+    const int64_t vb = h->dbl ? 8 : 4;
+    int64_t stream = 0;
+    for (const Layout& L : h->L) stream += L.npad * (vb + (L.idx16 ? 2 : 4));
+    bool stores_given = false;
+    for (int li = 0; li < 2; ++li) {
+        Layout& L = h->L[li];
+        const bool eligible = !h->dbl && L.gather == kGatherLds;
+        const int forced = opt ? opt->cache[li] : 0;
+        if (forced > 1 && !eligible)
+            return fail(h, CCDPP_EINVAL, "cache policy %d needs a tiled float copy", forced);
+        if (forced > 0) {
+            L.cache = forced - 1;
+        } else if (!eligible) {
+            L.cache = kCacheStream;
+        } else if (stream <= kCachedStreamBytes) {
+            L.cache = kCacheAll;
+        } else if (L.P == 1 && !stores_given) {
+            L.cache = kCacheStores;
+            stores_given = true;
+        } else {
+            L.cache = kCacheStream;
+        }
+    }
+    return CCDPP_OK;
+}
+
 int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float* val,
                   uint64_t seed, const ccdpp_options_t* opt) {
     using namespace ccdk;
@@ -736,6 +777,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, launch_compose(pos1, e01, N, h->map01, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
+    RCK(choose_cache(h, opt));
     h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid) * kWaves, kReduceParts);
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
@@ -923,6 +965,8 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
             if (opts->tile_width[i] < 0) return fail(nullptr, CCDPP_EINVAL, "tile_width < 0");
             if (opts->gather_mode[i] == ccdk::kGatherHot && opts->tile_width[i] % 32 != 0)
                 return fail(nullptr, CCDPP_EINVAL, "a hot tile_width must be a multiple of 32");
+            if (opts->cache[i] < 0 || opts->cache[i] > 3)
+                return fail(nullptr, CCDPP_EINVAL, "cache must be 0, 1, 2 or 3");
         }
         if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
         if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
@@ -1436,13 +1480,13 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     auto width = [](const ccdk::Layout& L) -> int64_t {
         return L.gather == ccdk::kGatherHot ? L.hot : L.T;
     };
-    const int64_t v[21] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[23] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
                            h->dbl ? 8 : 4, h->L[0].ncut, h->L[0].ncomb, h->L[1].ncut,
-                           h->L[1].ncomb};
-    int32_t w = std::min<int32_t>(len, 21);
+                           h->L[1].ncomb, h->L[0].cache + 1, h->L[1].cache + 1};
+    int32_t w = std::min<int32_t>(len, 23);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

@@ -212,6 +212,17 @@ struct CombineArgs {
 };
 
 // One compressed copy of the residual plus its schedule.
+// How the passes access a copy's residual stream.  Streaming (non-temporal) loads
+// and stores keep a copy that is read once per pass from displacing everything
+// else; a copy small enough to stay in the memory-side cache between passes
+// gains from ordinary cached accesses.  The write-back policies exist for tiled
+// float copies only.
+enum CachePolicy : int32_t {
+    kCacheStream = 0,  // non-temporal loads and stores
+    kCacheStores = 1,  // non-temporal loads, write-back R-hat stores
+    kCacheAll = 2,     // cached loads and write-back stores
+};
+
 struct Layout {
     int64_t rows = 0, cols = 0, nnz = 0;
     int64_t npad = 0;                // entries including alignment padding
@@ -223,6 +234,7 @@ struct Layout {
     uint32_t swz_lim = 0;            // indices below it are swizzled LDS positions: all of
                                      // them (tiled), the hot width (hot), none (global)
     bool idx16 = false;
+    int32_t cache = kCacheStream;    // CachePolicy of the passes over this copy
     void* idx = nullptr;             // [npad + kEntryPad]
     void* val = nullptr;             // [npad + kEntryPad] of the handle's value type
     int64_t* seg_start = nullptr;    // [S + 1], in padded positions

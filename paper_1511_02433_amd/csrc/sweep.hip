@@ -338,27 +338,43 @@ struct Win {
     V pr, ppr;
 };
 
+// Loads and stores of the residual stream under a copy's cache policy.
+template <int CA, class T>
+__device__ __forceinline__ T load_res(const T* p) {
+    if constexpr (CA == kCacheAll)
+        return *p;
+    else
+        return __builtin_nontemporal_load(p);
+}
+template <int CA, class T>
+__device__ __forceinline__ void store_res(T v, T* p) {
+    if constexpr (CA == kCacheStream)
+        __builtin_nontemporal_store(v, p);
+    else
+        *p = v;
+}
+
 // Data loads of the window block at b (a multiple of kWin): lane l's values from
 // the two halves of the block (val_slot order), its indices in entry order.
 // Chunks start and end at multiples of kWin, so every block a chunk reads lies
 // whole inside the arrays.  A window past the chunk's end (own == false) rereads
 // lane 0's part of block b on every lane: one line, never used.  Positions fit
-// 31 bits (the layout build checks), so they are 32-bit here.
-template <bool IDX16, class V>
+// 31 bits (the layout build checks), so they are 32-bit here.  CA: the copy's
+// cache policy (streaming loads, unless the copy stays cached).
+template <bool IDX16, int CA, class V>
 __device__ __forceinline__ void load_data(const PassArgs<V>& a, int32_t b, bool own, uint32_t le,
                                           Win<V>& w) {
     using VV = typename Vec16<V>::type;
     const uint32_t lo = own ? le : 0u;
     const VV* vp = reinterpret_cast<const VV*>(a.val + b) + (int)(lo / kE);
 #pragma unroll
-    for (int q = 0; q < kE / Win<V>::E; ++q) w.vv[q] = __builtin_nontemporal_load(vp + 64 * q);
+    for (int q = 0; q < kE / Win<V>::E; ++q) w.vv[q] = load_res<CA>(vp + 64 * q);
     if constexpr (IDX16) {
-        w.c0 = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + b + lo));
+        w.c0 = load_res<CA>(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + b + lo));
     } else {
         const u32x4* ip = reinterpret_cast<const u32x4*>(static_cast<const int32_t*>(a.idx) + b + lo);
-        w.c0 = __builtin_nontemporal_load(ip);
-        w.c1 = __builtin_nontemporal_load(ip + 1);
+        w.c0 = load_res<CA>(ip);
+        w.c1 = load_res<CA>(ip + 1);
     }
 }
 // Row scalars of segments sb .. sb + 63, one per lane.
@@ -464,7 +480,7 @@ __device__ __forceinline__ void emit(const PassArgs<V>& a, const Walk& wk, int s
 // gives every segment's window sum at its last lane, and the lane that starts
 // the next segment emits it.  The data of the window after next is requested
 // first, so two windows' loads are in flight while this one is reduced.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+template <int MODE, bool STAGED, bool IDX16, bool P1, int CA, bool XQ, class V>
 __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx, Walk& wk,
                                        const Win<V>& cur, Win<V>& nxt, Win<V>& nn, int lane,
                                        uint32_t le) {
@@ -505,7 +521,7 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     {
         const int32_t b2 = we + kWin;
         const bool more = b2 < wk.c1;
-        load_data<IDX16, V>(a, more ? b2 : b, more, le, nn);
+        load_data<IDX16, CA, V>(a, more ? b2 : b, more, le, nn);
     }
     const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
     const bool lv = lane < nl;
@@ -574,7 +590,7 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
                 VV w;
 #pragma unroll
                 for (int e = 0; e < E; ++e) w[e] = r[q * E + e];
-                __builtin_nontemporal_store(w, wp + 64 * q);
+                store_res<CA>(w, wp + 64 * q);
             }
         }
     }
@@ -626,18 +642,18 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
 // with the staging of the tile.  s0 is the segment holding entry
 // c0; it began in an earlier chunk when the chunk's first lane does not start it
 // (flag kChunkMid).
-template <int MODE, bool IDX16, class V>
+template <int MODE, bool IDX16, int CA, class V>
 __device__ __forceinline__ void begin_chunk(const PassArgs<V>& a, int32_t c0, int32_t c1, int s0,
                                             int flags, int lane, Win<V>& wa, Win<V>& wb) {
     const uint32_t le = (uint32_t)lane * kE;
-    load_data<IDX16, V>(a, c0, true, le, wa);
+    load_data<IDX16, CA, V>(a, c0, true, le, wa);
     load_slots<MODE, V>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
     const bool more = c0 + kWin < c1;
-    load_data<IDX16, V>(a, more ? c0 + kWin : c0, more, le, wb);
+    load_data<IDX16, CA, V>(a, more ? c0 + kWin : c0, more, le, wb);
 }
 
 // wa and wb hold the requests of begin_chunk.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+template <int MODE, bool STAGED, bool IDX16, bool P1, int CA, bool XQ, class V>
 __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>& gx, int32_t c0,
                                           int32_t c1, int s0, int flags, int gc, int lane,
                                           Win<V>& wa, Win<V>& wb, double& sse) {
@@ -646,11 +662,11 @@ __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>&
     Walk wk{c0, c1, mid ? s0 : s0 - 1, mid, 0.0, 0.0, sse, mid ? s0 : -1, a.nseg + 2 * gc};
     Win<V> wc;
     while (true) {
-        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wa, wb, wc, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wa, wb, wc, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wb, wc, wa, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wb, wc, wa, lane, le);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, wk, wc, wa, wb, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wc, wa, wb, lane, le);
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
@@ -671,7 +687,7 @@ __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>&
 // One pass: the workgroup's pieces in order, each staging its tile (when it
 // differs from the one staged) and then giving every wave its chunk.  XQ: the
 // update gathers the same vector as the add-back (x == q), read once per entry.
-template <int MODE, bool STAGED, bool IDX16, bool P1, bool XQ, class V>
+template <int MODE, bool STAGED, bool IDX16, bool P1, int CA, bool XQ, class V>
 __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
     using N = Needs<MODE>;
     V* lds = reinterpret_cast<V*>(lds_raw);
@@ -726,7 +742,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
         // The chunk's first windows are requested before the staging, which they do
         // not depend on.
         Win<V> wa, wb;
-        if (c0 < c1) begin_chunk<MODE, IDX16, V>(a, c0, c1, s0, flags, lane, wa, wb);
+        if (c0 < c1) begin_chunk<MODE, IDX16, CA, V>(a, c0, c1, s0, flags, lane, wa, wb);
         if constexpr (STAGED) {
             const int tile = a.piece_tile[pc];
             if (tile != staged) {
@@ -737,7 +753,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
             }
         }
         if (c0 < c1)
-            run_chunk<MODE, STAGED, IDX16, P1, XQ, V>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
+            run_chunk<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -768,28 +784,28 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
 
 // Distinct kernel names per pass kind, so that profiles separate them.  The
 // template arguments select LDS staging, the index width, whether segments are
-// rows (P == 1) and the value type.
-template <bool STAGED, bool IDX16, bool P1, class V>
+// rows (P == 1), the copy's cache policy and the value type.
+template <bool STAGED, bool IDX16, bool P1, int CA, class V>
 __global__ __launch_bounds__(kWG) void ccd_pass(PassArgs<V> a) {
-    pass_main<kModePlain, STAGED, IDX16, P1, false, V>(a);
+    pass_main<kModePlain, STAGED, IDX16, P1, CA, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1, class V>
+template <bool STAGED, bool IDX16, bool P1, int CA, class V>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused_first(PassArgs<V> a) {
     if (a.x_is_q)
-        pass_main<kModeAdd, STAGED, IDX16, P1, true, V>(a);
+        pass_main<kModeAdd, STAGED, IDX16, P1, CA, true, V>(a);
     else
-        pass_main<kModeAdd, STAGED, IDX16, P1, false, V>(a);
+        pass_main<kModeAdd, STAGED, IDX16, P1, CA, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1, class V>
+template <bool STAGED, bool IDX16, bool P1, int CA, class V>
 __global__ __launch_bounds__(kWG) void ccd_pass_fused(PassArgs<V> a) {
     if (a.x_is_q)
-        pass_main<kModeSubAdd, STAGED, IDX16, P1, true, V>(a);
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, CA, true, V>(a);
     else
-        pass_main<kModeSubAdd, STAGED, IDX16, P1, false, V>(a);
+        pass_main<kModeSubAdd, STAGED, IDX16, P1, CA, false, V>(a);
 }
-template <bool STAGED, bool IDX16, bool P1, class V>
+template <bool STAGED, bool IDX16, bool P1, int CA, class V>
 __global__ __launch_bounds__(kWG) void ccd_flush(PassArgs<V> a) {
-    pass_main<kModeFlush, STAGED, IDX16, P1, false, V>(a);
+    pass_main<kModeFlush, STAGED, IDX16, P1, CA, false, V>(a);
 }
 
 // x summed over the 16 lanes of a DPP row; every lane of the row gets the same
@@ -889,10 +905,14 @@ int staged_vectors(PassMode mode, bool x_is_q) {
 }
 
 namespace {
-template <bool S, bool I, bool P1, class V>
+// The plain pass stores no residual: with write-back stores it is the streaming kernel.
+constexpr int plain_cache(int ca) { return ca == kCacheStores ? kCacheStream : ca; }
+
+template <bool S, bool I, bool P1, int CA, class V>
 hipError_t raise_lds() {
-    const void* ks[] = {(const void*)ccd_pass<S, I, P1, V>, (const void*)ccd_pass_fused_first<S, I, P1, V>,
-                        (const void*)ccd_pass_fused<S, I, P1, V>, (const void*)ccd_flush<S, I, P1, V>};
+    constexpr int CP = plain_cache(CA);
+    const void* ks[] = {(const void*)ccd_pass<S, I, P1, CP, V>, (const void*)ccd_pass_fused_first<S, I, P1, CA, V>,
+                        (const void*)ccd_pass_fused<S, I, P1, CA, V>, (const void*)ccd_flush<S, I, P1, CA, V>};
     for (const void* k : ks) {
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
         if (e != hipSuccess) return e;
@@ -900,31 +920,48 @@ hipError_t raise_lds() {
     return hipSuccess;
 }
 
-template <bool S, bool I, bool P1, class V>
+template <bool S, bool I, bool P1, int CA, class V>
 void launch_mode(PassMode mode, dim3 grid, size_t lds, hipStream_t s, const PassArgs<V>& a) {
+    constexpr int CP = plain_cache(CA);
     switch (mode) {
         case kModePlain:
-            hipLaunchKernelGGL((ccd_pass<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass<S, I, P1, CP, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeAdd:
-            hipLaunchKernelGGL((ccd_pass_fused_first<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass_fused_first<S, I, P1, CA, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeSubAdd:
-            hipLaunchKernelGGL((ccd_pass_fused<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_pass_fused<S, I, P1, CA, V>), grid, dim3(kWG), lds, s, a);
             break;
         case kModeFlush:
-            hipLaunchKernelGGL((ccd_flush<S, I, P1, V>), grid, dim3(kWG), lds, s, a);
+            hipLaunchKernelGGL((ccd_flush<S, I, P1, CA, V>), grid, dim3(kWG), lds, s, a);
             break;
     }
 }
 
+// Tiled float copies also come with the write-back policies.
+template <bool P1, class V>
+void launch_tiled(int cache, PassMode mode, dim3 grid, size_t lds, hipStream_t s, const PassArgs<V>& a) {
+    if constexpr (sizeof(V) == 4) {
+        if (cache == kCacheStores) return launch_mode<true, true, P1, kCacheStores, V>(mode, grid, lds, s, a);
+        if (cache == kCacheAll) return launch_mode<true, true, P1, kCacheAll, V>(mode, grid, lds, s, a);
+    }
+    launch_mode<true, true, P1, kCacheStream, V>(mode, grid, lds, s, a);
+}
+
 template <class V>
 hipError_t raise_lds_all() {
-    hipError_t e = raise_lds<true, true, true, V>();
-    if (e == hipSuccess) e = raise_lds<true, true, false, V>();
-    if (e == hipSuccess) e = raise_lds<true, false, true, V>();
-    if (e == hipSuccess) e = raise_lds<false, true, true, V>();
-    if (e == hipSuccess) e = raise_lds<false, false, true, V>();
+    hipError_t e = raise_lds<true, true, true, kCacheStream, V>();
+    if (e == hipSuccess) e = raise_lds<true, true, false, kCacheStream, V>();
+    if (e == hipSuccess) e = raise_lds<true, false, true, kCacheStream, V>();
+    if (e == hipSuccess) e = raise_lds<false, true, true, kCacheStream, V>();
+    if (e == hipSuccess) e = raise_lds<false, false, true, kCacheStream, V>();
+    if constexpr (sizeof(V) == 4) {
+        if (e == hipSuccess) e = raise_lds<true, true, true, kCacheStores, V>();
+        if (e == hipSuccess) e = raise_lds<true, true, false, kCacheStores, V>();
+        if (e == hipSuccess) e = raise_lds<true, true, true, kCacheAll, V>();
+        if (e == hipSuccess) e = raise_lds<true, true, false, kCacheAll, V>();
+    }
     return e;
 }
 }  // namespace
@@ -946,6 +983,8 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     // gathers and hot layouts have P == 1.
     if (staged ? !L.idx16 : L.P != 1) return hipErrorInvalidValue;
     if (hot && L.idx16) return hipErrorInvalidValue;
+    // Write-back cache policies: tiled float copies only.
+    if (L.cache != kCacheStream && (!staged || sizeof(V) != 4)) return hipErrorInvalidValue;
     PassArgs<V> a{};
     a.idx = L.idx;
     a.val = static_cast<V*>(L.val);
@@ -1003,15 +1042,15 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     const dim3 grid(L.grid);
     if (staged) {
         if (L.P == 1)
-            launch_mode<true, true, true, V>(mode, grid, lds, s, a);
+            launch_tiled<true, V>(L.cache, mode, grid, lds, s, a);
         else
-            launch_mode<true, true, false, V>(mode, grid, lds, s, a);
+            launch_tiled<false, V>(L.cache, mode, grid, lds, s, a);
     } else if (hot) {
-        launch_mode<true, false, true, V>(mode, grid, lds, s, a);
+        launch_mode<true, false, true, kCacheStream, V>(mode, grid, lds, s, a);
     } else if (L.idx16) {
-        launch_mode<false, true, true, V>(mode, grid, lds, s, a);
+        launch_mode<false, true, true, kCacheStream, V>(mode, grid, lds, s, a);
     } else {
-        launch_mode<false, false, true, V>(mode, grid, lds, s, a);
+        launch_mode<false, false, true, kCacheStream, V>(mode, grid, lds, s, a);
     }
     return hipGetLastError();
 }

@@ -57,6 +57,8 @@ def test_create_rejects_bad_arguments_on_the_host(kw, msg):
     (dict(gather_mode=(3, 0), tile_width=(100, 0)), "multiple of 32"),
     (dict(tile_width=(0, -1)), "tile_width"),
     (dict(precision=2), "precision"),
+    (dict(cache=(4, 0)), "cache"),
+    (dict(cache=(0, -1)), "cache"),
 ])
 def test_create_rejects_bad_options(kw, msg):
     _lib_or_skip()

@@ -218,6 +218,58 @@ def test_layout_strategies_match_oracle(name):
             assert info[f"{side}_rows_finished_in_pass"] > 0 and info[f"{side}_rows_combined"] == 0
 
 
+@pytest.mark.parametrize("tiles", ["one", "several"])
+def test_cache_policies_give_identical_results(tiles):
+    # The cache policy only changes how the residual stream is loaded and stored, so
+    # every policy gives bitwise the same factors and residual.  "one": one tile per
+    # side (the kernels for P == 1); "several": several tiles per side.
+    from paper_1511_02433_amd.ccdpp import CCDPPError, CCDPP_EINVAL, make_options
+    lens = [850, 700, 300, 40] + list(np.random.default_rng(31).integers(0, 80, 1496))
+    row, col, val, H0 = synth.lengths_problem(lens, 900, 4, seed=32)
+    tw = (0, 0) if tiles == "one" else (192, 128)
+    print(f"case: cache policies, {tiles} tile(s) per side", flush=True)
+    ref = None
+    for cache in [(1, 1), (0, 0), (2, 2), (3, 3), (2, 1), (1, 3), (3, 2)]:
+        g = CCDPP(1500, 900, 4, 0.1, row, col, val,
+                  opts=make_options(gather_mode=(2, 2), tile_width=tw, cache=cache))
+        info = g.info()
+        assert (info["u_tiles"] == 1) == (tiles == "one")
+        want = cache if cache != (0, 0) else (3, 3)  # automatic: the streams fit the cache
+        assert (info["u_cache"], info["v_cache"]) == want
+        g.set_factors(np.zeros((1500, 4), np.float32), H0)
+        g.run(1, 2)
+        first = g.factors()
+        g.run(1, 2)
+        out = first + g.factors() + (g.residual(),)
+        assert g.check_consistency() == 0
+        rmse = g.train_rmse()
+        g.close()
+        if ref is None:
+            ref = out
+            o = Oracle(1500, 900, 4, 0.1, row, col, val, H0)
+            o.run(1, 2)
+            Wo, Ho = o.factors()
+            assert colscaled_max_rel_err(first[0], Wo) <= W_TOL
+            assert colscaled_max_rel_err(first[1], Ho) <= W_TOL
+            o.run(1, 2)
+            assert abs(rmse - o.train_rmse()) <= RMSE_TOL
+        else:
+            for a, b in zip(ref, out):
+                assert np.array_equal(a, b), f"cache {cache} differs"
+    # Write-back policies need a tiled float copy.
+    for kw in (dict(gather_mode=(1, 1), cache=(3, 1)), dict(gather_mode=(3, 3), cache=(1, 2)),
+               dict(precision=1, cache=(2, 2))):
+        with pytest.raises(CCDPPError) as ei:
+            CCDPP(1500, 900, 4, 0.1, row, col, val, opts=make_options(**kw))
+        assert ei.value.code == CCDPP_EINVAL and "cache policy" in str(ei.value)
+    # Automatic choice elsewhere: copies that are not tiled, and double precision, stream.
+    for kw in (dict(gather_mode=(1, 3)), dict(precision=1)):
+        g = CCDPP(1500, 900, 4, 0.1, row, col, val, opts=make_options(**kw))
+        info = g.info()
+        assert (info["u_cache"], info["v_cache"]) == (1, 1)
+        g.close()
+
+
 @pytest.mark.parametrize("layout", ["auto", "global", "hot"])
 @pytest.mark.parametrize("transpose", [False, True])
 def test_short_segments_fill_windows(layout, transpose):
