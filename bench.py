@@ -32,7 +32,7 @@ KERNEL_NAMES = {0: "ccd_pass_fused", 1: "ccd_pass", 2: "ccd_combine", 3: "ccd_co
 LAYOUT_NAMES = {0: "rows", 1: "cols"}
 
 
-def kernel_symbol(kind: int, info: dict, layout: int) -> str:
+def kernel_symbol(kind: int, info: dict, layout: int, wb_stores: bool = True) -> str:
     """The kernel's name as a trace shows it (the sweep kernels are templated on
     LDS staging, 16-bit indices, P == 1 and the value type)."""
     v = "double" if info.get("value_bytes", 4) == 8 else "float"
@@ -46,8 +46,10 @@ def kernel_symbol(kind: int, info: dict, layout: int) -> str:
     idx16 = gather == 2 or (gather == 1 and info[f"{pre}_tile_width"] < 32768)
     p1 = info[f"{pre}_tiles"] == 1
     cache = info.get(f"{pre}_cache", 1) - 1  # 0 streaming, 1 write-back stores, 2 cached
-    if kind == 1 and cache == 1:
-        cache = 0  # the plain pass stores no residual: the streaming kernel
+    if cache == 1 and (kind == 1 or not wb_stores):
+        # The plain pass stores no residual, and automatic write-back stores apply to
+        # CCD++ with two or more inner iterations only: the streaming kernel.
+        cache = 0
     name = KERNEL_NAMES[kind]
     b = lambda x: "true" if x else "false"
     return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}, {cache}, {v}>(ccdk::PassArgs<{v}>)"
@@ -174,6 +176,8 @@ def main():
     info = g.info()
     log(f"device build {info['build_us'] / 1e3:.1f} ms; schedule {info}")
 
+    wb_stores = args.algorithm == "ccdpp" and inner >= 2
+
     def read_kernels():
         """Per-kernel and per-(kernel, residual copy) timings collected since profile()."""
         kinds, per_layout = {}, {}
@@ -186,7 +190,8 @@ def main():
                 n2, t2, b2 = g.profile_read(kind, lay)
                 if n2:
                     per_layout[f"{name}/{lname}"] = {
-                        "kernel": kernel_symbol(kind, info, lay), "kind": kind, "layout": lay,
+                        "kernel": kernel_symbol(kind, info, lay, wb_stores), "kind": kind,
+                        "layout": lay,
                         "launches": n2, "mean_us": round(t2 / n2 * 1e3, 3),
                         "total_ms": round(t2, 4), "algo_bytes_per_launch": b2 / n2,
                         "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}

@@ -115,7 +115,9 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 when their residual streams (values and indices) total at
  *                 most 160 MB, so that they stay in the memory-side cache;
  *                 otherwise 2 on the first copy staged with one tile, 1 on
- *                 the other.
+ *                 the other, where an automatic 2 applies to ccdpp_run and
+ *                 ccdpp_run_until with inner_iters >= 2 only (elsewhere the
+ *                 copy streams).
  * Results differ between layouts only by floating-point summation order; the
  * cache policy does not change them.
  */

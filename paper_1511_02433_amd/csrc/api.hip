@@ -85,6 +85,8 @@ struct ccdpp {
     bool prof = false;
     int32_t prof_kind = -1, prof_layout = -1;  // restrict timing to one kind / copy (-1: all)
     int32_t prof_every = 1;        // time every n-th launch that the selection matches
+    bool cache_auto[2] = {true, true};  // the copy's cache policy was chosen automatically
+    bool wb_stores = false;        // the running sweep takes automatic write-back stores
     int64_t prof_seen = 0;         // matching launches since the selection was set
     std::vector<ProfEvent> prof_pending;
     std::vector<hipEvent_t> event_pool;
@@ -683,6 +685,7 @@ int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
         Layout& L = h->L[li];
         const bool eligible = !h->dbl && L.gather == kGatherLds;
         const int forced = opt ? opt->cache[li] : 0;
+        h->cache_auto[li] = forced == 0;
         if (forced > 1 && !eligible)
             return fail(h, CCDPP_EINVAL, "cache policy %d needs a tiled float copy", forced);
         if (forced > 0) {
@@ -923,13 +926,22 @@ template <class V>
 int pass(ccdpp* h, int li, ccdk::PassMode mode, const V* x, int32_t pcol, int32_t ppcol,
          const V* q, const V* qq, V* y, int32_t commit, int gathered) {
     const Layout& L = h->L[li];
+    // Automatic write-back stores pay off only where a plain pass follows the first
+    // pass over the copy (CCD++ with inner_iters >= 2); elsewhere the copy streams.
+    Layout Ls;
+    const Layout* Lp = &L;
+    if (L.cache == ccdk::kCacheStores && h->cache_auto[li] && !h->wb_stores) {
+        Ls = L;
+        Ls.cache = ccdk::kCacheStream;
+        Lp = &Ls;
+    }
     const int kind = mode == ccdk::kModePlain ? CCDPP_K_PASS
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
                                                 : CCDPP_K_PASS_FUSED;
     const double vb = sizeof(V);
     {
         Timed tm(h, kind, li, pass_bytes(L, mode, gathered, vb));
-        HIPCK(h, ccdk::launch_pass<V>(L, mode, x, seg_col<V>(h, li, pcol), seg_col<V>(h, li, ppcol),
+        HIPCK(h, ccdk::launch_pass<V>(*Lp, mode, x, seg_col<V>(h, li, pcol), seg_col<V>(h, li, ppcol),
                                       q, qq, y, h->lambda, h->sse_part, h->stream));
         tm.done();
     }
@@ -1035,6 +1047,7 @@ template <class V>
 int ccd_impl(ccdpp* h, int32_t outer) {
     using namespace ccdk;
     const int64_t m = h->m, n = h->n;
+    h->wb_stores = false;
     if (outer > 0 && !h->slot01) {
         // Slot-to-slot maps between the copies, for the residual refresh after each phase.
         int32_t *s01, *s10;
@@ -1093,6 +1106,7 @@ template <class V>
 int run_impl(ccdpp* h, int32_t outer, int32_t inner) {
     using namespace ccdk;
     const int64_t m = h->m, n = h->n;
+    h->wb_stores = inner >= 2;
     V* const W = as<V>(h->W);
     V* const H = as<V>(h->H);
     V* const u = as<V>(h->u);

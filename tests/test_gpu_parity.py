@@ -243,6 +243,10 @@ def test_cache_policies_give_identical_results(tiles):
         out = first + g.factors() + (g.residual(),)
         assert g.check_consistency() == 0
         rmse = g.train_rmse()
+        g.run(1, 1)        # one inner iteration: automatic write-back stores off
+        g.ccd_run(1)       # element-wise CCD on the same copies
+        out += g.factors() + (g.residual(),)
+        assert g.check_consistency() == 0
         g.close()
         if ref is None:
             ref = out
