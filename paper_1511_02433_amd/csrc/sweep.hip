@@ -836,11 +836,30 @@ __global__ __launch_bounds__(256) void ccd_combine(CombineArgs<V> c) {
     if (i >= c.n) return;  // whole rows of lanes leave together
     const int b = c.src_ptr[i];
     const int e = c.src_ptr[i + 1];
+    int sb = 0, se = 0;
+    if (c.yseg) {  // requested now, used after the sums
+        sb = c.seg_ptr[i];
+        se = c.seg_ptr[i + 1];
+    }
+    // Four of the lane's slots at a time: their list entries, then their partials, so
+    // that a row of many partials waits for two loads per four slots, not per slot.
+    // Positions past the row's end reload its last slot and are not added; the sums
+    // still run over the lane's slots in entry order.
+    constexpr int U = 4;
     double num = 0.0, den = 0.0;
-    for (int k = b + l; k < e; k += L) {
-        const part_t<V> pv = c.part[c.srcs[k]];
-        num += (double)pv.x;
-        den += (double)pv.y;
+    for (int k0 = b + l; k0 < e; k0 += U * L) {
+        int32_t sl[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) sl[u] = c.srcs[min(k0 + u * L, e - 1)];
+        part_t<V> pv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) pv[u] = c.part[sl[u]];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (k0 + u * L < e) {
+                num += (double)pv[u].x;
+                den += (double)pv[u].y;
+            }
     }
     if constexpr (L == 16) {
         num = row16_sum(num);
@@ -852,7 +871,7 @@ __global__ __launch_bounds__(256) void ccd_combine(CombineArgs<V> c) {
     const V yr = coordinate<V>(num, den, c.lambda);
     if (l == 0) c.y[c.ids ? c.ids[i] : i] = yr;
     if (c.yseg)
-        for (int k = c.seg_ptr[i] + l; k < c.seg_ptr[i + 1]; k += L) c.yseg[c.segs[k]] = yr;
+        for (int k = sb + l; k < se; k += L) c.yseg[c.segs[k]] = yr;
 }
 
 template <class V>
