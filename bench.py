@@ -128,7 +128,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
-    ap.add_argument("--event-every", type=int, default=3,
+    ap.add_argument("--event-every", type=int, default=5,
                     help="bracket every n-th launch of the dominant kernel with HIP events")
     ap.add_argument("--algorithm", default="ccdpp", choices=["ccdpp", "ccd"],
                     help="ccdpp: Algorithm 3 (the headline); ccd: element-wise CCD, Algorithm 2")
