@@ -35,9 +35,20 @@ def _say(msg):
     print(f"[fullsize] {msg}", flush=True)
 
 
+# The automatic cache policy of the two copies (1 streaming, 2 write-back residual
+# stores, 3 cached): medium's residual streams fit in the memory-side cache; large
+# takes write-back stores on its one-tile user-major copy; the very large matrix has
+# no one-tile copy.
+EXPECT_CACHE = {"medium": (3, 3), "large": (2, 1), "vlarge": (1, 1)}
+
+
 def _gpu(ds, k):
     w = ds.workload
     g = CCDPP(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val)
+    info = g.info()
+    _say(f"layout {({key: v for key, v in info.items() if key.startswith(('u_', 'v_'))})}")
+    if w.name in EXPECT_CACHE:
+        assert (info["u_cache"], info["v_cache"]) == EXPECT_CACHE[w.name]
     g.set_factors(np.zeros((w.m, k), np.float32), ds.h0(k))
     return g
 
