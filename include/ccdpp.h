@@ -118,8 +118,14 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 the other, where an automatic 2 applies to ccdpp_run and
  *                 ccdpp_run_until with inner_iters >= 2 only (elsewhere the
  *                 copy streams).
+ *   index_coding: 0 automatic: in a copy staged in LDS with 16-bit indices
+ *                 (gather_mode 2 and fewer than 32,768 tile columns) whose
+ *                 cache policy is not 3, every window of 512 entries whose
+ *                 lanes' sorted columns climb by at most 2047 from one entry
+ *                 to the next stores its indices delta-coded, 12 bytes per 8
+ *                 entries instead of 16; 1 plain 16-bit indices everywhere.
  * Results differ between layouts only by floating-point summation order; the
- * cache policy does not change them.
+ * cache policy and the index coding do not change them.
  */
 typedef struct ccdpp_options {
     int32_t gather_mode[2];
@@ -128,6 +134,7 @@ typedef struct ccdpp_options {
     int32_t seg_weight;
     int32_t precision;
     int32_t cache[2];
+    int32_t index_coding[2];
 } ccdpp_options_t;
 
 /* ccdpp_create with explicit layout options (opts may be NULL). */
@@ -246,7 +253,9 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   between the waves of one workgroup), [18] rows the combine kernel finishes
  *   after each pass, [19..20] the same two for the item-major copy,
  *   [21..22] the cache policy of the user-major and item-major copies
- *   (numbered as ccdpp_options_t.cache: 1, 2 or 3).
+ *   (numbered as ccdpp_options_t.cache: 1, 2 or 3), [23] user-major windows
+ *   (512 entries) with delta-coded indices, [24] its windows, [25..26] the
+ *   same two for the item-major copy.
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

@@ -26,14 +26,16 @@ KERNEL_KINDS = {K_PASS_FUSED: "ccd_pass_fused*", K_PASS: "ccd_pass", K_COMBINE: 
 class Options(ctypes.Structure):
     """ccdpp_options_t: layout knobs (0 = automatic).  Index 0 is the user-major copy,
     1 the item-major copy.  gather_mode: 1 global memory, 2 LDS-staged, 3 hot.
-    cache: 1 streaming, 2 write-back residual stores, 3 cached loads and stores."""
+    cache: 1 streaming, 2 write-back residual stores, 3 cached loads and stores.
+    index_coding: 0 delta-coded windows where they fit, 1 plain 16-bit indices."""
     _fields_ = [("gather_mode", ctypes.c_int32 * 2), ("tile_width", ctypes.c_int32 * 2),
                 ("workgroups", ctypes.c_int32), ("seg_weight", ctypes.c_int32),
-                ("precision", ctypes.c_int32), ("cache", ctypes.c_int32 * 2)]
+                ("precision", ctypes.c_int32), ("cache", ctypes.c_int32 * 2),
+                ("index_coding", ctypes.c_int32 * 2)]
 
 
 def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight=0,
-                 precision=0, cache=(0, 0)) -> Options:
+                 precision=0, cache=(0, 0), index_coding=(0, 0)) -> Options:
     """precision: 0 float32 residual and factors, 1 float64."""
     o = Options()
     o.gather_mode[0], o.gather_mode[1] = gather_mode
@@ -42,6 +44,7 @@ def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight
     o.seg_weight = seg_weight
     o.precision = precision
     o.cache[0], o.cache[1] = cache
+    o.index_coding[0], o.index_coding[1] = index_coding
     return o
 
 
@@ -252,7 +255,7 @@ INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_
                "u_workgroups", "u_segments", "v_gather", "v_tiles", "v_tile_width", "v_workgroups",
                "v_segments", "device_bytes", "value_bytes", "u_rows_finished_in_pass",
                "u_rows_combined", "v_rows_finished_in_pass", "v_rows_combined", "u_cache",
-               "v_cache")
+               "v_cache", "u_delta_windows", "u_windows", "v_delta_windows", "v_windows")
 
 
 def ccdpp_info(h):

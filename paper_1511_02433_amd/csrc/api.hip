@@ -651,6 +651,30 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     return CCDPP_OK;
 }
 
+// Delta-coded index windows (12 index bytes per lane instead of 16 where a whole
+// window allows it) for copies staged in LDS with 16-bit indices whose passes
+// stream the residual.  Measured on MI355X: 3% less time per outer iteration on
+// large (100M ratings), where the passes are bound by HBM; 3% more on medium (10M
+// ratings), whose cached streams leave the decoding exposed.
+int code_windows(ccdpp* h, int side, const ccdpp_options_t* opt) {
+    using namespace ccdk;
+    Layout& L = h->L[side];
+    const int forced = opt ? opt->index_coding[side] : 0;
+    if (forced == 1 || L.gather != kGatherLds || !L.idx16 || L.npad == 0 || L.cache == kCacheAll)
+        return CCDPP_OK;
+    const hipStream_t s = h->stream;
+    const int64_t words = (L.npad / kWin + 63) / 64;
+    HIPCK(h, dalloc(h, &L.dmask, words));
+    HIPCK(h, hipMemsetAsync(L.dmask, 0, (size_t)words * 8, s));
+    HIPCK(h, launch_delta_windows(L.idx, L.npad, L.pad, L.dmask, s));
+    std::vector<uint64_t> bits((size_t)words);
+    HIPCK(h, hipMemcpyAsync(bits.data(), L.dmask, (size_t)words * 8, hipMemcpyDeviceToHost, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    L.ndelta = 0;
+    for (uint64_t b : bits) L.ndelta += __builtin_popcountll(b);
+    return CCDPP_OK;
+}
+
 // Refresh the per-segment copies of W (user-major copy) and H (item-major copy).
 int spread_factors(ccdpp* h) {
     return with_value_type(h, [&](auto z) -> int {
@@ -781,6 +805,8 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, hipStreamSynchronize(s));
     }
     RCK(choose_cache(h, opt));
+    RCK(code_windows(h, 0, opt));
+    RCK(code_windows(h, 1, opt));
     h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid) * kWaves, kReduceParts);
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
@@ -897,11 +923,14 @@ void collect_profile(ccdpp* h) {
 
 // Algorithmic bytes of one pass over layout L (see ccdpp_profile_read): index and
 // value arrays, residual write-back, per-segment row scalars, outputs, and every
-// gathered vector read once.
+// gathered vector read once.  Delta-coded windows hold 1.5 index bytes per entry
+// instead of 2 (counted in proportion to the windows coded).
 double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors, double vb) {
     using namespace ccdk;
     const double nnz = (double)L.nnz, S = (double)L.nseg, cols = (double)L.cols;
-    double b = (L.idx16 ? 2.0 : 4.0) * nnz + vb * nnz;
+    const double nwin = (double)(L.npad / kWin);
+    const double coded = nwin > 0 ? (double)L.ndelta / nwin : 0.0;
+    double b = (L.idx16 ? 2.0 - 0.5 * coded : 4.0) * nnz + vb * nnz;
     if (mode != kModePlain) b += vb * nnz;
     if (mode != kModeFlush) b += L.P == 1 ? vb * S : 2.0 * vb * S;  // coordinate or partial
     if (mode == kModeAdd || mode == kModeSubAdd) b += vb * S;
@@ -979,6 +1008,8 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
                 return fail(nullptr, CCDPP_EINVAL, "a hot tile_width must be a multiple of 32");
             if (opts->cache[i] < 0 || opts->cache[i] > 3)
                 return fail(nullptr, CCDPP_EINVAL, "cache must be 0, 1, 2 or 3");
+            if (opts->index_coding[i] < 0 || opts->index_coding[i] > 1)
+                return fail(nullptr, CCDPP_EINVAL, "index_coding must be 0 or 1");
         }
         if (opts->workgroups < 0) return fail(nullptr, CCDPP_EINVAL, "workgroups < 0");
         if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
@@ -1494,13 +1525,15 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     auto width = [](const ccdk::Layout& L) -> int64_t {
         return L.gather == ccdk::kGatherHot ? L.hot : L.T;
     };
-    const int64_t v[23] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[27] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
                            h->dbl ? 8 : 4, h->L[0].ncut, h->L[0].ncomb, h->L[1].ncut,
-                           h->L[1].ncomb, h->L[0].cache + 1, h->L[1].cache + 1};
-    int32_t w = std::min<int32_t>(len, 23);
+                           h->L[1].ncomb, h->L[0].cache + 1, h->L[1].cache + 1,
+                           h->L[0].ndelta, h->L[0].npad / ccdk::kWin, h->L[1].ndelta,
+                           h->L[1].npad / ccdk::kWin};
+    int32_t w = std::min<int32_t>(len, 27);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

@@ -158,10 +158,65 @@ __global__ void k_factor_out(const V* __restrict__ colmajor, const int32_t* __re
 // in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
 // unpadded layout order) has its value in slot pos[e]; its segment, and from it the
 // row and the tile, are found by binary search.
+// Rewrites, one wave per window, every window whose lanes' valid entries each climb
+// by at most kDeltaMax unswizzled columns into the delta-coded format, and sets its
+// bit.  Valid entries come first in a lane (padding only ends a segment); a lane
+// of padding alone is coded as its first index with one valid entry.  Every lane
+// reads its 16 bytes before the vote, so the window is rewritten in place.
+__global__ __launch_bounds__(kT) void k_delta_windows(uint16_t* __restrict__ idx, int64_t nwin,
+                                                       uint32_t pad, uint64_t* __restrict__ dmask) {
+    const int lane = (int)(threadIdx.x & 63u);
+    const int64_t w = (int64_t)blockIdx.x * (kT / 64) + (threadIdx.x >> 6);
+    if (w >= nwin) return;  // whole waves leave together
+    uint16_t* blk = idx + w * kWin;
+    const uint4 v = *reinterpret_cast<const uint4*>(blk + lane * kE);
+    const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+    uint32_t c[8];
+    for (int k = 0; k < 8; ++k) c[k] = (wd[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+    int cnt = 0;
+    while (cnt < 8 && c[cnt] != pad) ++cnt;
+    bool ok = true;
+    for (int k = cnt; k < 8; ++k) ok = ok && c[k] == pad;  // padding only after the valid entries
+    uint32_t st[7] = {0, 0, 0, 0, 0, 0, 0};
+    if (cnt > 0) {
+        uint32_t prev = lds_swizzle(c[0] & 0x7FFFu);
+        for (int k = 1; k < cnt; ++k) {
+            const uint32_t cur = lds_swizzle(c[k]);
+            ok = ok && cur >= prev && cur - prev <= kDeltaMax;
+            st[k - 1] = (cur - prev) & kDeltaMax;
+            prev = cur;
+        }
+    }
+    if (!__all(ok)) return;
+    const uint32_t last = (uint32_t)(cnt > 0 ? cnt - 1 : 0);
+    uint32_t* words = reinterpret_cast<uint32_t*>(blk);
+    words[3 * lane] = c[0] | (st[0] << 16) | (st[1] << 27);
+    words[3 * lane + 1] = (st[1] >> 5) | (st[2] << 6) | (st[3] << 17) | (st[4] << 28);
+    words[3 * lane + 2] = (st[4] >> 4) | (st[5] << 7) | (st[6] << 18) | (last << 29);
+    if (lane == 0) atomicOr(reinterpret_cast<unsigned long long*>(dmask + (w >> 6)),
+                            1ull << (w & 63));
+}
+
+// Index of entry q as the plain format holds it, from a delta-coded window when
+// its bit is set.
+template <class I>
+__device__ __forceinline__ uint32_t index_at(const I* idx, const uint64_t* dmask, uint32_t pad,
+                                             int64_t q) {
+    const int64_t w = q / kWin;
+    if (dmask && ((dmask[w >> 6] >> (w & 63)) & 1u)) {
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(idx + w * kWin) + 3 * ((q % kWin) / kE);
+        uint32_t c[8];
+        delta_decode(rec[0], rec[1], rec[2], pad, c);
+        return c[q % kE];
+    }
+    return (uint32_t)idx[q];
+}
+
 template <class I, class V>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,
                           int32_t P, int32_t T, uint32_t swz_lim, const I* __restrict__ idx,
+                          const uint64_t* __restrict__ dmask, uint32_t pad,
                           const int32_t* __restrict__ pos, const V* __restrict__ A,
                           const V* __restrict__ W, const V* __restrict__ H, int64_t m,
                           int64_t n, int32_t k, int64_t nnz, V* __restrict__ val) {
@@ -180,7 +235,7 @@ __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
             if (tile_seg[mid] <= lo) plo = mid; else phi = mid;
         }
         const int64_t i = seg_row[lo];
-        const uint32_t c = (uint32_t)idx[q] & IndexBits<I>::mask;
+        const uint32_t c = index_at<I>(idx, dmask, pad, q) & IndexBits<I>::mask;
         const int64_t j = (int64_t)plo * T + (int64_t)(c < swz_lim ? lds_swizzle(c) : c);
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
@@ -380,6 +435,15 @@ hipError_t launch_gather_factor_out(const V* colmajor, const int32_t* old2new, i
     return hipGetLastError();
 }
 
+hipError_t launch_delta_windows(void* idx, int64_t npad, int32_t pad, uint64_t* dmask,
+                                hipStream_t s) {
+    const int64_t nwin = npad / kWin;
+    if (nwin == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_delta_windows, dim3((unsigned)((nwin + kT / 64 - 1) / (kT / 64))), dim3(kT),
+                       0, s, static_cast<uint16_t*>(idx), nwin, (uint32_t)pad, dmask);
+    return hipGetLastError();
+}
+
 template <class V>
 hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const V* A, const V* W,
                                    const V* H, int64_t m, int64_t n, int32_t k, hipStream_t s) {
@@ -387,13 +451,13 @@ hipError_t launch_rebuild_residual(const Layout& L, const int32_t* pos, const V*
     if (L.idx16)
         hipLaunchKernelGGL((k_rebuild<uint16_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz_lim,
-                           static_cast<const uint16_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
-                           static_cast<V*>(L.val));
+                           static_cast<const uint16_t*>(L.idx), L.dmask, (uint32_t)L.pad, pos, A, W,
+                           H, m, n, k, L.nnz, static_cast<V*>(L.val));
     else
         hipLaunchKernelGGL((k_rebuild<int32_t, V>), grid_for(L.nnz), dim3(kT), 0, s, L.seg_start,
                            L.nseg, L.seg_row, L.tile_seg, L.P, L.T, L.swz_lim,
-                           static_cast<const int32_t*>(L.idx), pos, A, W, H, m, n, k, L.nnz,
-                           static_cast<V*>(L.val));
+                           static_cast<const int32_t*>(L.idx), nullptr, (uint32_t)L.pad, pos, A, W,
+                           H, m, n, k, L.nnz, static_cast<V*>(L.val));
     return hipGetLastError();
 }
 

@@ -101,6 +101,35 @@ constexpr int kEntryPad = 64;             // entries of padding after idx and va
 
 __host__ __device__ inline uint32_t lds_swizzle(uint32_t c) { return c ^ ((c >> 5) & 31u); }
 
+// Delta-coded index windows (copies staged in LDS with 16-bit indices).  A window
+// in which every lane's valid entries climb by at most kDeltaMax columns from one
+// to the next keeps its indices in the first 768 of its 1024 index bytes, 12 bytes
+// per lane: lane l's 96-bit record is words 3l, 3l + 1 and 3l + 2, with
+//   bits 0-15   the lane's first index as the plain format holds it (swizzled,
+//               start bit included),
+//   bits 16-92  seven 11-bit steps between its consecutive unswizzled columns,
+//   bits 93-95  the number of valid entries less one (the others are padding).
+// A bit per window (Layout::dmask) marks the windows coded this way.
+constexpr uint32_t kDeltaBits = 11;
+constexpr uint32_t kDeltaMax = (1u << kDeltaBits) - 1u;
+
+// The lane's 8 indices in the plain format, from its record (d0, d1, d2).
+__host__ __device__ inline void delta_decode(uint32_t d0, uint32_t d1, uint32_t d2, uint32_t pad,
+                                             uint32_t out[8]) {
+    const uint32_t first = d0 & 0xFFFFu;
+    const uint32_t last = d2 >> 29;  // valid entries - 1
+    const uint32_t st[7] = {(d0 >> 16) & kDeltaMax,         ((d0 >> 27) | (d1 << 5)) & kDeltaMax,
+                            (d1 >> 6) & kDeltaMax,          (d1 >> 17) & kDeltaMax,
+                            ((d1 >> 28) | (d2 << 4)) & kDeltaMax, (d2 >> 7) & kDeltaMax,
+                            (d2 >> 18) & kDeltaMax};
+    uint32_t c = lds_swizzle(first & 0x7FFFu);
+    out[0] = first;
+    for (int k = 1; k < 8; ++k) {
+        c += st[k - 1];
+        out[k] = (uint32_t)k <= last ? lds_swizzle(c) : pad;
+    }
+}
+
 // Storage slot of the value of entry p (see above), and its inverse.  A 128-bit
 // access holds E = 16 / sizeof(V) values; the block of kWin entries is stored as
 // kE / E parts of 64 x E values, lane l's values k (E of them per part) at
@@ -168,6 +197,8 @@ struct PassArgs {
     const int64_t* piece_chunk; // [npieces * (kWaves + 1)] chunk bounds of the waves
     const int32_t* piece_seg;   // [npieces * kWaves] segment holding each chunk's first entry
     const int32_t* chunk_flags; // [npieces * kWaves] kChunkMid | kChunkCont
+    const uint64_t* dmask;      // 16-bit staged copies: bit w set when window w is
+                                // delta-coded (null: none is)
     const int32_t* wg_cut;      // P == 1: [grid + 1] rows cut between the workgroup's waves,
     const int32_t* cut_row;     //   which it finishes at the end of the pass from the
     const uint64_t* cut_desc;   //   head (2w) and tail (2w + 1) partials of its waves w:
@@ -235,6 +266,8 @@ struct Layout {
                                      // them (tiled), the hot width (hot), none (global)
     bool idx16 = false;
     int32_t cache = kCacheStream;    // CachePolicy of the passes over this copy
+    uint64_t* dmask = nullptr;       // [ceil(npad / kWin / 64)] delta-coded windows, or null
+    int64_t ndelta = 0;              // windows coded so
     void* idx = nullptr;             // [npad + kEntryPad]
     void* val = nullptr;             // [npad + kEntryPad] of the handle's value type
     int64_t* seg_start = nullptr;    // [S + 1], in padded positions
@@ -295,6 +328,10 @@ hipError_t launch_layout_fill(const uint64_t* keys, const int32_t* perm, const f
                               int64_t nnz, int cbits, const int32_t* seg_off, uint32_t swz_lim, bool idx16,
                               void* idx, V* val, int32_t* pos, hipStream_t s);
 hipError_t launch_fill_idx(void* idx, bool idx16, int32_t value, int64_t n, hipStream_t s);
+// Delta-codes the windows of a 16-bit index stream that allow it and marks them in
+// dmask (zeroed by the caller, ceil(npad / kWin / 64) words).
+hipError_t launch_delta_windows(void* idx, int64_t npad, int32_t pad, uint64_t* dmask,
+                                hipStream_t s);
 hipError_t launch_invert(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 hipError_t launch_slot_map(const int32_t* from, const int32_t* to, int64_t n, int32_t* out,
                           hipStream_t s);

@@ -334,8 +334,10 @@ template <class V>
 struct Win {
     static constexpr int E = 16 / sizeof(V);  // values per 128-bit access
     typename Vec16<V>::type vv[kE / E];
-    u32x4 c0, c1;  // IDX16: c0 holds the 8 indices packed in pairs
+    u32x4 c0, c1;  // IDX16: c0 holds the 8 indices packed in pairs (or, with dz,
+                   // the lane's delta-coded record in its first three words)
     V pr, ppr;
+    bool dz;       // IDX16: the window is delta-coded (uniform)
 };
 
 // Loads and stores of the residual stream under a copy's cache policy.
@@ -361,16 +363,44 @@ __device__ __forceinline__ void store_res(T v, T* p) {
 // lane 0's part of block b on every lane: one line, never used.  Positions fit
 // 31 bits (the layout build checks), so they are 32-bit here.  CA: the copy's
 // cache policy (streaming loads, unless the copy stays cached).
+// The delta-coded window bits of the 64 windows around the current one (wave-uniform).
+struct DMask {
+    uint64_t w;
+    int32_t i;  // word index, -1 before the first load
+};
+typedef uint32_t u32x3a __attribute__((ext_vector_type(3), aligned(4)));
+
 template <bool IDX16, int CA, class V>
 __device__ __forceinline__ void load_data(const PassArgs<V>& a, int32_t b, bool own, uint32_t le,
-                                          Win<V>& w) {
+                                          Win<V>& w, DMask& dm) {
     using VV = typename Vec16<V>::type;
     const uint32_t lo = own ? le : 0u;
     const VV* vp = reinterpret_cast<const VV*>(a.val + b) + (int)(lo / kE);
 #pragma unroll
     for (int q = 0; q < kE / Win<V>::E; ++q) w.vv[q] = load_res<CA>(vp + 64 * q);
     if constexpr (IDX16) {
-        w.c0 = load_res<CA>(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + b + lo));
+        bool dz = false;
+        if (a.dmask) {
+            const int32_t wi = b / kWin;
+            if ((wi >> 6) != dm.i) {  // once per 64 windows
+                dm.i = wi >> 6;
+                dm.w = a.dmask[dm.i];
+            }
+            dz = ((dm.w >> (wi & 63)) & 1u) != 0;
+        }
+        w.dz = dz;
+        if (dz) {
+            // 12 bytes per lane: the window's indices take its first 768 bytes.
+            const u32x3a* rp = reinterpret_cast<const u32x3a*>(static_cast<const uint32_t*>(a.idx) +
+                                                              b / 2 + 3 * (int)(lo / kE));
+            const u32x3a r = load_res<CA>(rp);
+            w.c0.x = r.x;
+            w.c0.y = r.y;
+            w.c0.z = r.z;
+        } else {
+            w.c0 = load_res<CA>(
+                reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.idx) + b + lo));
+        }
     } else {
         const u32x4* ip = reinterpret_cast<const u32x4*>(static_cast<const int32_t*>(a.idx) + b + lo);
         w.c0 = load_res<CA>(ip);
@@ -482,9 +512,19 @@ __device__ __forceinline__ void emit(const PassArgs<V>& a, const Walk& wk, int s
 // first, so two windows' loads are in flight while this one is reduced.
 template <int MODE, bool STAGED, bool IDX16, bool P1, int CA, bool XQ, class V>
 __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx, Walk& wk,
-                                       const Win<V>& cur, Win<V>& nxt, Win<V>& nn, int lane,
-                                       uint32_t le) {
+                                       Win<V>& cur, Win<V>& nxt, Win<V>& nn, int lane,
+                                       uint32_t le, DMask& dm) {
     using N = Needs<MODE>;
+    if constexpr (IDX16) {
+        if (cur.dz) {  // back to the plain format: 8 indices packed in pairs
+            uint32_t c[8];
+            delta_decode(cur.c0.x, cur.c0.y, cur.c0.z, (uint32_t)a.pad, c);
+            cur.c0.x = c[0] | (c[1] << 16);
+            cur.c0.y = c[2] | (c[3] << 16);
+            cur.c0.z = c[4] | (c[5] << 16);
+            cur.c0.w = c[6] | (c[7] << 16);
+        }
+    }
     constexpr bool HOT = STAGED && !IDX16;
     constexpr bool GLOBAL = !STAGED || HOT;  // some gathers read global memory
     // Float gathers are issued before the loads of the window after next; double
@@ -521,7 +561,7 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
     {
         const int32_t b2 = we + kWin;
         const bool more = b2 < wk.c1;
-        load_data<IDX16, CA, V>(a, more ? b2 : b, more, le, nn);
+        load_data<IDX16, CA, V>(a, more ? b2 : b, more, le, nn, dm);
     }
     const int nl = (int)((we - b) / kE);  // lanes holding entries of this window
     const bool lv = lane < nl;
@@ -644,29 +684,30 @@ __device__ __forceinline__ void window(const PassArgs<V>& a, const Gather<V>& gx
 // (flag kChunkMid).
 template <int MODE, bool IDX16, int CA, class V>
 __device__ __forceinline__ void begin_chunk(const PassArgs<V>& a, int32_t c0, int32_t c1, int s0,
-                                            int flags, int lane, Win<V>& wa, Win<V>& wb) {
+                                            int flags, int lane, Win<V>& wa, Win<V>& wb,
+                                            DMask& dm) {
     const uint32_t le = (uint32_t)lane * kE;
-    load_data<IDX16, CA, V>(a, c0, true, le, wa);
+    load_data<IDX16, CA, V>(a, c0, true, le, wa, dm);
     load_slots<MODE, V>(a, (flags & kChunkMid) ? s0 : s0 - 1, lane, wa);
     const bool more = c0 + kWin < c1;
-    load_data<IDX16, CA, V>(a, more ? c0 + kWin : c0, more, le, wb);
+    load_data<IDX16, CA, V>(a, more ? c0 + kWin : c0, more, le, wb, dm);
 }
 
 // wa and wb hold the requests of begin_chunk.
 template <int MODE, bool STAGED, bool IDX16, bool P1, int CA, bool XQ, class V>
 __device__ __forceinline__ void run_chunk(const PassArgs<V>& a, const Gather<V>& gx, int32_t c0,
                                           int32_t c1, int s0, int flags, int gc, int lane,
-                                          Win<V>& wa, Win<V>& wb, double& sse) {
+                                          Win<V>& wa, Win<V>& wb, double& sse, DMask& dm) {
     const uint32_t le = (uint32_t)lane * kE;
     const bool mid = flags & kChunkMid;
     Walk wk{c0, c1, mid ? s0 : s0 - 1, mid, 0.0, 0.0, sse, mid ? s0 : -1, a.nseg + 2 * gc};
     Win<V> wc;
     while (true) {
-        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wa, wb, wc, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wa, wb, wc, lane, le, dm);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wb, wc, wa, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wb, wc, wa, lane, le, dm);
         if (wk.elo >= c1) break;
-        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wc, wa, wb, lane, le);
+        window<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, wk, wc, wa, wb, lane, le, dm);
         if (wk.elo >= c1) break;
     }
     if constexpr (MODE != kModeFlush) {
@@ -734,6 +775,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
 
     double sse = 0.0;
     int staged = -1;
+    DMask dm{0, -1};
     for (int pc = a.wg_piece[wg]; pc < a.wg_piece[wg + 1]; ++pc) {
         const int32_t c0 = (int32_t)a.piece_chunk[pc * (kWaves + 1) + wave];
         const int32_t c1 = (int32_t)a.piece_chunk[pc * (kWaves + 1) + wave + 1];
@@ -742,7 +784,7 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
         // The chunk's first windows are requested before the staging, which they do
         // not depend on.
         Win<V> wa, wb;
-        if (c0 < c1) begin_chunk<MODE, IDX16, CA, V>(a, c0, c1, s0, flags, lane, wa, wb);
+        if (c0 < c1) begin_chunk<MODE, IDX16, CA, V>(a, c0, c1, s0, flags, lane, wa, wb, dm);
         if constexpr (STAGED) {
             const int tile = a.piece_tile[pc];
             if (tile != staged) {
@@ -753,7 +795,8 @@ __device__ __forceinline__ void pass_main(const PassArgs<V>& a) {
             }
         }
         if (c0 < c1)
-            run_chunk<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse);
+            run_chunk<MODE, STAGED, IDX16, P1, CA, XQ, V>(a, gx, c0, c1, s0, flags, gc, lane, wa, wb, sse,
+                                                           dm);
     }
     if constexpr (MODE == kModeFlush) {
         const double t = wave_sum(sse);
@@ -1012,6 +1055,7 @@ hipError_t launch_pass(const Layout& L, PassMode mode, const V* x, const V* p, c
     a.piece_chunk = L.piece_chunk;
     a.piece_seg = L.piece_seg;
     a.chunk_flags = L.chunk_flags;
+    a.dmask = L.dmask;
     a.wg_cut = L.wg_cut;
     a.cut_row = L.cut_row;
     a.cut_desc = L.cut_desc;

@@ -59,6 +59,7 @@ def test_create_rejects_bad_arguments_on_the_host(kw, msg):
     (dict(precision=2), "precision"),
     (dict(cache=(4, 0)), "cache"),
     (dict(cache=(0, -1)), "cache"),
+    (dict(index_coding=(2, 0)), "index_coding"),
 ])
 def test_create_rejects_bad_options(kw, msg):
     _lib_or_skip()

@@ -274,6 +274,51 @@ def test_cache_policies_give_identical_results(tiles):
         g.close()
 
 
+@pytest.mark.parametrize("case", ["one_tile", "tiles", "double", "mixed_gaps"])
+def test_index_coding_gives_identical_results(case):
+    # Delta-coded index windows decode to the plain indices, so the passes, the
+    # residual rebuild of set_factors and element-wise CCD give bitwise the same
+    # results with and without them.  "mixed_gaps": rows of 1 to 5000 entries over
+    # 6000 columns, so that some windows have steps past 2047 and stay plain.
+    from paper_1511_02433_amd.ccdpp import make_options
+    if case == "mixed_gaps":
+        lens = [5000, 3000, 2049, 1025, 1024, 513, 200, 64, 9, 1, 0] * 3
+        m, n, k = len(lens), 6000, 3
+        row, col, val, H0 = synth.lengths_problem(lens, n, k, seed=41)
+    else:
+        lens = [850, 700, 300, 40] + list(np.random.default_rng(31).integers(0, 80, 1496))
+        m, n, k = 1500, 900, 4
+        row, col, val, H0 = synth.lengths_problem(lens, n, k, seed=32)
+    # Streaming copies: the automatic choice codes no window of a copy that stays cached.
+    kw = {"one_tile": dict(gather_mode=(2, 2)), "tiles": dict(gather_mode=(2, 2), tile_width=(192, 128)),
+          "double": dict(gather_mode=(2, 2), precision=1), "mixed_gaps": dict()}[case]
+    kw["cache"] = (1, 1)
+    print(f"case: index coding, {case}", flush=True)
+    W1 = (np.random.default_rng(5).standard_normal((m, k)) * 0.1).astype(np.float32)
+    outs = []
+    for coding in [(1, 1), (0, 0)]:
+        g = CCDPP(m, n, k, 0.1, row, col, val, opts=make_options(index_coding=coding, **kw))
+        info = g.info()
+        print({key: v for key, v in info.items() if "windows" in key})
+        if coding == (1, 1):
+            assert info["u_delta_windows"] == 0 and info["v_delta_windows"] == 0
+        else:
+            assert info["u_delta_windows"] > 0 and info["v_delta_windows"] > 0
+        g.set_factors(np.zeros((m, k), np.float32), H0)
+        g.run(1, 2)
+        out = list(g.factors())
+        g.set_factors(W1, H0)  # rebuilds the residual from the stored indices
+        out.append(g.residual())
+        g.run(1, 3)
+        g.ccd_run(1)
+        out += list(g.factors()) + [g.residual()]
+        assert g.check_consistency() == 0
+        g.close()
+        outs.append(out)
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("layout", ["auto", "global", "hot"])
 @pytest.mark.parametrize("transpose", [False, True])
 def test_short_segments_fill_windows(layout, transpose):
