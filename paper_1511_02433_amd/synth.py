@@ -170,7 +170,7 @@ def _sample_positions(deg: np.ndarray, q: np.ndarray, rng: np.random.Generator,
 
     light = np.flatnonzero(~heavy)
     need = deg[light].astype(np.int64)
-    # Round 1: sorted draws per row -> duplicates are adjacent.
+    # First draw: sorted uniforms per row, so duplicate columns are adjacent.
     u = _sorted_uniforms(need, rng)
     cols = np.searchsorted(cdf, u, side="right").astype(np.int64)
     np.minimum(cols, n - 1, out=cols)
