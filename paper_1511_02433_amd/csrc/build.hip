@@ -154,10 +154,6 @@ __global__ void k_factor_out(const V* __restrict__ colmajor, const int32_t* __re
     }
 }
 
-// R = A - w_i^T h_j for every entry of the user-major layout (prediction summed
-// in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
-// unpadded layout order) has its value in slot pos[e]; its segment, and from it the
-// row and the tile, are found by binary search.
 // Rewrites, one wave per window, every window whose lanes' valid entries each climb
 // by at most kDeltaMax unswizzled columns into the delta-coded format, and sets its
 // bit.  Valid entries come first in a lane (padding only ends a segment); a lane
@@ -212,6 +208,10 @@ __device__ __forceinline__ uint32_t index_at(const I* idx, const uint64_t* dmask
     return (uint32_t)idx[q];
 }
 
+// R = A - w_i^T h_j for every entry of the user-major layout (prediction summed
+// in fp64 over ascending features, one rounding to fp32).  Entry e (A[e], in the
+// unpadded layout order) has its value in slot pos[e]; its segment, and from it the
+// row and the tile, are found by binary search.
 template <class I, class V>
 __global__ void k_rebuild(const int64_t* __restrict__ seg_start, int64_t nseg,
                           const int32_t* __restrict__ seg_row, const int32_t* __restrict__ tile_seg,

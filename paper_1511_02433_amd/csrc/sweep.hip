@@ -356,20 +356,22 @@ __device__ __forceinline__ void store_res(T v, T* p) {
         *p = v;
 }
 
-// Data loads of the window block at b (a multiple of kWin): lane l's values from
-// the two halves of the block (val_slot order), its indices in entry order.
-// Chunks start and end at multiples of kWin, so every block a chunk reads lies
-// whole inside the arrays.  A window past the chunk's end (own == false) rereads
-// lane 0's part of block b on every lane: one line, never used.  Positions fit
-// 31 bits (the layout build checks), so they are 32-bit here.  CA: the copy's
-// cache policy (streaming loads, unless the copy stays cached).
-// The delta-coded window bits of the 64 windows around the current one (wave-uniform).
+// The delta-coded window bits of 64 consecutive windows, kept while a wave walks
+// them (wave-uniform).
 struct DMask {
     uint64_t w;
     int32_t i;  // word index, -1 before the first load
 };
 typedef uint32_t u32x3a __attribute__((ext_vector_type(3), aligned(4)));
 
+// Data loads of the window block at b (a multiple of kWin): lane l's values from
+// the two halves of the block (val_slot order), its indices in entry order (or,
+// in a delta-coded window, its 12-byte record, decoded when the window is used).
+// Chunks start and end at multiples of kWin, so every block a chunk reads lies
+// whole inside the arrays.  A window past the chunk's end (own == false) rereads
+// lane 0's part of block b on every lane: one line, never used.  Positions fit
+// 31 bits (the layout build checks), so they are 32-bit here.  CA: the copy's
+// cache policy (streaming loads, unless the copy stays cached).
 template <bool IDX16, int CA, class V>
 __device__ __forceinline__ void load_data(const PassArgs<V>& a, int32_t b, bool own, uint32_t le,
                                           Win<V>& w, DMask& dm) {
