@@ -2,9 +2,12 @@
 """Throughput of the CCD++ sweep on one MI355X.
 
 A step is one outer iteration of Algorithm 3 on the whole workload: all k
-features, each with inner_iters u/v alternations, the fused residual
-bookkeeping, and the final residual flush with the training sum of squares
-(one ccdpp_run(1, inner) call).  Inputs are resident in HBM before timing.
+features, each with inner_iters u/v alternations and the fused residual
+bookkeeping (one ccdpp_run(1, inner) call).  ccdpp_run leaves the last
+feature's residual update pending for the next call's first passes; the timed
+region ends with it (the final flush, with the training sum of squares), so K
+timed steps do all the work of K outer iterations.  Inputs are resident in HBM
+before timing.
 
   value    = 2 * inner * k * nnz / (seconds per step) / 1e9   [G nonzero visits / s]
   roofline = algorithmic bytes of the dominant kernel per launch / its mean
@@ -208,6 +211,7 @@ def main():
         t0 = time.perf_counter()
         for _ in range(steps):
             step()
+        g.train_rmse()  # the pending residual update of the last feature, and sum R^2
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) * 1e3 / steps
 
@@ -220,6 +224,7 @@ def main():
             g.profile(True)
         step()
         if last:
+            g.train_rmse()  # the flush, so that the kernel table shows it once per step
             torch.cuda.synchronize()
             kinds, per_layout = read_kernels()
     torch.cuda.synchronize()

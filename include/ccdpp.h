@@ -147,7 +147,11 @@ int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  * in order), each feature with inner_iters alternations of eq. 15 then
  * eq. 16.  outer_iters >= 0, inner_iters >= 1.  State (W, H, residual)
  * persists across calls: two calls of 1 outer iteration give bitwise the
- * same result as one call of 2.  Blocking.
+ * same result as one call of 2.  Blocking.  W and H are final on return; the
+ * residual update of the last feature (eq. 18) is left pending and applied by
+ * the first passes of the next ccdpp_run, or before any call that reads the
+ * residual (ccdpp_train_rmse, ccdpp_get_residual, ccdpp_check_consistency,
+ * ccdpp_ccd_run), so a run split into calls costs what one call does.
  */
 int ccdpp_run(ccdpp_t *h, int32_t outer_iters, int32_t inner_iters);
 

@@ -1173,24 +1173,38 @@ int run_impl(ccdpp* h, int32_t outer, int32_t inner) {
             h->pending = t;
         }
     }
-    if (h->pending >= 0) {
-        // Final eq. 18 on both copies; the user-major one also sums R^2 for the training RMSE.
-        const V* Wp = W + (int64_t)h->pending * m;
-        const V* Hp = H + (int64_t)h->pending * n;
-        RCK(pass<V>(h, 0, kModeFlush, nullptr, -1, h->pending, nullptr, Hp, nullptr, -1, 1));
-        HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
-        RCK(pass<V>(h, 1, kModeFlush, nullptr, -1, h->pending, nullptr, Wp, nullptr, -1, 1));
-        h->pending = -1;
-        double sse = 0.0;
-        HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
-        HIPCK(h, hipStreamSynchronize(h->stream));
-        h->train_sse = h->L[0].grid ? sse : 0.0;
-        h->train_sse_valid = true;
-    } else {
-        HIPCK(h, hipStreamSynchronize(h->stream));
-    }
+    // The last feature's eq. 18 stays pending: the next call's first passes apply it
+    // (as between features), and flush_pending does when the residual is read.
+    if (outer > 0 && h->pending >= 0) h->train_sse_valid = false;
+    HIPCK(h, hipStreamSynchronize(h->stream));
     if (h->prof) collect_profile(h);
     return CCDPP_OK;
+}
+
+// The pending eq. 18 on both copies; the user-major flush also sums R^2 for the
+// training RMSE.
+template <class V>
+int flush_impl(ccdpp* h) {
+    using namespace ccdk;
+    const V* Wp = as<V>(h->W) + (int64_t)h->pending * h->m;
+    const V* Hp = as<V>(h->H) + (int64_t)h->pending * h->n;
+    RCK(pass<V>(h, 0, kModeFlush, nullptr, -1, h->pending, nullptr, Hp, nullptr, -1, 1));
+    HIPCK(h, launch_reduce_sum(h->sse_part, h->L[0].grid * kWaves, h->d_scalar, h->stream));
+    RCK(pass<V>(h, 1, kModeFlush, nullptr, -1, h->pending, nullptr, Wp, nullptr, -1, 1));
+    h->pending = -1;
+    double sse = 0.0;
+    HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
+    HIPCK(h, hipStreamSynchronize(h->stream));
+    h->train_sse = h->L[0].grid ? sse : 0.0;
+    h->train_sse_valid = true;
+    if (h->prof) collect_profile(h);
+    return CCDPP_OK;
+}
+
+// Brings the residual up to date before anything reads it.
+int flush_pending(ccdpp* h) {
+    if (h->pending < 0) return CCDPP_OK;
+    return h->dbl ? flush_impl<double>(h) : flush_impl<float>(h);
 }
 
 template <class S>
@@ -1267,6 +1281,7 @@ int get_residual_impl(ccdpp* h, S* R) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (!R && h->nnz) return fail(h, CCDPP_EINVAL, "R is NULL");
     if (h->nnz == 0) return CCDPP_OK;
+    RCK(flush_pending(h));
     hipStream_t s = h->stream;
     S* d;
     Tmp t;
@@ -1306,7 +1321,7 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
 int ccdpp_ccd_run(ccdpp_t* h, int32_t outer) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (outer < 0) return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0");
-    if (h->pending >= 0) return fail(h, CCDPP_ESTATE, "internal: a subtract is pending");
+    RCK(flush_pending(h));
     return h->dbl ? ccd_impl<double>(h, outer) : ccd_impl<float>(h, outer);
 }
 
@@ -1353,6 +1368,7 @@ int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol
     int32_t done = 0;
     for (int32_t it = 0; it < max_outer; ++it) {
         RCK(ccdpp_run(h, 1, inner));
+        RCK(flush_pending(h));  // the training sum of squares
         double w2 = 0.0, h2 = 0.0, te = std::nan("");
         RCK(launch_sq_sum_any(h, h->W, h->m * h->k));
         RCK(reduce(&w2));
@@ -1425,6 +1441,7 @@ int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (!rmse_out) return fail(h, CCDPP_EINVAL, "rmse_out is NULL");
     if (h->nnz < 1) return fail(h, CCDPP_EINVAL, "no observed entries");
+    RCK(flush_pending(h));
     if (!h->train_sse_valid) {
         hipStream_t s = h->stream;
         RCK(launch_sq_sum_any(h, h->L[0].val, h->L[0].npad));
@@ -1446,6 +1463,7 @@ int ccdpp_get_residual_f64(ccdpp_t* h, double* R) { return get_residual_impl<dou
 int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (!mismatches) return fail(h, CCDPP_EINVAL, "mismatches is NULL");
+    RCK(flush_pending(h));
     hipStream_t s = h->stream;
     HIPCK(h, hipMemsetAsync(h->d_count, 0, 8, s));
     RCK(with_value_type(h, [&](auto z) -> int {
