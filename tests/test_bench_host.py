@@ -1,0 +1,53 @@
+"""Host-side logic of bench.py (no GPU): kernel names, stored traffic lookup, and
+the refusal of more than one GPU."""
+import json
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# ccdpp_info fields of the large layouts: user-major tiled with one tile (write-back
+# stores), item-major tiled with 36 tiles (streaming).
+INFO = {"value_bytes": 4, "u_gather": 2, "u_tiles": 1, "u_tile_width": 17770, "u_cache": 2,
+        "v_gather": 2, "v_tiles": 36, "v_tile_width": 13376, "v_cache": 1}
+
+
+def test_kernel_symbols_follow_the_layout_and_cache_policy():
+    k = bench.kernel_symbol
+    assert k(0, INFO, 0) == "void ccdk::ccd_pass_fused<true, true, true, 1, float>(ccdk::PassArgs<float>)"
+    # the plain pass stores no residual: the streaming kernel
+    assert k(1, INFO, 0) == "void ccdk::ccd_pass<true, true, true, 0, float>(ccdk::PassArgs<float>)"
+    assert k(1, INFO, 1) == "void ccdk::ccd_pass<true, true, false, 0, float>(ccdk::PassArgs<float>)"
+    assert k(4, INFO, 1) == "void ccdk::ccd_flush<true, true, false, 0, float>(ccdk::PassArgs<float>)"
+    # automatic write-back stores apply to CCD++ with two or more inner iterations only
+    assert k(0, INFO, 0, wb_stores=False) == \
+        "void ccdk::ccd_pass_fused<true, true, true, 0, float>(ccdk::PassArgs<float>)"
+    hot = dict(INFO, v_gather=3, v_tiles=1, v_tile_width=40768, value_bytes=8)
+    assert k(1, hot, 1) == "void ccdk::ccd_pass<true, false, true, 0, double>(ccdk::PassArgs<double>)"
+    assert k(2, INFO, 1) == "void ccdk::ccd_combine<16, float>(ccdk::CombineArgs<float>)"
+
+
+def test_stored_traffic_only_for_the_sources_it_was_taken_on():
+    # The committed counters carry the digest of the kernel sources they were taken on;
+    # bench.py reports them only while the sources are unchanged.
+    with open(os.path.join(ROOT, "profiles", "traffic_large.json")) as f:
+        t = json.load(f)
+    assert len(t["source_digest"]) == 16
+    for key, v in t["kernels"].items():
+        assert v["bytes_per_launch"] > 0 and v["algo_bytes_per_launch"] > 0
+        got = bench.stored_traffic(key, "large")
+        if t["source_digest"] == bench.source_digest():
+            assert got == v["bytes_per_launch"]
+        else:
+            assert got is None
+    assert bench.stored_traffic("ccd_pass/rows", "no_such_workload") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
