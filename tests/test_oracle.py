@@ -2,6 +2,10 @@
 by re-typing the oracle's own formulas.
 
 * a hand-worked example (tests/golden/hand_example.txt, from eq. 13-18);
+* a hand-worked two-feature example (tests/golden/hand_example_k2.txt) that
+  fixes the order of the feature updates of element-wise CCD (Algorithm 2,
+  eq. 5-10) and of CCD++ (Algorithm 3), which the one-feature example and the
+  fixed-point pins cannot see;
 * every single-coordinate update is the minimiser of its 1-D quadratic, found
   by golden-section search (eq. 14 restricted to u_i or v_j);
 * the objective of eq. 1 never increases, block by block;
@@ -29,11 +33,12 @@ from oracle import Oracle
 from paper_1511_02433_amd import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_example.txt")
+GOLDEN_K2 = os.path.join(os.path.dirname(__file__), "golden", "hand_example_k2.txt")
 
 
-def _golden():
+def _golden(path=GOLDEN):
     g = {"entry": []}
-    with open(GOLDEN) as f:
+    with open(path) as f:
         for line in f:
             line = line.strip()
             if not line or line.startswith("#"):
@@ -62,6 +67,26 @@ def test_hand_example(from_scratch):
     np.testing.assert_allclose(tr, g["objective_trace"], rtol=1e-14)
     assert abs(o.train_rmse() ** 2 - g["train_rmse_squared"][0]) < 1e-14
     assert abs(o.objective() - g["objective_trace"][-1]) < 1e-13
+
+
+@pytest.mark.parametrize("algorithm", ["ccd", "ccdpp"])
+def test_hand_example_two_features(algorithm):
+    """Feature order at k = 2: ascending t, for Algorithm 2 (every row's features
+    in turn, then every column's) and for Algorithm 3 (feature 0 in full, then
+    feature 1).  A descending or shuffled feature loop fails here."""
+    g = _golden(GOLDEN_K2)
+    e = np.array(g["entry"])
+    m, n, k, lam = int(g["m"][0]), int(g["n"][0]), int(g["k"][0]), g["lambda"][0]
+    o = Oracle(m, n, k, lam, e[:, 0], e[:, 1], e[:, 2], np.array(g["H0"]).reshape(n, k))
+    if algorithm == "ccd":
+        o.ccd_run(1)
+    else:
+        o.run(1, 1)
+    W, H = o.factors()
+    np.testing.assert_allclose(W.reshape(-1), g[f"{algorithm}_W"], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(H.reshape(-1), g[f"{algorithm}_H"], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(o.residual(), g[f"{algorithm}_R"], rtol=0, atol=1e-14)
+    o.close()
 
 
 def _golden_min(f, lo, hi, iters=200):
