@@ -12,9 +12,20 @@ before timing.
   value    = 2 * inner * k * nnz / (seconds per step) / 1e9   [G nonzero visits / s]
   roofline = algorithmic bytes of the dominant kernel per launch / its mean
              duration (HIP events on the library's stream, inside the timed
-             region), against 8 TB/s HBM peak
+             region), against 8 TB/s HBM peak.  The algorithmic bytes follow
+             the byte model of the sweep with 4-byte indices and row pointers:
+             a plain pass reads index and value of every entry (8 B per entry
+             in float), a first pass or flush also writes the value back
+             (12 B), plus per pass the row pointers, the per-row factor
+             scalars read, the coordinates written and one read of each
+             gathered vector.  `frac` is that rate over the peak; `frac_hw`
+             is the HBM traffic the hardware counters measured for the same
+             kernel (profiles/traffic_*.json) over the same time and peak;
+             `frac_stored` prices the bytes the compressed layout must move
+             (16-bit or delta-coded indices), which is less than the model.
   cpu_baseline = the fp64 oracle on the host cores, on a bounded sample of
-             features of the same matrix
+             features of the same matrix: once on one thread, once on all
+             the threads the host gives this process
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -58,6 +69,31 @@ def kernel_symbol(kind: int, info: dict, layout: int, wb_stores: bool = True) ->
     return f"void ccdk::{name}<{b(staged)}, {b(idx16)}, {b(p1)}, {cache}, {v}>(ccdk::PassArgs<{v}>)"
 
 
+# Vectors a pass gathers, per (kind, copy): the plain pass its update vector; the first
+# pass of a feature over the user-major copy h_t and h_(t-1) (u's update vector is h_t),
+# over the item-major copy u, w_t and w_(t-1); the flush the previous feature's vector.
+GATHERED = {(0, 0): 2, (0, 1): 3, (1, 0): 1, (1, 1): 1, (4, 0): 1, (4, 1): 1}
+
+
+def model_bytes(kind: int, layout: int, info: dict) -> float | None:
+    """Bytes of one pass (kind 0 first pass, 1 plain pass, 4 flush) over one residual
+    copy under the sweep's byte model: 4-byte indices and row pointers, values,
+    factor entries and coordinates of the value type."""
+    if (kind, layout) not in GATHERED:
+        return None
+    vb = info.get("value_bytes", 4)
+    nnz = info["nnz"]
+    rows, cols = (info["m"], info["n"]) if layout == 0 else (info["n"], info["m"])
+    b = (4 + vb) * nnz + 4 * (rows + 1)            # index and value read, row pointers
+    if kind in (0, 4):
+        b += vb * nnz                               # the residual written back
+    if kind in (0, 1):
+        b += vb * rows                              # the coordinates written
+    b += vb * rows * (2 if kind == 0 else 1 if kind == 4 else 0)  # per-row factor scalars
+    b += vb * cols * GATHERED[(kind, layout)]        # each gathered vector, once
+    return float(b)
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -85,13 +121,42 @@ def stored_traffic(key: str, workload: str, precision: str = "f32"):
     return None if k is None else k.get("bytes_per_launch")
 
 
-def cpu_baseline(ds, k, inner, budget_s, threads, algorithm="ccdpp"):
-    import numpy as np
+def host_threads() -> dict:
+    """What the host offers this process: all logical CPUs, the ones this process may
+    run on, the thread count the environment sets for OpenMP, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    use = affinity
+    if omp.isdigit() and int(omp) > 0:
+        use = min(use, int(omp))
+    return {"cores_all": os.cpu_count(), "affinity": affinity, "omp_num_threads": omp or None,
+            "threads": use, "cpu_model": model}
+
+
+def cpu_baseline(ds, k, inner, budget_s, algorithm="ccdpp"):
+    """The oracle, as it stands, on a bounded sample of the workload: feature updates
+    in Algorithm 3's order, first on one thread (about a third of the budget), then
+    on every thread the host gives this process (the rest).  `value` is the latter."""
     from oracle import Oracle
 
     w = ds.workload
-    log(f"cpu baseline: building the oracle on {w.name} ({threads} threads)")
+    host = host_threads()
+    threads = host["threads"]
+    log(f"cpu baseline: building the oracle on {w.name}; host {host}")
     o = Oracle(w.m, w.n, k, w.lam, ds.row, ds.col, ds.val, ds.h0(k), threads=threads)
+    out = {"unit": "Gnnz/s", "cores": threads, "kind": "oracle", **host}
     if algorithm == "ccd":
         # One whole outer iteration of Algorithm 2 (it cannot be cut per feature).
         t0 = time.perf_counter()
@@ -99,26 +164,38 @@ def cpu_baseline(ds, k, inner, budget_s, threads, algorithm="ccdpp"):
         dt = time.perf_counter() - t0
         o.close()
         log(f"cpu baseline: one element-wise CCD outer iteration in {dt:.2f}s")
-        return {"value": 2.0 * k * w.nnz / dt / 1e9, "unit": "Gnnz/s", "cores": threads,
-                "kind": "oracle", "sample": f"one outer iteration of element-wise CCD on the full "
-                                            f"{w.name} matrix, fp64 oracle, {dt:.1f} s"}
+        v = 2.0 * k * w.nnz / dt / 1e9
+        out.update(value=v, value_all=v, value_1t=None,
+                   sample=f"one outer iteration of element-wise CCD on the full {w.name} "
+                          f"matrix, fp64 oracle, {threads} threads, {dt:.1f} s")
+        return out
+
     # Feature updates in Algorithm 3's order (features 0..k-1, then the next outer
-    # iteration), until the budget is spent, at most three outer iterations.
-    done = 0
-    t0 = time.perf_counter()
-    while done < 3 * k:
-        o.rank(done % k, inner, debug=False)
-        done += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
+    # iteration) until the budget of each leg is spent.
+    def leg(nthreads, budget, start, cap):
+        o.set_threads(nthreads)
+        done = 0
+        t0 = time.perf_counter()
+        while done < cap:
+            o.rank((start + done) % k, inner, debug=False)
+            done += 1
+            if time.perf_counter() - t0 >= budget:
+                break
+        return done, time.perf_counter() - t0
+
+    n1, dt1 = leg(1, budget_s / 3.0, 0, k)
+    log(f"cpu baseline: 1 thread, {n1} feature updates x {inner} inner in {dt1:.2f}s")
+    na, dta = leg(threads, budget_s - dt1, n1, 3 * k)
+    log(f"cpu baseline: {threads} threads, {na} feature updates x {inner} inner in {dta:.2f}s")
     o.close()
-    visits = 2.0 * inner * w.nnz * done
-    log(f"cpu baseline: {done} feature updates x {inner} inner in {dt:.2f}s")
-    return {"value": visits / dt / 1e9, "unit": "Gnnz/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} feature updates in Algorithm 3's order ({done / k:.2f} outer "
-                      f"iterations of {k} features, inner {inner}) on the full {w.name} matrix, "
-                      f"fp64 oracle, {dt:.1f} s"}
+    v1 = 2.0 * inner * w.nnz * n1 / dt1 / 1e9
+    va = 2.0 * inner * w.nnz * na / dta / 1e9
+    out.update(value=va, value_all=va, value_1t=v1,
+               sample=f"feature updates in Algorithm 3's order on the full {w.name} matrix "
+                      f"(k {k}, inner {inner}), fp64 oracle: features 0..{n1 - 1} on 1 thread "
+                      f"({dt1:.1f} s), then the next {na} ({na / k:.2f} outer iterations) on "
+                      f"{threads} threads ({dta:.1f} s)")
+    return out
 
 
 def main():
@@ -128,7 +205,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="large", choices=["tiny", "medium", "large", "vlarge"])
     ap.add_argument("--k", type=int, default=0, help="override the number of features")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prof", action="store_true", help="time without per-kernel events")
     ap.add_argument("--event-every", type=int, default=5,
@@ -192,12 +269,15 @@ def main():
             for lay, lname in LAYOUT_NAMES.items():
                 n2, t2, b2 = g.profile_read(kind, lay)
                 if n2:
+                    mb = model_bytes(kind, lay, info)
                     per_layout[f"{name}/{lname}"] = {
                         "kernel": kernel_symbol(kind, info, lay, wb_stores), "kind": kind,
                         "layout": lay,
                         "launches": n2, "mean_us": round(t2 / n2 * 1e3, 3),
-                        "total_ms": round(t2, 4), "algo_bytes_per_launch": b2 / n2,
-                        "gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
+                        "total_ms": round(t2, 4), "model_bytes_per_launch": mb,
+                        "model_gbs": None if mb is None else round(mb / (t2 / n2 * 1e-3) / 1e9, 1),
+                        "stored_bytes_per_launch": b2 / n2,
+                        "stored_gbs": round(b2 / (t2 * 1e-3) / 1e9, 1)}
         return kinds, per_layout
 
     def step():
@@ -266,13 +346,21 @@ def main():
     roofline = None
     if prof and dom:
         d = per_layout[dom]
-        achieved = live["algo_bytes_per_launch"] / (live["mean_us"] * 1e-6) / 1e9
+        sec = live["mean_us"] * 1e-6
+        mb = d["model_bytes_per_launch"]
+        achieved = mb / sec / 1e9
+        stored = live["algo_bytes_per_launch"] / sec / 1e9
+        traffic = stored_traffic(dom, w.name, args.precision)
         roofline = {"kernel": d["kernel"], "layout": dom.split("/")[1], "bound": "hbm",
                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": stored_traffic(dom, w.name, args.precision), "mean_us": live["mean_us"],
-                    "launches": live["launches"],
-                    "algo_bytes_per_launch": live["algo_bytes_per_launch"]}
+                    "traffic": traffic,
+                    "frac_hw": None if traffic is None
+                    else round(traffic / sec / 1e9 / HBM_PEAK_GBS, 4),
+                    "frac_stored": round(stored / HBM_PEAK_GBS, 4),
+                    "mean_us": live["mean_us"], "launches": live["launches"],
+                    "algo_bytes_per_launch": mb,
+                    "stored_bytes_per_launch": live["algo_bytes_per_launch"]}
     train_rmse = g.train_rmse()
     test_rmse = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
     # The open outer loop with monitoring: three more outer iterations, each followed by
@@ -298,9 +386,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        threads = min(16, os.cpu_count() or 1)
-        cpu = cpu_baseline(synth.load(args.workload), k, inner, args.cpu_budget, threads,
-                           args.algorithm)
+        cpu = cpu_baseline(synth.load(args.workload), k, inner, args.cpu_budget, args.algorithm)
 
     out = {
         "metric": "CCD++ nonzeros/sec (G/s) + achieved HBM GB/s vs peak; s per outer iter",

@@ -19,8 +19,9 @@
  * R = R-hat - u v^T (eq. 18).
  *
  * Conventions for every call:
- *  - Indices are 0-based int32; m and n must be below 2^30 and nnz at most
- *    2^31 - 1.
+ *  - Indices are 0-based int32; m and n must be below 2^28 (the passes
+ *    address gathered records of up to 16 bytes with 32-bit byte offsets) and
+ *    nnz at most 2^31 - 1.
  *  - Every array argument is HOST memory owned by the caller.  The library
  *    copies what it needs during the call and keeps no pointer to it.
  *  - Factor matrices at the boundary are row-major float32: W is m x k
@@ -29,7 +30,9 @@
  *    ccdpp_create) and is not thread-safe.
  *  - Calls return CCDPP_OK (0) or a negative status.  Out-parameters are left
  *    untouched on error.  After a device error the handle answers every
- *    later call with CCDPP_ESTATE until it is destroyed.
+ *    later call with CCDPP_ESTATE until it is destroyed.  A failed device
+ *    allocation (ENOMEM) is reported before the call changes any state, so
+ *    the handle stays usable.
  *  - Calls that compute are blocking: they synchronise the handle's stream
  *    before returning.
  */
@@ -56,7 +59,7 @@ enum ccdpp_status {
 /*
  * Create a factorization problem from training triplets (Section 3: A as
  * triplets i, j, a_ij; Algorithms 3 and 7: W = 0, R = A).
- *   m, n    : rows (users) and columns (items), 1 <= m, n < 2^30
+ *   m, n    : rows (users) and columns (items), 1 <= m, n < 2^28
  *   k       : number of features, >= 1
  *   lambda  : regularisation of eq. 1, finite and >= 0
  *   nnz     : number of observed entries, 0 <= nnz <= 2^31 - 1
@@ -179,8 +182,15 @@ int ccdpp_run_until(ccdpp_t *h, int32_t max_outer, int32_t inner_iters, double r
                     int64_t test_nnz, const int32_t *test_row, const int32_t *test_col,
                     const float *test_val, double *history, int32_t *outer_done);
 
-/* Copy the factors out: W as m x k, H as n x k, row-major float32.  Either
- * pointer may be NULL to skip it.  Blocking. */
+/* Copy the factors out (Section 3: W in R^(m x k) profiles the users, row i
+ * being w_i; H in R^(n x k) profiles the items, row j being h_j; together they
+ * minimise eq. 1.  Algorithm 7 ends with them on the host, its columns
+ * wbar_t, hbar_t having been committed by eq. 17).
+ *   W : NULL, or m * k floats, written row-major (W[i * k + t] = w_it)
+ *   H : NULL, or n * k floats, written row-major (H[j * k + t] = h_jt)
+ * Host memory owned by the caller.  Either pointer may be NULL to skip it.
+ * A float64 handle rounds its factors to float32 here.  Returns ESTATE on a
+ * NULL or poisoned handle.  Blocking. */
 int ccdpp_get_factors(ccdpp_t *h, float *W, float *H);
 /* The same in float64 (exact for a float64 handle). */
 int ccdpp_get_factors_f64(ccdpp_t *h, double *W, double *H);
@@ -199,8 +209,14 @@ int ccdpp_set_factors_f64(ccdpp_t *h, const double *W, const double *H);
 int ccdpp_rmse(ccdpp_t *h, int64_t nnz, const int32_t *row, const int32_t *col,
                const float *val, double *rmse_out);
 
-/* Training RMSE sqrt(sum_{Omega} R_ij^2 / nnz) of the current residual
- * (float64 accumulation).  nnz must be >= 1.  Blocking. */
+/* Training RMSE of the current factors: the RMSE of Section 8 evaluated on
+ * the training set itself, from the residual of Section 3.2
+ * (R_ij = A_ij - w_i^T h_j on Omega, kept up to date by eq. 18):
+ * sqrt(sum_{Omega} R_ij^2 / nnz), accumulated in float64 on the device in a
+ * fixed order.  A residual update left pending by ccdpp_run is applied first.
+ *   rmse_out : receives the RMSE (host memory, not NULL)
+ * Returns EINVAL when the handle holds no observed entries (nnz = 0) or
+ * rmse_out is NULL.  Blocking. */
 int ccdpp_train_rmse(ccdpp_t *h, double *rmse_out);
 
 /* Residual R in the order of the triplets given to ccdpp_create
@@ -262,6 +278,18 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   same two for the item-major copy.
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
+
+/* Testing hook for the error paths, forced from the host (process-wide):
+ *   what = 0 : the device allocation made by the library after `after` more
+ *              successful ones fails as if the device were out of memory;
+ *   what = 1 : the sweep-kernel launch after `after` more is not made and
+ *              reports a device error (EDEVICE, which poisons the handle).
+ * after < 0 disarms it.  Once triggered it disarms itself.  A failed
+ * allocation is reported before the call changes the handle's state: ENOMEM
+ * leaves factors and residual as they were and the handle usable (a failed
+ * ccdpp_create frees everything and leaves *out untouched).  Returns EINVAL
+ * for another `what`. */
+int ccdpp_debug_inject(int32_t what, int64_t after);
 
 /* Human-readable message of the last failure on this handle; with h == NULL,
  * of the last failed ccdpp_create on this thread.  Never NULL. */

@@ -90,6 +90,7 @@ def lib() -> ctypes.CDLL:
             "ccdpp_profile_read": ([P, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(dbl),
                                     ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_info": ([P, ctypes.POINTER(i64), i32], ctypes.c_int),
+            "ccdpp_debug_inject": ([i32, i64], ctypes.c_int),
             "ccdpp_last_error": ([P], ctypes.c_char_p),
             "ccdpp_destroy": ([P], None),
         }
@@ -105,7 +106,7 @@ def declared_symbols() -> list[str]:
     """Function names declared in include/ccdpp.h."""
     with open(HEADER) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(ccdpp_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(ccdpp_[a-z0-9_]+)\s*\(", text)))
 
 
 def _p(a):
@@ -262,6 +263,12 @@ def ccdpp_info(h):
     buf = (ctypes.c_int64 * len(INFO_FIELDS))()
     w = _check(h, lib().ccdpp_info(h, buf, len(INFO_FIELDS)))
     return {INFO_FIELDS[i]: int(buf[i]) for i in range(w)}
+
+
+def ccdpp_debug_inject(what, after):
+    """Testing hook of the error paths: what 0 fails the device allocation after
+    `after` more, what 1 the sweep launch after `after` more; after < 0 disarms."""
+    _check(None, lib().ccdpp_debug_inject(int(what), int(after)))
 
 
 def ccdpp_last_error(h=None):

@@ -9,6 +9,7 @@
 // only enqueues kernels on one stream, and ccdpp_run synchronises once at the
 // end.
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <cstdarg>
@@ -24,7 +25,23 @@ namespace {
 
 thread_local std::string g_create_error;
 
-constexpr int64_t kMaxDim = int64_t(1) << 30;
+// Failures forced from the host for tests of the error paths (ccdpp_debug_inject):
+// the device allocation, or the sweep-kernel launch, after this many more
+// successful ones fails (-1: never).
+std::atomic<int64_t> g_inject_alloc{-1};
+std::atomic<int64_t> g_inject_launch{-1};
+
+// True when the countdown c reaches this event (and disarms it).
+bool injected(std::atomic<int64_t>& c) {
+    int64_t v = c.load();
+    while (v >= 0) {
+        if (c.compare_exchange_weak(v, v - 1)) return v == 0;
+    }
+    return false;
+}
+
+// Gathers address records of up to 16 bytes per column with 32-bit byte offsets.
+constexpr int64_t kMaxDim = int64_t(1) << 28;
 constexpr int64_t kMaxNnz = INT32_MAX;
 // Residual streams (values and indices of both copies) up to this size stay in
 // MI355X's 256 MB memory-side cache from one pass to the next when the passes
@@ -40,6 +57,15 @@ struct ProfEvent {
 };
 
 }  // namespace
+
+// Every device allocation of the library goes through here.
+hipError_t ccdk::dev_malloc(void** p, size_t bytes) {
+    if (injected(g_inject_alloc)) {
+        *p = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    return hipMalloc(p, bytes);
+}
 
 struct ccdpp {
     int64_t m = 0, n = 0, nnz = 0;
@@ -140,7 +166,7 @@ template <class T>
 hipError_t dalloc(ccdpp* h, T** p, int64_t count) {
     size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
     void* q = nullptr;
-    hipError_t e = hipMalloc(&q, bytes);
+    hipError_t e = ccdk::dev_malloc(&q, bytes);
     if (e != hipSuccess) return e;
     h->allocs.push_back(q);
     h->bytes_held += (int64_t)bytes;
@@ -165,7 +191,7 @@ struct Tmp {
 };
 template <class T>
 hipError_t talloc(Tmp& t, T** p, int64_t count) {
-    hipError_t e = hipMalloc(&t.p, (size_t)std::max<int64_t>(count, 1) * sizeof(T));
+    hipError_t e = ccdk::dev_malloc(&t.p, (size_t)std::max<int64_t>(count, 1) * sizeof(T));
     *p = static_cast<T*>(t.p);
     return e;
 }
@@ -968,6 +994,8 @@ int pass(ccdpp* h, int li, ccdk::PassMode mode, const V* x, int32_t pcol, int32_
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
                                                 : CCDPP_K_PASS_FUSED;
     const double vb = sizeof(V);
+    if (injected(g_inject_launch))
+        return fail(h, CCDPP_EDEVICE, "sweep launch failed (forced by ccdpp_debug_inject)");
     {
         Timed tm(h, kind, li, pass_bytes(L, mode, gathered, vb));
         HIPCK(h, ccdk::launch_pass<V>(*Lp, mode, x, seg_col<V>(h, li, pcol), seg_col<V>(h, li, ppcol),
@@ -992,7 +1020,7 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
     g_create_error.clear();
     if (!out) return fail(nullptr, CCDPP_EINVAL, "out is NULL");
     if (m < 1 || m >= kMaxDim || n < 1 || n >= kMaxDim)
-        return fail(nullptr, CCDPP_EINVAL, "m and n must be in [1, 2^30)");
+        return fail(nullptr, CCDPP_EINVAL, "m and n must be in [1, 2^28)");
     if (k < 1) return fail(nullptr, CCDPP_EINVAL, "k must be >= 1");
     if (!std::isfinite(lambda) || lambda < 0.0)
         return fail(nullptr, CCDPP_EINVAL, "lambda must be finite and >= 0");
@@ -1081,9 +1109,17 @@ int ccd_impl(ccdpp* h, int32_t outer) {
     h->wb_stores = false;
     if (outer > 0 && !h->slot01) {
         // Slot-to-slot maps between the copies, for the residual refresh after each phase.
+        // Both maps are allocated before the handle keeps either, so a failed
+        // allocation leaves the handle as it was.
         int32_t *s01, *s10;
-        HIPCK(h, dalloc(h, &s01, h->L[0].npad));
-        HIPCK(h, dalloc(h, &s10, h->L[1].npad));
+        Tmp t01, t10;
+        HIPCK(h, talloc(t01, &s01, h->L[0].npad));
+        HIPCK(h, talloc(t10, &s10, h->L[1].npad));
+        for (Tmp* t : {&t01, &t10}) {
+            h->allocs.push_back(t->p);
+            t->p = nullptr;
+        }
+        h->bytes_held += 4 * (h->L[0].npad + h->L[1].npad);
         HIPCK(h, hipMemsetAsync(s01, 0xFF, (size_t)h->L[0].npad * 4, h->stream));
         HIPCK(h, hipMemsetAsync(s10, 0xFF, (size_t)h->L[1].npad * 4, h->stream));
         HIPCK(h, launch_slot_map(h->pos0, h->map01, h->nnz, s01, h->stream));
@@ -1211,26 +1247,22 @@ template <class S>
 int get_factors_impl(ccdpp* h, S* W, S* H) {
     if (!usable(h)) return CCDPP_ESTATE;
     hipStream_t s = h->stream;
-    return with_value_type(h, [&](auto z) -> int {
+    // Both staging buffers first, so that an error leaves W and H untouched.
+    S *dW = nullptr, *dH = nullptr;
+    Tmp tw, th;
+    if (W) HIPCK(h, talloc(tw, &dW, h->m * h->k));
+    if (H) HIPCK(h, talloc(th, &dH, h->n * h->k));
+    RCK(with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
-        if (W) {
-            S* d;
-            Tmp t;
-            HIPCK(h, talloc(t, &d, h->m * h->k));
-            HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->W), h->rold2new, h->m, h->k, d, s)));
-            HIPCK(h, hipMemcpyAsync(W, d, h->m * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
-            HIPCK(h, hipStreamSynchronize(s));
-        }
-        if (H) {
-            S* d;
-            Tmp t;
-            HIPCK(h, talloc(t, &d, h->n * h->k));
-            HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->H), h->cold2new, h->n, h->k, d, s)));
-            HIPCK(h, hipMemcpyAsync(H, d, h->n * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
-            HIPCK(h, hipStreamSynchronize(s));
-        }
+        if (W) HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->W), h->rold2new, h->m, h->k, dW, s)));
+        if (H) HIPCK(h, (ccdk::launch_gather_factor_out<V, S>(as<V>(h->H), h->cold2new, h->n, h->k, dH, s)));
+        HIPCK(h, hipStreamSynchronize(s));
         return CCDPP_OK;
-    });
+    }));
+    if (W) HIPCK(h, hipMemcpyAsync(W, dW, h->m * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
+    if (H) HIPCK(h, hipMemcpyAsync(H, dH, h->n * h->k * sizeof(S), hipMemcpyDeviceToHost, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    return CCDPP_OK;
 }
 
 template <class S>
@@ -1245,24 +1277,18 @@ int set_factors_impl(ccdpp* h, const S* W, const S* H) {
             if (!std::isfinite(H[e]))
                 return fail(h, CCDPP_EINVAL, "H[%lld] is not finite", (long long)e);
     hipStream_t s = h->stream;
+    // Staging buffers first: a failed allocation leaves the factors and the residual
+    // as they were.
+    S *dW = nullptr, *dH = nullptr;
+    Tmp tw, th;
+    if (W) HIPCK(h, talloc(tw, &dW, h->m * h->k));
+    if (H) HIPCK(h, talloc(th, &dH, h->n * h->k));
+    if (W) HIPCK(h, hipMemcpyAsync(dW, W, h->m * h->k * sizeof(S), hipMemcpyHostToDevice, s));
+    if (H) HIPCK(h, hipMemcpyAsync(dH, H, h->n * h->k * sizeof(S), hipMemcpyHostToDevice, s));
     RCK(with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
-        if (W) {
-            S* d;
-            Tmp t;
-            HIPCK(h, talloc(t, &d, h->m * h->k));
-            HIPCK(h, hipMemcpyAsync(d, W, h->m * h->k * sizeof(S), hipMemcpyHostToDevice, s));
-            HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(d, h->rnew2old, h->m, h->k, as<V>(h->W), s)));
-            HIPCK(h, hipStreamSynchronize(s));
-        }
-        if (H) {
-            S* d;
-            Tmp t;
-            HIPCK(h, talloc(t, &d, h->n * h->k));
-            HIPCK(h, hipMemcpyAsync(d, H, h->n * h->k * sizeof(S), hipMemcpyHostToDevice, s));
-            HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(d, h->cnew2old, h->n, h->k, as<V>(h->H), s)));
-            HIPCK(h, hipStreamSynchronize(s));
-        }
+        if (W) HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(dW, h->rnew2old, h->m, h->k, as<V>(h->W), s)));
+        if (H) HIPCK(h, (ccdk::launch_scatter_factor_in<S, V>(dH, h->cnew2old, h->n, h->k, as<V>(h->H), s)));
         RCK(spread_factors(h));
         HIPCK(h, ccdk::launch_rebuild_residual<V>(h->L[0], h->pos0, as<V>(h->A), as<V>(h->W),
                                                   as<V>(h->H), h->m, h->n, h->k, s));
@@ -1281,11 +1307,11 @@ int get_residual_impl(ccdpp* h, S* R) {
     if (!usable(h)) return CCDPP_ESTATE;
     if (!R && h->nnz) return fail(h, CCDPP_EINVAL, "R is NULL");
     if (h->nnz == 0) return CCDPP_OK;
-    RCK(flush_pending(h));
     hipStream_t s = h->stream;
     S* d;
     Tmp t;
     HIPCK(h, talloc(t, &d, h->nnz));
+    RCK(flush_pending(h));
     RCK(with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
         HIPCK(h, (ccdk::launch_copy_mapped<V, S>(as<V>(h->L[0].val), h->pos0, d, h->perm0, h->nnz, s)));
@@ -1554,6 +1580,16 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     int32_t w = std::min<int32_t>(len, 27);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
+}
+
+int ccdpp_debug_inject(int32_t what, int64_t after) {
+    if (what == 0)
+        g_inject_alloc.store(after < 0 ? -1 : after);
+    else if (what == 1)
+        g_inject_launch.store(after < 0 ? -1 : after);
+    else
+        return CCDPP_EINVAL;
+    return CCDPP_OK;
 }
 
 const char* ccdpp_last_error(const ccdpp_t* h) {

@@ -549,7 +549,7 @@ hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, i
     if (need > *tmp_bytes) {
         if (*tmp) hipFree(*tmp);
         *tmp = nullptr;
-        e = hipMalloc(tmp, need);
+        e = dev_malloc(tmp, need);
         if (e != hipSuccess) return e;
         *tmp_bytes = need;
     }

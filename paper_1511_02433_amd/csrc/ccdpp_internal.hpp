@@ -300,6 +300,10 @@ struct Layout {
     int32_t grid = 0;                // persistent workgroups per pass
 };
 
+// Every device allocation of the library (api.hip); a host-forced failure for tests
+// of the error paths returns hipErrorOutOfMemory.
+hipError_t dev_malloc(void** p, size_t bytes);
+
 // Launchers (sweep.hip), instantiated for V = float and V = double.
 hipError_t sweep_init();  // raise the dynamic-LDS limit of the staged kernels
 template <class V>

@@ -20,6 +20,7 @@ def test_every_declared_function_is_exported():
     L = _lib_or_skip()
     names = C.declared_symbols()
     assert len(names) >= 15
+    assert "ccdpp_get_factors_f64" in names and "ccdpp_debug_inject" in names
     for name in names:
         assert hasattr(L, name), name
     # and the binding knows a signature for each of them
@@ -36,6 +37,8 @@ def _create(m=10, n=8, k=2, lam=0.1, row=(0, 1), col=(0, 1), val=(1.0, 2.0), opt
     (dict(m=0), "m and n"),
     (dict(n=0), "m and n"),
     (dict(m=1 << 30), "m and n"),
+    (dict(m=1 << 28), "m and n"),
+    (dict(n=1 << 28), "m and n"),
     (dict(k=0), "k must be"),
     (dict(lam=-1.0), "lambda"),
     (dict(lam=float("nan")), "lambda"),
@@ -95,6 +98,14 @@ def test_null_pointers_and_handles():
     buf = (ctypes.c_int64 * 4)()
     assert L.ccdpp_info(None, buf, 4) == C.CCDPP_ESTATE
     L.ccdpp_destroy(None)
+
+
+def test_debug_inject_arguments():
+    L = _lib_or_skip()
+    assert L.ccdpp_debug_inject(2, 0) == C.CCDPP_EINVAL
+    for what in (0, 1):
+        assert L.ccdpp_debug_inject(what, 5) == C.CCDPP_OK
+        assert L.ccdpp_debug_inject(what, -1) == C.CCDPP_OK  # disarmed again
 
 
 def test_without_a_device_create_reports_edevice():

@@ -51,3 +51,31 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
+
+
+LARGE = dict(INFO, m=480_189, n=17_770, nnz=100_480_507)
+
+
+def test_model_bytes_follow_the_byte_model():
+    # Plain pass over the user-major copy of the large matrix: 8 B per entry (4-byte
+    # index, 4-byte value), row pointers, coordinates, one gathered vector.
+    N, m, n = 100_480_507, 480_189, 17_770
+    assert bench.model_bytes(1, 0, LARGE) == 8 * N + 4 * (m + 1) + 4 * m + 4 * n
+    assert abs(bench.model_bytes(1, 0, LARGE) / 1e6 - 807.8) < 0.05
+    # A first pass writes the residual back (12 B per entry), reads two per-row scalars
+    # and gathers two (user-major) or three (item-major) vectors.
+    assert bench.model_bytes(0, 0, LARGE) == 12 * N + 4 * (m + 1) + 4 * m + 8 * m + 8 * n
+    assert bench.model_bytes(0, 1, LARGE) == 12 * N + 4 * (n + 1) + 4 * n + 8 * n + 12 * m
+    # The flush reads and writes the residual, one per-row scalar and one vector.
+    assert bench.model_bytes(4, 1, LARGE) == 12 * N + 4 * (n + 1) + 4 * n + 4 * m
+    # Doubles: 8-byte values and factor entries, still 4-byte indices.
+    d = dict(LARGE, value_bytes=8)
+    assert bench.model_bytes(1, 1, d) == 12 * N + 4 * (n + 1) + 8 * n + 8 * m
+    assert bench.model_bytes(2, 1, LARGE) is None  # the combine is not a pass
+
+
+def test_host_threads_reports_the_host():
+    h = bench.host_threads()
+    assert h["cores_all"] == os.cpu_count()
+    assert 1 <= h["threads"] <= h["affinity"] <= h["cores_all"]
+    assert h["cpu_model"] is None or isinstance(h["cpu_model"], str)
