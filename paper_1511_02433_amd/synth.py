@@ -184,12 +184,30 @@ def _sample_positions(deg: np.ndarray, q: np.ndarray, rng: np.random.Generator,
     krow = keys // n
     got = np.bincount(krow, minlength=m)
     deficit = np.where(heavy, 0, deg - got)
-    # Rows already complete leave the working set; only deficient rows are redrawn.
+    # Rows already complete are set aside; only deficient rows are redrawn.  Their
+    # entries are kept as one sorted array (`work`) plus a smaller sorted array of the
+    # entries added since it was last merged (`fresh`), so that a round costs about
+    # as much as its own draws; each row remembers the round that completed it.
     short = deficit > 0
     sel = short[krow]
-    done = [keys[~sel]]
+    done0 = keys[~sel]
     work = keys[sel]
     del keys, krow, sel
+    fresh = np.zeros(0, dtype=np.int64)
+    fin_round = np.zeros(m, dtype=np.int32)
+
+    def held_in(arr, x):
+        if arr.size == 0:
+            return np.zeros(x.size, dtype=bool)
+        pos = np.searchsorted(arr, x)
+        h = np.zeros(x.size, dtype=bool)
+        inside = pos < arr.size
+        h[inside] = arr[pos[inside]] == x[inside]
+        return h
+
+    def merged(a, b):
+        return np.insert(a, np.searchsorted(a, b), b)
+
     rounds = 0
     while deficit.sum() > 0:
         rounds += 1
@@ -197,16 +215,25 @@ def _sample_positions(deg: np.ndarray, q: np.ndarray, rng: np.random.Generator,
         add_u = _sorted_uniforms(deficit[bad], rng)
         add_c = np.minimum(np.searchsorted(cdf, add_u, side="right"), n - 1).astype(np.int64)
         add_r = np.repeat(bad.astype(np.int64), deficit[bad])
-        work = np.unique(np.concatenate([work, add_r * n + add_c]))
-        wrow = work // n
-        got = np.bincount(wrow, minlength=m)
-        deficit = np.zeros(m, dtype=np.int64)
-        deficit[bad] = deg[bad] - got[bad]
-        fin = deficit[wrow] == 0
-        done.append(work[fin])
-        work = work[~fin]
+        # The draws come sorted (rows ascending, columns ascending inside a row).
+        add = add_r * n + add_c
+        del add_u, add_c, add_r
+        keep = np.ones(add.size, dtype=bool)
+        keep[1:] = add[1:] != add[:-1]
+        add = add[keep]
+        add = add[~(held_in(work, add) | held_in(fresh, add))]
+        fresh = merged(fresh, add)
+        if fresh.size > work.size // 8:
+            work = merged(work, fresh)
+            fresh = np.zeros(0, dtype=np.int64)
+        deficit[bad] -= np.bincount(add // n, minlength=m)[bad]
+        fin_round[bad[deficit[bad] == 0]] = rounds
         if rounds > 10_000:
             raise RuntimeError("successive sampling did not converge")
+    work = merged(work, fresh)
+    # Rows in the order they were completed, each row's entries in column order.
+    done = [done0, work[np.argsort(fin_round[work // n], kind="stable")]]
+    del work, fresh
     keys = np.concatenate(done)
     _log(f"positions: {keys.size + sum(c.size for c in cols_out)} drawn, {rounds} top-up rounds", verbose)
     rows_out.append((keys // n).astype(np.int32))
