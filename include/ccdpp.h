@@ -209,6 +209,25 @@ int ccdpp_set_factors_f64(ccdpp_t *h, const double *W, const double *H);
 int ccdpp_rmse(ccdpp_t *h, int64_t nnz, const int32_t *row, const int32_t *col,
                const float *val, double *rmse_out);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): ccdpp_rmse with the
+ * held-out triplets already in DEVICE memory, on the handle's device.  It
+ * allocates nothing: its partial sums live in a fixed device array of
+ * 16,400 bytes (1024 partial sums, 1024 per-block counts, two totals), one per
+ * device the library has run on, held until the process ends.  Every call on
+ * one device shares that array, so calls that overlap on one device (two
+ * handles on two streams) race; calls in sequence do not.
+ *   row, col : device int32[nnz] held-out positions
+ *   val      : device float32[nnz] held-out ratings
+ *   nnz      : 1 <= nnz <= 2^31 - 1; the array's size does not depend on it
+ *   rmse_out : receives the RMSE (host memory)
+ * The triplets are checked on the device: entries out of range or not finite are
+ * never used as indices, and any such entry makes the call return EINVAL.  On
+ * valid triplets the result is bitwise that of ccdpp_rmse (the same kernel and
+ * the same fixed order).  Blocking. */
+int ccdpp_rmse_noalloc(ccdpp_t *h, int64_t nnz, const int32_t *row, const int32_t *col,
+                       const float *val, double *rmse_out);
+
 /* Training RMSE of the current factors: the RMSE of Section 8 evaluated on
  * the training set itself, from the residual of Section 3.2
  * (R_ij = A_ij - w_i^T h_j on Omega, kept up to date by eq. 18):

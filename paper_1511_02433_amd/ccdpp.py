@@ -79,6 +79,7 @@ def lib() -> ctypes.CDLL:
             "ccdpp_set_factors": ([P, P, P], ctypes.c_int),
             "ccdpp_set_factors_f64": ([P, P, P], ctypes.c_int),
             "ccdpp_rmse": ([P, i64, P, P, P, ctypes.POINTER(dbl)], ctypes.c_int),
+            "ccdpp_rmse_noalloc": ([P, i64, P, P, P, ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_train_rmse": ([P, ctypes.POINTER(dbl)], ctypes.c_int),
             "ccdpp_get_residual": ([P, P], ctypes.c_int),
             "ccdpp_get_residual_f64": ([P, P], ctypes.c_int),
@@ -202,6 +203,16 @@ def ccdpp_rmse(h, row, col, val):
     val = np.ascontiguousarray(val, dtype=np.float32)
     out = ctypes.c_double()
     _check(h, lib().ccdpp_rmse(h, int(row.size), _p(row), _p(col), _p(val), ctypes.byref(out)))
+    return out.value
+
+
+def ccdpp_rmse_noalloc(h, nnz, row_ptr, col_ptr, val_ptr):
+    """Held-out RMSE from triplets in device memory (device addresses, e.g. torch's
+    data_ptr() of int32, int32 and float32 tensors); allocates no device memory."""
+    out = ctypes.c_double()
+    _check(h, lib().ccdpp_rmse_noalloc(h, int(nnz), ctypes.c_void_p(row_ptr),
+                                       ctypes.c_void_p(col_ptr), ctypes.c_void_p(val_ptr),
+                                       ctypes.byref(out)))
     return out.value
 
 
@@ -333,6 +344,9 @@ class CCDPP:
 
     def rmse(self, row, col, val):
         return ccdpp_rmse(self._h, row, col, val)
+
+    def rmse_noalloc(self, nnz, row_ptr, col_ptr, val_ptr):
+        return ccdpp_rmse_noalloc(self._h, nnz, row_ptr, col_ptr, val_ptr)
 
     def train_rmse(self):
         return ccdpp_train_rmse(self._h)

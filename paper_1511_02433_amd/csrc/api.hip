@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <mutex>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -67,6 +68,25 @@ hipError_t ccdk::dev_malloc(void** p, size_t bytes) {
     return hipMalloc(p, bytes);
 }
 
+// ---- scratch of the allocation-free entry point (ccdpp_rmse_noalloc) --------------
+// kReduceParts partial sums of squared errors, as many per-block counts of rejected
+// triplets, then the two totals: 2 * 1024 + 2 doubles, 16,400 bytes, held on every
+// device the library runs on until the process ends.  Every call on a device shares
+// that device's copy; each call overwrites all of it before reading it.
+namespace {
+constexpr int kNaPart = 0;                       // [kReduceParts] squared-error partials
+constexpr int kNaRejected = kReduceParts;        // [kReduceParts] rejected-entry counts
+constexpr int kNaTotals = 2 * kReduceParts;      // [2] their totals
+constexpr int kNaDoubles = 2 * kReduceParts + 2;
+constexpr int kMaxDevices = 64;
+}  // namespace
+static __device__ __align__(256) double scratch[kNaDoubles];
+
+namespace {
+std::mutex g_scratch_mu;
+double* g_scratch_dev[kMaxDevices] = {};  // the device address of `scratch` per device
+}  // namespace
+
 struct ccdpp {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t k = 0;
@@ -99,6 +119,7 @@ struct ccdpp {
     int32_t sse_nparts = 0;
     double* d_scalar = nullptr;
     unsigned long long* d_count = nullptr;
+    double* scratch = nullptr;     // device address of this device's `scratch` array
     int32_t pending = -1;          // feature whose eq. 18 subtract is still folded into R-hat
     double train_sse = 0.0;
     bool train_sse_valid = false;
@@ -770,6 +791,20 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
                     prop.sharedMemPerBlock, kLdsBytes);
     h->cus = prop.multiProcessorCount;
     HIPCK(h, sweep_init());
+    // The device address of the allocation-free entry point's scratch, looked up once
+    // per device with that device current (host code never uses the array's name).
+    if (h->device < 0 || h->device >= kMaxDevices)
+        return fail(h, CCDPP_EDEVICE, "device %d: the library serves devices 0..%d", h->device,
+                    kMaxDevices - 1);
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (!g_scratch_dev[h->device]) {
+            void* p = nullptr;
+            HIPCK(h, hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+            g_scratch_dev[h->device] = static_cast<double*>(p);
+        }
+        h->scratch = g_scratch_dev[h->device];
+    }
     HIPCK(h, hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
     h->stream = h->own_stream;
     hipStream_t s = h->stream;
@@ -1083,11 +1118,12 @@ int launch_sq_sum_any(ccdpp* h, void* p, int64_t n) {
     });
 }
 int launch_test_err_any(ccdpp* h, const int32_t* dr, const int32_t* dc, const float* dv,
-                        int64_t nnz) {
+                        int64_t nnz, double* part = nullptr, double* rejected = nullptr) {
     return with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
         HIPCK(h, ccdk::launch_test_err<V>(dr, dc, dv, nnz, h->rold2new, h->cold2new, as<V>(h->W),
-                                          as<V>(h->H), h->m, h->n, h->k, h->sse_part, kReduceParts,
+                                          as<V>(h->H), h->m, h->n, h->k,
+                                          part ? part : h->sse_part, kReduceParts, rejected,
                                           h->stream));
         return CCDPP_OK;
     });
@@ -1460,6 +1496,29 @@ int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, 
     HIPCK(h, hipMemcpyAsync(&sum, h->d_scalar, 8, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
     *rmse_out = std::sqrt(sum / (double)nnz);
+    return CCDPP_OK;
+}
+
+int ccdpp_rmse_noalloc(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col,
+                       const float* val, double* rmse_out) {
+    if (!usable(h)) return CCDPP_ESTATE;
+    if (!rmse_out) return fail(h, CCDPP_EINVAL, "rmse_out is NULL");
+    if (nnz < 1 || nnz > kMaxNnz) return fail(h, CCDPP_EINVAL, "nnz must be in [1, 2^31-1]");
+    if (!row || !col || !val) return fail(h, CCDPP_EINVAL, "row, col and val must be non-NULL");
+    if (!h->scratch) return fail(h, CCDPP_ESTATE, "no scratch address on this device");
+    hipStream_t s = h->stream;
+    double* sc = h->scratch;
+    // The same kernel as ccdpp_rmse with the triplets checked on the device (they
+    // cannot be checked on the host), partials and counts in the scratch array.
+    RCK(launch_test_err_any(h, row, col, val, nnz, sc + kNaPart, sc + kNaRejected));
+    HIPCK(h, ccdk::launch_reduce_sum(sc + kNaPart, kReduceParts, sc + kNaTotals, s));
+    HIPCK(h, ccdk::launch_reduce_sum(sc + kNaRejected, kReduceParts, sc + kNaTotals + 1, s));
+    double tot[2] = {0.0, 0.0};
+    HIPCK(h, hipMemcpyAsync(tot, sc + kNaTotals, sizeof tot, hipMemcpyDeviceToHost, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    if (tot[1] != 0.0)
+        return fail(h, CCDPP_EINVAL, "%.0f held-out entries are out of range or not finite", tot[1]);
+    *rmse_out = std::sqrt(tot[0] / (double)nnz);
     return CCDPP_OK;
 }
 

@@ -299,24 +299,43 @@ __global__ void k_sq_sum(const V* __restrict__ v, int64_t n, double* __restrict_
     block_total(acc, &part[blockIdx.x]);
 }
 
-template <class V>
+// Squared prediction errors of held-out triplets, one fixed-order partial per block.
+// CHECK: the triplets were not validated on the host; an entry whose indices are out
+// of range or whose value is not finite is skipped (never used as an index) and
+// counted in rejected[blockIdx.x].  Valid entries take the same arithmetic in the
+// same order either way.
+template <class V, bool CHECK>
 __global__ void k_test_err(const int32_t* __restrict__ row, const int32_t* __restrict__ col,
                            const float* __restrict__ val, int64_t nnz,
                            const int32_t* __restrict__ rnew, const int32_t* __restrict__ cnew,
                            const V* __restrict__ W, const V* __restrict__ H, int64_t m,
-                           int64_t n, int32_t k, double* __restrict__ part) {
+                           int64_t n, int32_t k, double* __restrict__ part,
+                           double* __restrict__ rejected) {
     double acc = 0.0;
+    double bad = 0.0;
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
          e += (int64_t)gridDim.x * kT) {
-        const int64_t i = rnew[row[e]];
-        const int64_t j = cnew[col[e]];
+        const int32_t r = row[e], c = col[e];
+        const float a = val[e];
+        if constexpr (CHECK) {
+            if (r < 0 || (int64_t)r >= m || c < 0 || (int64_t)c >= n || !__builtin_isfinite(a)) {
+                bad += 1.0;
+                continue;
+            }
+        }
+        const int64_t i = rnew[r];
+        const int64_t j = cnew[c];
         double pred = 0.0;
         for (int32_t t = 0; t < k; ++t)
             pred = __builtin_fma((double)W[(int64_t)t * m + i], (double)H[(int64_t)t * n + j], pred);
-        const double err = (double)val[e] - pred;
+        const double err = (double)a - pred;
         acc = __builtin_fma(err, err, acc);
     }
     block_total(acc, &part[blockIdx.x]);
+    if constexpr (CHECK) {
+        __syncthreads();  // block_total's LDS is reused
+        block_total(bad, &rejected[blockIdx.x]);
+    }
 }
 
 }  // namespace
@@ -496,9 +515,13 @@ template <class V>
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,
                            const int32_t* rold2new, const int32_t* cold2new, const V* W,
                            const V* H, int64_t m, int64_t n, int32_t k, double* part,
-                           int32_t nparts, hipStream_t s) {
-    hipLaunchKernelGGL(k_test_err<V>, dim3(nparts), dim3(kT), 0, s, row, col, val, nnz, rold2new,
-                       cold2new, W, H, m, n, k, part);
+                           int32_t nparts, double* rejected, hipStream_t s) {
+    if (rejected)
+        hipLaunchKernelGGL((k_test_err<V, true>), dim3(nparts), dim3(kT), 0, s, row, col, val, nnz,
+                           rold2new, cold2new, W, H, m, n, k, part, rejected);
+    else
+        hipLaunchKernelGGL((k_test_err<V, false>), dim3(nparts), dim3(kT), 0, s, row, col, val, nnz,
+                           rold2new, cold2new, W, H, m, n, k, part, nullptr);
     return hipGetLastError();
 }
 
@@ -530,7 +553,7 @@ hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* 
     template hipError_t launch_test_err<V>(const int32_t*, const int32_t*, const float*,        \
                                            int64_t, const int32_t*, const int32_t*, const V*,   \
                                            const V*, int64_t, int64_t, int32_t, double*,        \
-                                           int32_t, hipStream_t);
+                                           int32_t, double*, hipStream_t);
 CCDK_BUILD_INSTANTIATE(float)
 CCDK_BUILD_INSTANTIATE(double)
 #undef CCDK_BUILD_INSTANTIATE

@@ -367,11 +367,14 @@ hipError_t launch_seg_spread(const V* F, int64_t rows, const int32_t* seg_row, i
                              int32_t k, V* out, hipStream_t s);
 template <class V>
 hipError_t launch_sq_sum(const V* v, int64_t n, double* part, int32_t nparts, hipStream_t s);
+// Squared errors of held-out triplets into part[0 .. nparts); with `rejected`, the
+// triplets are checked on the device and entries out of range or not finite are
+// skipped and counted per block in rejected[0 .. nparts).
 template <class V>
 hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* val, int64_t nnz,
                            const int32_t* rold2new, const int32_t* cold2new, const V* W,
                            const V* H, int64_t m, int64_t n, int32_t k, double* part,
-                           int32_t nparts, hipStream_t s);
+                           int32_t nparts, double* rejected, hipStream_t s);
 hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, int32_t* vout,
                       int64_t n, int bits, hipStream_t s, void** tmp, size_t* tmp_bytes);
 
