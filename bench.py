@@ -380,8 +380,12 @@ def main():
                      "test_rmse": None if test is None else float(hist[-1, 2])}
         log(f"open loop: {per:.3f} ms per outer iteration with monitoring "
             f"({per - ms_plain:+.3f} ms against the plain step)")
-    model_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / kinds_steps \
+    step_bytes = sum(v["algo_bytes_per_launch"] * v["launches"] for v in kinds.values()) / kinds_steps \
         if kinds else None
+    # The byte model over the passes of a step (the combine and commit kernels move
+    # O(m + n) bytes and are not part of it).
+    step_model = sum(v["model_bytes_per_launch"] * v["launches"] for v in per_layout.values()
+                     if v["model_bytes_per_launch"]) / kinds_steps if per_layout else None
     g.close()
 
     cpu = None
@@ -409,8 +413,10 @@ def main():
                    "algorithm": args.algorithm},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "model_bytes_per_step": model_bytes,
-        "model_gbs": round(model_bytes / (ms * 1e-3) / 1e9, 1) if model_bytes else None,
+        "model_bytes_per_step": step_model,
+        "model_gbs": round(step_model / (ms * 1e-3) / 1e9, 1) if step_model else None,
+        "stored_bytes_per_step": step_bytes,
+        "stored_gbs": round(step_bytes / (ms * 1e-3) / 1e9, 1) if step_bytes else None,
         "ms_per_step_without_kernel_events": round(ms_plain, 4),
         "kernels_note": ("per-kernel timings: the last warmup step" if kinds_steps == 1
                          else "per-kernel timings: the timed steps"),
