@@ -127,6 +127,15 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 lanes' sorted columns climb by at most 2047 from one entry
  *                 to the next stores its indices delta-coded, 12 bytes per 8
  *                 entries instead of 16; 1 plain 16-bit indices everywhere.
+ *   split_rows  : the item-major copy only.  0 automatic: when tiles of the
+ *                 whole copy would hold too few entries per row segment (where
+ *                 it would otherwise become hot), its leading items (the ones
+ *                 with the most ratings) may be tiled and the others kept hot,
+ *                 if their segments cost less than the gathers from global
+ *                 memory they save; -1 never split; n1 > 0 (needs
+ *                 gather_mode[1] = 0 and n1 < n) tile the n1 items with the most
+ *                 ratings, the others hot.  The two parts are passed over one
+ *                 after the other, as one pass of the copy.
  * Results differ between layouts only by floating-point summation order; the
  * cache policy and the index coding do not change them.
  */
@@ -138,6 +147,7 @@ typedef struct ccdpp_options {
     int32_t precision;
     int32_t cache[2];
     int32_t index_coding[2];
+    int32_t split_rows;
 } ccdpp_options_t;
 
 /* ccdpp_create with explicit layout options (opts may be NULL). */
@@ -294,7 +304,11 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   [21..22] the cache policy of the user-major and item-major copies
  *   (numbered as ccdpp_options_t.cache: 1, 2 or 3), [23] user-major windows
  *   (512 entries) with delta-coded indices, [24] its windows, [25..26] the
- *   same two for the item-major copy.
+ *   same two for the item-major copy, [27] the items of a split item-major copy
+ *   that are tiled (0: not split; fields 10..14, 19..22 and 25..26 then describe
+ *   that tiled part), [28..34] the hot part of a split copy: gather mode, hot
+ *   width, workgroups, segments, rows finished in the pass, rows combined,
+ *   cache policy (zeros when not split).
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

@@ -31,12 +31,14 @@ class Options(ctypes.Structure):
     _fields_ = [("gather_mode", ctypes.c_int32 * 2), ("tile_width", ctypes.c_int32 * 2),
                 ("workgroups", ctypes.c_int32), ("seg_weight", ctypes.c_int32),
                 ("precision", ctypes.c_int32), ("cache", ctypes.c_int32 * 2),
-                ("index_coding", ctypes.c_int32 * 2)]
+                ("index_coding", ctypes.c_int32 * 2), ("split_rows", ctypes.c_int32)]
 
 
 def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight=0,
-                 precision=0, cache=(0, 0), index_coding=(0, 0)) -> Options:
-    """precision: 0 float32 residual and factors, 1 float64."""
+                 precision=0, cache=(0, 0), index_coding=(0, 0), split_rows=0) -> Options:
+    """precision: 0 float32 residual and factors, 1 float64.  split_rows: item-major
+    copy split into tiled leading items and hot others (0 automatic, -1 never, n1 > 0
+    that many tiled items)."""
     o = Options()
     o.gather_mode[0], o.gather_mode[1] = gather_mode
     o.tile_width[0], o.tile_width[1] = tile_width
@@ -45,6 +47,7 @@ def make_options(gather_mode=(0, 0), tile_width=(0, 0), workgroups=0, seg_weight
     o.precision = precision
     o.cache[0], o.cache[1] = cache
     o.index_coding[0], o.index_coding[1] = index_coding
+    o.split_rows = split_rows
     return o
 
 
@@ -267,7 +270,9 @@ INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_
                "u_workgroups", "u_segments", "v_gather", "v_tiles", "v_tile_width", "v_workgroups",
                "v_segments", "device_bytes", "value_bytes", "u_rows_finished_in_pass",
                "u_rows_combined", "v_rows_finished_in_pass", "v_rows_combined", "u_cache",
-               "v_cache", "u_delta_windows", "u_windows", "v_delta_windows", "v_windows")
+               "v_cache", "u_delta_windows", "u_windows", "v_delta_windows", "v_windows",
+               "v_split_rows", "v2_gather", "v2_tile_width", "v2_workgroups", "v2_segments",
+               "v2_rows_finished_in_pass", "v2_rows_combined", "v2_cache")
 
 
 def ccdpp_info(h):

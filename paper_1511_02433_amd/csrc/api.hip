@@ -49,6 +49,9 @@ constexpr int64_t kMaxNnz = INT32_MAX;
 // use cached accesses.
 constexpr int64_t kCachedStreamBytes = int64_t(160) << 20;
 constexpr int32_t kReduceParts = 1024;
+// A row segment of a tiled layout costs about as much as this many gathers from
+// global memory (its emission, partial and combine against one cache line each).
+constexpr int64_t kSplitSegCost = 2;
 
 struct ProfEvent {
     int kind;
@@ -95,7 +98,13 @@ struct ccdpp {
     int cus = 0;
     hipStream_t own_stream = nullptr;
     hipStream_t stream = nullptr;
-    Layout L[2];                   // 0: rows are users (eq. 15), 1: rows are items (eq. 16)
+    // 0: rows are users (eq. 15); 1: rows are items (eq. 16).  When the item-major copy
+    // is split, L[1] holds its rows 0 .. split - 1 (the items with the most ratings),
+    // tiled, and L[2] the others as a hot layout, its row r being item split + r; the
+    // two parts' values sit in one array, L[2]'s from slot off2 on.
+    Layout L[3];
+    int64_t split = 0;
+    int64_t off2 = 0;
     int32_t* rnew2old = nullptr;   // relabelled user id -> input user id
     int32_t* rold2new = nullptr;
     int32_t* cnew2old = nullptr;
@@ -110,7 +119,7 @@ struct ccdpp {
     // double with options.precision = 1.  The arrays below hold that type.
     bool dbl = false;
     void* A = nullptr;             // A[e], the rating of entry e
-    void* fseg[2] = {};            // P > 1: own factor columns spread over segments (k x S)
+    void* fseg[3] = {};            // P > 1: own factor columns spread over segments (k x S)
     void* W = nullptr;             // k x m: W[t*m + i]
     void* H = nullptr;             // k x n
     void* u = nullptr;
@@ -127,7 +136,7 @@ struct ccdpp {
     bool poisoned = false;
     int64_t build_us = 0;
     int64_t bytes_held = 0;
-    std::vector<void*> allocs;
+    std::vector<std::pair<void*, int64_t>> allocs;  // device allocations and their sizes
     // kernel timing
     bool prof = false;
     int32_t prof_kind = -1, prof_layout = -1;  // restrict timing to one kind / copy (-1: all)
@@ -189,7 +198,7 @@ hipError_t dalloc(ccdpp* h, T** p, int64_t count) {
     void* q = nullptr;
     hipError_t e = ccdk::dev_malloc(&q, bytes);
     if (e != hipSuccess) return e;
-    h->allocs.push_back(q);
+    h->allocs.emplace_back(q, (int64_t)bytes);
     h->bytes_held += (int64_t)bytes;
     *p = static_cast<T*>(q);
     return hipSuccess;
@@ -201,6 +210,22 @@ int upload(ccdpp* h, T** dst, const std::vector<T>& src) {
     if (!src.empty())
         HIPCK(h, hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
     return CCDPP_OK;
+}
+
+// Frees one of the handle's device allocations before the handle goes.
+void dfree(ccdpp* h, void* p) {
+    for (size_t i = 0; i < h->allocs.size(); ++i)
+        if (h->allocs[i].first == p) {
+            h->bytes_held -= h->allocs[i].second;
+            h->allocs.erase(h->allocs.begin() + (std::ptrdiff_t)i);
+            (void)hipFree(p);
+            return;
+        }
+}
+
+// Value slots of the item-major copy: both parts when it is split.
+int64_t item_slots(const ccdpp* h) {
+    return h->split > 0 ? h->off2 + h->L[2].npad : h->L[1].npad;
 }
 
 // Temporary device buffer freed when it goes out of scope.
@@ -255,16 +280,47 @@ void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
     for (int64_t i = 0; i < N; ++i) old2new[new2old[i]] = (int32_t)i;
 }
 
-// Build one layout.  lrow/lcol: relabelled row and gathered-column id of every
-// input triplet (device).  side 0 is the user-major copy (its first pass stages
-// q and qq, x being q), side 1 the item-major copy (first pass stages x, q, qq).
-// On return, for every entry e in layout order (padding excluded), perm[e] holds
-// its input triplet index and epos[e] the slot of its value (val_slot).
+// Rows 0 .. H - 1 of a copy (the longest: rows are relabelled by decreasing length)
+// are worth tiling when their segments cost less than the gathers from global memory
+// a hot layout would give them.  cnt holds the entries per (tile, row) of the tiled
+// layout; a row's segments are its non-empty tiles, and its entries in tiles at or
+// past `hot` columns are those a hot layout staging `hot` columns gathers from global
+// memory.  H maximises the sum of (gathers - seg_cost * segments) over the rows it
+// takes.
+int64_t choose_split(const std::vector<int32_t>& cnt, int64_t P, int64_t rows, int64_t T,
+                     int64_t hot, int64_t seg_cost) {
+    int64_t best = 0, H = 0, gain = 0;
+    for (int64_t r = 0; r < rows; ++r) {
+        int64_t segs = 0, cold = 0;
+        for (int64_t p = 0; p < P; ++p) {
+            const int32_t c = cnt[(size_t)(p * rows + r)];
+            segs += c > 0;
+            if (p * T >= hot) cold += c;
+        }
+        if (segs == 0) break;  // the empty rows come last
+        gain += cold - seg_cost * segs;
+        if (gain > best) {
+            best = gain;
+            H = r + 1;
+        }
+    }
+    return H;
+}
+
+// Build one layout of nnz entries.  lrow/lcol: relabelled row and gathered-column id
+// of every entry (device).  side 0 is the user-major copy (its first pass stages q
+// and qq, x being q), side 1 the item-major copy (first pass stages x, q, qq).  On
+// return, for every entry e in layout order (padding excluded), perm[e] holds its
+// index in lrow/lcol/val_in and epos[e] the slot of its value (val_slot).  With
+// split_out, a copy that automatic mode would make hot may instead ask to be split:
+// *split_out receives the number of leading rows to tile (0: not split), and a
+// nonzero answer returns before anything is built.
 int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, const int32_t* lrow,
                  const int32_t* lcol, const float* val_in, const ccdpp_options_t* opt,
-                 int32_t* perm, int32_t* epos, hipStream_t s) {
+                 int32_t* perm, int32_t* epos, hipStream_t s, int64_t nnz,
+                 int64_t* split_out = nullptr) {
     using namespace ccdk;
-    const int64_t N = h->nnz;
+    const int64_t N = nnz;
     L.rows = rows;
     L.cols = cols;
     L.nnz = N;
@@ -320,6 +376,14 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         int64_t nonempty = 0;
         for (int32_t c : cnt) nonempty += c > 0;
         if (nonempty > 0 && N / nonempty >= kMinTiledSeg) break;
+        if (split_out && forced == 0) {
+            // Stage the hot part's plain passes as wide as one vector allows.
+            const int64_t H = choose_split(cnt, P, rows, T, hmax, kSplitSegCost);
+            if (H > 0 && H < rows) {
+                *split_out = H;
+                return CCDPP_OK;
+            }
+        }
         mode = kGatherHot;
         T = cols;
         P = 1;
@@ -703,10 +767,10 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
 // stream the residual.  Measured on MI355X: 3% less time per outer iteration on
 // large (100M ratings), where the passes are bound by HBM; 3% more on medium (10M
 // ratings), whose cached streams leave the decoding exposed.
-int code_windows(ccdpp* h, int side, const ccdpp_options_t* opt) {
+int code_windows(ccdpp* h, int part, const ccdpp_options_t* opt) {
     using namespace ccdk;
-    Layout& L = h->L[side];
-    const int forced = opt ? opt->index_coding[side] : 0;
+    Layout& L = h->L[part];
+    const int forced = opt ? opt->index_coding[part == 0 ? 0 : 1] : 0;
     if (forced == 1 || L.gather != kGatherLds || !L.idx16 || L.npad == 0 || L.cache == kCacheAll)
         return CCDPP_OK;
     const hipStream_t s = h->stream;
@@ -726,12 +790,13 @@ int code_windows(ccdpp* h, int side, const ccdpp_options_t* opt) {
 int spread_factors(ccdpp* h) {
     return with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
-        for (int li = 0; li < 2; ++li)
-            if (h->fseg[li]) {
-                const Layout& L = h->L[li];
-                HIPCK(h, ccdk::launch_seg_spread<V>(as<V>(li == 0 ? h->W : h->H), L.rows,
-                                                    L.seg_row, L.nseg, h->k, as<V>(h->fseg[li]),
-                                                    h->stream));
+        for (int part = 0; part < 3; ++part)
+            if (h->fseg[part]) {
+                // (a tiled part's rows start at row 0 of its side)
+                const Layout& L = h->L[part];
+                HIPCK(h, ccdk::launch_seg_spread<V>(as<V>(part == 0 ? h->W : h->H),
+                                                    part == 0 ? h->m : h->n, L.seg_row, L.nseg,
+                                                    h->k, as<V>(h->fseg[part]), h->stream));
             }
         return CCDPP_OK;
     });
@@ -752,10 +817,13 @@ int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
     int64_t stream = 0;
     for (const Layout& L : h->L) stream += L.npad * (vb + (L.idx16 ? 2 : 4));
     bool stores_given = false;
-    for (int li = 0; li < 2; ++li) {
-        Layout& L = h->L[li];
+    for (int part = 0; part < 3; ++part) {
+        Layout& L = h->L[part];
+        const int li = part == 0 ? 0 : 1;
+        if (L.npad == 0 && part == 2) break;  // the item-major copy is not split
         const bool eligible = !h->dbl && L.gather == kGatherLds;
-        const int forced = opt ? opt->cache[li] : 0;
+        int forced = opt ? opt->cache[li] : 0;
+        if (part == 2 && forced > 1) forced = 1;  // a split copy's hot part always streams
         h->cache_auto[li] = forced == 0;
         if (forced > 1 && !eligible)
             return fail(h, CCDPP_EINVAL, "cache policy %d needs a tiled float copy", forced);
@@ -772,6 +840,96 @@ int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
             L.cache = kCacheStream;
         }
     }
+    return CCDPP_OK;
+}
+
+// The item-major copy: one layout, or, when the automatic choice (or
+// options.split_rows) splits it, its leading items tiled (L[1]) and the others hot
+// (L[2]).  lrow: relabelled item of every triplet, lcol: relabelled user.  perm1 and
+// pos1 as for build_layout, over the two parts in turn (heavy entries first), with
+// the light part's slots offset by off2 into the one value array of the copy.
+int build_item_major(ccdpp* h, const int32_t* lrow, const int32_t* lcol, const float* val,
+                     const ccdpp_options_t* opt, int32_t* perm1, int32_t* pos1, hipStream_t s) {
+    using namespace ccdk;
+    const int64_t m = h->m, n = h->n, N = h->nnz;
+    const int32_t forced = opt ? opt->split_rows : 0;
+    int64_t H = forced > 0 ? forced : 0;
+    if (forced == 0) {
+        RCK(build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N, &H));
+        if (H == 0) return CCDPP_OK;  // built whole
+    } else if (forced < 0) {
+        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N);
+    }
+    // The entries of the leading H items and of the others, each in input order.
+    int32_t *ih, *il;
+    int64_t* d_cnt;
+    Tmp tih, til, tcnt, ttmp;
+    size_t tmp_bytes = 0;
+    HIPCK(h, talloc(tih, &ih, N));
+    HIPCK(h, talloc(til, &il, N));
+    HIPCK(h, talloc(tcnt, &d_cnt, 2));
+    HIPCK(h, select_range(lrow, N, 0, (int32_t)H, ih, d_cnt, s, &ttmp.p, &tmp_bytes));
+    HIPCK(h, select_range(lrow, N, (int32_t)H, (int32_t)n, il, d_cnt + 1, s, &ttmp.p, &tmp_bytes));
+    int64_t cnt[2] = {0, 0};
+    HIPCK(h, hipMemcpyAsync(cnt, d_cnt, sizeof cnt, hipMemcpyDeviceToHost, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    const int64_t nh = cnt[0], nl = cnt[1];
+    if (nh + nl != N) return fail(h, CCDPP_EDEVICE, "internal: the split does not cover nnz");
+    if (nh == 0 || nl == 0) {  // one part would be empty: no split
+        ccdpp_options_t o1{};
+        if (opt) o1 = *opt;
+        o1.split_rows = -1;
+        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, &o1, perm1, pos1, s, N);
+    }
+    int32_t *rh, *ch, *rl, *cl, *ph, *qh, *pl, *ql;
+    float *vh, *vl;
+    Tmp trh, tch, tvh, trl, tcl, tvl, tph, tqh, tpl, tql;
+    HIPCK(h, talloc(trh, &rh, nh));
+    HIPCK(h, talloc(tch, &ch, nh));
+    HIPCK(h, talloc(tvh, &vh, nh));
+    HIPCK(h, talloc(trl, &rl, nl));
+    HIPCK(h, talloc(tcl, &cl, nl));
+    HIPCK(h, talloc(tvl, &vl, nl));
+    HIPCK(h, talloc(tph, &ph, nh));
+    HIPCK(h, talloc(tqh, &qh, nh));
+    HIPCK(h, talloc(tpl, &pl, nl));
+    HIPCK(h, talloc(tql, &ql, nl));
+    HIPCK(h, launch_map(ih, lrow, nh, rh, s));
+    HIPCK(h, launch_map(ih, lcol, nh, ch, s));
+    HIPCK(h, (launch_copy_mapped<float, float>(val, ih, vh, nullptr, nh, s)));
+    HIPCK(h, launch_map(il, lrow, nl, rl, s));
+    HIPCK(h, launch_add(rl, nl, -(int32_t)H, s));  // the light part's own row ids
+    HIPCK(h, launch_map(il, lcol, nl, cl, s));
+    HIPCK(h, (launch_copy_mapped<float, float>(val, il, vl, nullptr, nl, s)));
+    ccdpp_options_t oh{}, ol{};
+    if (opt) oh = ol = *opt;
+    oh.gather_mode[1] = kGatherLds;
+    ol.gather_mode[1] = kGatherHot;
+    ol.tile_width[1] = 0;
+    RCK(build_layout(h, 1, h->L[1], H, m, rh, ch, vh, &oh, ph, qh, s, nh));
+    RCK(build_layout(h, 1, h->L[2], n - H, m, rl, cl, vl, &ol, pl, ql, s, nl));
+    const int64_t off2 = h->L[1].npad + kEntryPad;
+    if (off2 + h->L[2].npad + kEntryPad > (int64_t)INT32_MAX)
+        return fail(h, CCDPP_EINVAL, "the split item-major copy exceeds 2^31 value slots");
+    // Triplet index of every entry, heavy part first; slots in the one value array.
+    HIPCK(h, launch_map(ph, ih, nh, perm1, s));
+    HIPCK(h, launch_map(pl, il, nl, perm1 + nh, s));
+    HIPCK(h, hipMemcpyAsync(pos1, qh, (size_t)nh * 4, hipMemcpyDeviceToDevice, s));
+    HIPCK(h, hipMemcpyAsync(pos1 + nh, ql, (size_t)nl * 4, hipMemcpyDeviceToDevice, s));
+    HIPCK(h, launch_add(pos1 + nh, nl, (int32_t)off2, s));
+    const size_t vb = h->dbl ? 8 : 4;
+    void* both;
+    HIPCK(h, dalloc(h, reinterpret_cast<char**>(&both), (int64_t)((off2 + h->L[2].npad + kEntryPad) * vb)));
+    HIPCK(h, hipMemcpyAsync(both, h->L[1].val, (size_t)off2 * vb, hipMemcpyDeviceToDevice, s));
+    HIPCK(h, hipMemcpyAsync(static_cast<char*>(both) + off2 * vb, h->L[2].val,
+                            (size_t)(h->L[2].npad + kEntryPad) * vb, hipMemcpyDeviceToDevice, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    dfree(h, h->L[1].val);
+    dfree(h, h->L[2].val);
+    h->L[1].val = both;
+    h->L[2].val = static_cast<char*>(both) + off2 * vb;
+    h->split = H;
+    h->off2 = off2;
     return CCDPP_OK;
 }
 
@@ -850,13 +1008,13 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     // The two copies, the ratings in user-major order and the map between copies.
     HIPCK(h, dalloc(h, &h->perm0, N));
     HIPCK(h, dalloc(h, &h->pos0, N));
-    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s));
+    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s, N));
     {
         int32_t *perm1, *pos1, *inv1, *e01;
         Tmp tp1, tq1, tinv, te;
         HIPCK(h, talloc(tp1, &perm1, N));
         HIPCK(h, talloc(tq1, &pos1, N));
-        RCK(build_layout(h, 1, h->L[1], n, m, d_ci, d_ru, d_val, opt, perm1, pos1, s));
+        RCK(build_item_major(h, d_ci, d_ru, d_val, opt, perm1, pos1, s));
         HIPCK(h, talloc(tinv, &inv1, N));
         HIPCK(h, launch_invert(perm1, N, inv1, s));
         HIPCK(h, talloc(te, &e01, N));
@@ -866,15 +1024,16 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, hipStreamSynchronize(s));
     }
     RCK(choose_cache(h, opt));
-    RCK(code_windows(h, 0, opt));
-    RCK(code_windows(h, 1, opt));
-    h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid) * kWaves, kReduceParts);
+    for (int part = 0; part < 3; ++part) RCK(code_windows(h, part, opt));
+    h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid + h->L[2].grid) * kWaves,
+                                      kReduceParts);
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
     HIPCK(h, dalloc(h, &h->d_count, 1));
-    for (int li = 0; li < 2; ++li)  // partials are written before they are read: start them as NaN
-        HIPCK(h, launch_fill<float>(static_cast<float*>(h->L[li].part), __builtin_nanf(""),
-                                    (h->dbl ? 4 : 2) * h->L[li].nslots, s));
+    for (int part = 0; part < 3; ++part)  // partials are written before they are read: start them as NaN
+        if (h->L[part].part)
+            HIPCK(h, launch_fill<float>(static_cast<float*>(h->L[part].part), __builtin_nanf(""),
+                                        (h->dbl ? 4 : 2) * h->L[part].nslots, s));
     RCK(with_value_type(h, [&](auto z) -> int {
         using V = decltype(z);
         V *A, *W, *H, *u, *v;
@@ -893,11 +1052,11 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, launch_fill<V>(W, V(0), (int64_t)h->k * m, s));
         HIPCK(h, launch_fill<V>(u, V(0), m, s));
         HIPCK(h, launch_fill<V>(v, V(0), n, s));
-        for (int li = 0; li < 2; ++li)
-            if (h->L[li].P > 1) {
+        for (int part = 0; part < 3; ++part)
+            if (h->L[part].P > 1) {
                 V* f;
-                HIPCK(h, dalloc(h, &f, (int64_t)h->k * h->L[li].nseg));
-                h->fseg[li] = f;
+                HIPCK(h, dalloc(h, &f, (int64_t)h->k * h->L[part].nseg));
+                h->fseg[part] = f;
             }
         std::vector<float> h0((size_t)n * h->k);
         for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
@@ -918,7 +1077,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
 }
 
 void destroy_all(ccdpp* h) {
-    for (void* p : h->allocs) (void)hipFree(p);
+    for (auto& a : h->allocs) (void)hipFree(a.first);
     h->allocs.clear();
     for (auto& pe : h->prof_pending) {
         h->event_pool.push_back(pe.a);
@@ -1000,50 +1159,79 @@ double pass_bytes(const Layout& L, ccdk::PassMode mode, int gathered_vectors, do
     return b;
 }
 
-// Own factor column t of layout li as the pass reads it: by segment, which with
-// P == 1 is the column itself.
+// Own factor column t of layout part `part` as the pass reads it: by segment, which
+// with P == 1 is the column itself (from the part's first row on).
 template <class V>
-V* seg_col(ccdpp* h, int li, int32_t t) {
-    const Layout& L = h->L[li];
+V* seg_col(ccdpp* h, int part, int32_t t) {
+    const Layout& L = h->L[part];
     if (t < 0) return nullptr;
-    if (L.P == 1) return as<V>(li == 0 ? h->W : h->H) + (int64_t)t * L.rows;
-    return as<V>(h->fseg[li]) + (int64_t)t * L.nseg;
+    if (L.P == 1)
+        return as<V>(part == 0 ? h->W : h->H) + (int64_t)t * (part == 0 ? h->m : h->n) +
+               (part == 2 ? h->split : 0);
+    return as<V>(h->fseg[part]) + (int64_t)t * L.nseg;
 }
 
-// One pass over layout li, then (P > 1) the combine, which also refreshes the
+// One pass over residual copy li (both parts of a split item-major copy, one after
+// the other), then the combine of the parts that need it, which also refreshes the
 // per-segment copy of column `commit` when the pass produces a committed column.
 template <class V>
 int pass(ccdpp* h, int li, ccdk::PassMode mode, const V* x, int32_t pcol, int32_t ppcol,
          const V* q, const V* qq, V* y, int32_t commit, int gathered) {
-    const Layout& L = h->L[li];
-    // Automatic write-back stores pay off only where a plain pass follows the first
-    // pass over the copy (CCD++ with inner_iters >= 2); elsewhere the copy streams.
-    Layout Ls;
-    const Layout* Lp = &L;
-    if (L.cache == ccdk::kCacheStores && h->cache_auto[li] && !h->wb_stores) {
-        Ls = L;
-        Ls.cache = ccdk::kCacheStream;
-        Lp = &Ls;
-    }
+    const int parts[2] = {li, 2};
+    const int nparts = li == 1 && h->split > 0 ? 2 : 1;
     const int kind = mode == ccdk::kModePlain ? CCDPP_K_PASS
                      : mode == ccdk::kModeFlush ? CCDPP_K_FLUSH
                                                 : CCDPP_K_PASS_FUSED;
     const double vb = sizeof(V);
     if (injected(g_inject_launch))
         return fail(h, CCDPP_EDEVICE, "sweep launch failed (forced by ccdpp_debug_inject)");
+    double bytes = 0.0, cbytes = 0.0;
+    bool combine = false;
+    for (int i = 0; i < nparts; ++i) {
+        const Layout& L = h->L[parts[i]];
+        bytes += pass_bytes(L, mode, gathered, vb);
+        if (mode != ccdk::kModeFlush && L.ncomb > 0) {
+            // Partial slots read (two values) and listed (4 B), per row a list bound, an id
+            // and y; with a committed column the segment list and the per-segment copy.
+            const bool yseg = commit >= 0 && L.P > 1;
+            cbytes += (2.0 * vb + 4.0) * L.nsrc + (8.0 + vb) * L.ncomb +
+                      (yseg ? (4.0 + vb) * L.nseg : 0.0);
+            combine = true;
+        }
+    }
     {
-        Timed tm(h, kind, li, pass_bytes(L, mode, gathered, vb));
-        HIPCK(h, ccdk::launch_pass<V>(*Lp, mode, x, seg_col<V>(h, li, pcol), seg_col<V>(h, li, ppcol),
-                                      q, qq, y, h->lambda, h->sse_part, h->stream));
+        Timed tm(h, kind, li, bytes);
+        for (int i = 0; i < nparts; ++i) {
+            const int part = parts[i];
+            const Layout& L = h->L[part];
+            // Automatic write-back stores pay off only where a plain pass follows the first
+            // pass over the copy (CCD++ with inner_iters >= 2); elsewhere the copy streams.
+            Layout Ls;
+            const Layout* Lp = &L;
+            if (L.cache == ccdk::kCacheStores && h->cache_auto[li] && !h->wb_stores) {
+                Ls = L;
+                Ls.cache = ccdk::kCacheStream;
+                Lp = &Ls;
+            }
+            const int64_t r0 = part == 2 ? h->split : 0;
+            // The flush's per-wave sums of squares: the parts' waves in turn.
+            double* sse = h->sse_part + (part == 2 ? (int64_t)h->L[1].grid * ccdk::kWaves : 0);
+            HIPCK(h, ccdk::launch_pass<V>(*Lp, mode, x, seg_col<V>(h, part, pcol),
+                                          seg_col<V>(h, part, ppcol), q, qq, y ? y + r0 : nullptr,
+                                          h->lambda, sse, h->stream));
+        }
         tm.done();
     }
-    if (mode != ccdk::kModeFlush && L.ncomb > 0) {
-        V* yseg = commit >= 0 && L.P > 1 ? seg_col<V>(h, li, commit) : nullptr;
-        // Partial slots read (two values) and listed (4 B), per row a list bound, an id and y;
-        // with yseg the segment list and the per-segment copy.
-        Timed tc(h, CCDPP_K_COMBINE, li,
-                 (2.0 * vb + 4.0) * L.nsrc + (8.0 + vb) * L.ncomb + (yseg ? (4.0 + vb) * L.nseg : 0.0));
-        HIPCK(h, ccdk::launch_combine<V>(L, y, yseg, h->lambda, h->stream));
+    if (combine) {
+        Timed tc(h, CCDPP_K_COMBINE, li, cbytes);
+        for (int i = 0; i < nparts; ++i) {
+            const int part = parts[i];
+            const Layout& L = h->L[part];
+            if (L.ncomb == 0) continue;
+            V* yseg = commit >= 0 && L.P > 1 ? seg_col<V>(h, part, commit) : nullptr;
+            HIPCK(h, ccdk::launch_combine<V>(L, y + (part == 2 ? h->split : 0), yseg, h->lambda,
+                                             h->stream));
+        }
         tc.done();
     }
     return CCDPP_OK;
@@ -1078,6 +1266,10 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
         if (opts->seg_weight < -1) return fail(nullptr, CCDPP_EINVAL, "seg_weight < -1");
         if (opts->precision != 0 && opts->precision != 1)
             return fail(nullptr, CCDPP_EINVAL, "precision must be 0 (float) or 1 (double)");
+        if (opts->split_rows < -1 || (opts->split_rows > 0 && opts->split_rows >= n))
+            return fail(nullptr, CCDPP_EINVAL, "split_rows must be -1, 0 or in [1, n)");
+        if (opts->split_rows > 0 && opts->gather_mode[1] != 0)
+            return fail(nullptr, CCDPP_EINVAL, "split_rows needs gather_mode[1] = 0");
     }
     for (int64_t e = 0; e < nnz; ++e) {
         if (row[e] < 0 || row[e] >= m)
@@ -1150,14 +1342,14 @@ int ccd_impl(ccdpp* h, int32_t outer) {
         int32_t *s01, *s10;
         Tmp t01, t10;
         HIPCK(h, talloc(t01, &s01, h->L[0].npad));
-        HIPCK(h, talloc(t10, &s10, h->L[1].npad));
+        HIPCK(h, talloc(t10, &s10, item_slots(h)));
         for (Tmp* t : {&t01, &t10}) {
-            h->allocs.push_back(t->p);
+            h->allocs.emplace_back(t->p, 4 * (t == &t01 ? h->L[0].npad : item_slots(h)));
             t->p = nullptr;
         }
-        h->bytes_held += 4 * (h->L[0].npad + h->L[1].npad);
+        h->bytes_held += 4 * (h->L[0].npad + item_slots(h));
         HIPCK(h, hipMemsetAsync(s01, 0xFF, (size_t)h->L[0].npad * 4, h->stream));
-        HIPCK(h, hipMemsetAsync(s10, 0xFF, (size_t)h->L[1].npad * 4, h->stream));
+        HIPCK(h, hipMemsetAsync(s10, 0xFF, (size_t)item_slots(h) * 4, h->stream));
         HIPCK(h, launch_slot_map(h->pos0, h->map01, h->nnz, s01, h->stream));
         HIPCK(h, launch_slot_map(h->map01, h->pos0, h->nnz, s10, h->stream));
         h->slot01 = s01;
@@ -1184,20 +1376,21 @@ int ccd_impl(ccdpp* h, int32_t outer) {
             RCK(pass<V>(h, li, kModeFlush, nullptr, -1, h->k - 1, nullptr,
                         other + (int64_t)(h->k - 1) * cols, nullptr, -1, 1));
             if (li == 1)
-                HIPCK(h, launch_reduce_sum(h->sse_part, h->L[1].grid * kWaves, h->d_scalar, h->stream));
+                HIPCK(h, launch_reduce_sum(h->sse_part, (h->L[1].grid + h->L[2].grid) * kWaves,
+                                           h->d_scalar, h->stream));
             if (li == 0)
                 HIPCK(h, (launch_copy_slots<V>(as<V>(h->L[0].val), h->slot01, as<V>(h->L[1].val),
                                                h->L[0].npad, h->stream)));
             else
                 HIPCK(h, (launch_copy_slots<V>(as<V>(h->L[1].val), h->slot10, as<V>(h->L[0].val),
-                                               h->L[1].npad, h->stream)));
+                                               item_slots(h), h->stream)));
         }
     }
     if (outer > 0) {
         double sse = 0.0;
         HIPCK(h, hipMemcpyAsync(&sse, h->d_scalar, 8, hipMemcpyDeviceToHost, h->stream));
         HIPCK(h, hipStreamSynchronize(h->stream));
-        h->train_sse = h->L[1].grid ? sse : 0.0;
+        h->train_sse = h->L[1].grid + h->L[2].grid ? sse : 0.0;
         h->train_sse_valid = true;
     }
     HIPCK(h, hipStreamSynchronize(h->stream));
@@ -1628,15 +1821,20 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     auto width = [](const ccdk::Layout& L) -> int64_t {
         return L.gather == ccdk::kGatherHot ? L.hot : L.T;
     };
-    const int64_t v[27] = {h->m,         h->n,         h->nnz,       h->k,
+    const ccdk::Layout& L2 = h->L[2];
+    const bool sp = h->split > 0;
+    const int64_t v[35] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
                            h->dbl ? 8 : 4, h->L[0].ncut, h->L[0].ncomb, h->L[1].ncut,
                            h->L[1].ncomb, h->L[0].cache + 1, h->L[1].cache + 1,
                            h->L[0].ndelta, h->L[0].npad / ccdk::kWin, h->L[1].ndelta,
-                           h->L[1].npad / ccdk::kWin};
-    int32_t w = std::min<int32_t>(len, 27);
+                           h->L[1].npad / ccdk::kWin, h->split,
+                           sp ? L2.gather : 0, sp ? width(L2) : 0, sp ? L2.grid : 0,
+                           sp ? L2.nseg : 0, sp ? L2.ncut : 0, sp ? L2.ncomb : 0,
+                           sp ? L2.cache + 1 : 0};
+    int32_t w = std::min<int32_t>(len, 35);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

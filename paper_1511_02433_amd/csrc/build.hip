@@ -7,7 +7,9 @@
 // counts -- and a radix sort brings the entries into layout order, carrying the
 // triplet index along so values and the map between the two copies follow.
 // Adjacent equal keys after the user-major sort are repeated positions.
-#include <hipcub/hipcub.hpp>
+#include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/device/device_select.hpp>
+#include <rocprim/iterator/counting_iterator.hpp>
 
 #include <type_traits>
 
@@ -29,6 +31,18 @@ __global__ void k_histogram(const int32_t* __restrict__ key, int64_t n, int32_t*
     for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < n; e += (int64_t)gridDim.x * kT)
         atomicAdd(&count[key[e]], 1);
 }
+
+__global__ void k_add(int32_t* __restrict__ a, int64_t n, int32_t delta) {
+    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < n; e += (int64_t)gridDim.x * kT)
+        a[e] += delta;
+}
+
+// Entries whose key lies in [lo, hi).
+struct KeyInRange {
+    const int32_t* key;
+    int32_t lo, hi;
+    __device__ bool operator()(int32_t e) const { return key[e] >= lo && key[e] < hi; }
+};
 
 __global__ void k_map(const int32_t* __restrict__ in, const int32_t* __restrict__ table,
                       int64_t n, int32_t* __restrict__ out) {
@@ -563,20 +577,43 @@ template hipError_t launch_copy_mapped<float, double>(const float*, const int32_
                                                       const int32_t*, int64_t, hipStream_t);
 
 // Radix sort of (key, id) pairs on the low `bits` bits of the key.
+// Grows the shared temporary buffer of the device-wide primitives when needed.
+hipError_t ensure_tmp(void** tmp, size_t* tmp_bytes, size_t need) {
+    if (need <= *tmp_bytes) return hipSuccess;
+    if (*tmp) (void)hipFree(*tmp);
+    *tmp = nullptr;
+    *tmp_bytes = 0;
+    hipError_t e = dev_malloc(tmp, need);
+    if (e == hipSuccess) *tmp_bytes = need;
+    return e;
+}
+
 hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, int32_t* vout,
                       int64_t n, int bits, hipStream_t s, void** tmp, size_t* tmp_bytes) {
     size_t need = 0;
-    hipError_t e = hipcub::DeviceRadixSort::SortPairs(nullptr, need, kin, kout, vin, vout, (int)n,
-                                                      0, bits, s);
+    hipError_t e = rocprim::radix_sort_pairs(nullptr, need, kin, kout, vin, vout, (size_t)n, 0u,
+                                             (unsigned)bits, s);
+    if (e == hipSuccess) e = ensure_tmp(tmp, tmp_bytes, need);
     if (e != hipSuccess) return e;
-    if (need > *tmp_bytes) {
-        if (*tmp) hipFree(*tmp);
-        *tmp = nullptr;
-        e = dev_malloc(tmp, need);
-        if (e != hipSuccess) return e;
-        *tmp_bytes = need;
-    }
-    return hipcub::DeviceRadixSort::SortPairs(*tmp, need, kin, kout, vin, vout, (int)n, 0, bits, s);
+    return rocprim::radix_sort_pairs(*tmp, need, kin, kout, vin, vout, (size_t)n, 0u,
+                                     (unsigned)bits, s);
+}
+
+hipError_t select_range(const int32_t* key, int64_t n, int32_t lo, int32_t hi, int32_t* out,
+                        int64_t* count, hipStream_t s, void** tmp, size_t* tmp_bytes) {
+    const rocprim::counting_iterator<int32_t> ids(0);
+    const KeyInRange pred{key, lo, hi};
+    size_t need = 0;
+    hipError_t e = rocprim::select(nullptr, need, ids, out, count, (size_t)n, pred, s);
+    if (e == hipSuccess) e = ensure_tmp(tmp, tmp_bytes, need);
+    if (e != hipSuccess) return e;
+    return rocprim::select(*tmp, need, ids, out, count, (size_t)n, pred, s);
+}
+
+hipError_t launch_add(int32_t* a, int64_t n, int32_t delta, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_add, grid_for(n), dim3(kT), 0, s, a, n, delta);
+    return hipGetLastError();
 }
 
 }  // namespace ccdk

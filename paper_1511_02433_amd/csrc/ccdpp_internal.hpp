@@ -375,7 +375,14 @@ hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* 
                            const int32_t* rold2new, const int32_t* cold2new, const V* W,
                            const V* H, int64_t m, int64_t n, int32_t k, double* part,
                            int32_t nparts, double* rejected, hipStream_t s);
+// Device-wide primitives (rocPRIM); tmp is a temporary buffer grown as needed and
+// freed by the caller.  sort_pairs: stable radix sort of (key, value) pairs on the
+// low `bits` bits of the keys.  select_range: out[0 .. *count) = the indices e < n
+// with lo <= key[e] < hi, in increasing order (count in device memory).
 hipError_t sort_pairs(const uint64_t* kin, uint64_t* kout, const int32_t* vin, int32_t* vout,
                       int64_t n, int bits, hipStream_t s, void** tmp, size_t* tmp_bytes);
+hipError_t select_range(const int32_t* key, int64_t n, int32_t lo, int32_t hi, int32_t* out,
+                        int64_t* count, hipStream_t s, void** tmp, size_t* tmp_bytes);
+hipError_t launch_add(int32_t* a, int64_t n, int32_t delta, hipStream_t s);
 
 }  // namespace ccdk

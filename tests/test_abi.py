@@ -63,6 +63,9 @@ def test_create_rejects_bad_arguments_on_the_host(kw, msg):
     (dict(cache=(4, 0)), "cache"),
     (dict(cache=(0, -1)), "cache"),
     (dict(index_coding=(2, 0)), "index_coding"),
+    (dict(split_rows=-2), "split_rows"),
+    (dict(split_rows=8), "split_rows"),  # n = 8 in _create
+    (dict(split_rows=3, gather_mode=(0, 2)), "split_rows"),
 ])
 def test_create_rejects_bad_options(kw, msg):
     _lib_or_skip()

@@ -14,8 +14,9 @@ run side by side:
 
 Workloads: medium (10 x 3), large (10 x 3), the rank sweep on the large matrix
 (k = 10 and k = 100, 5 x 3; k = 40 is the large workload's own k) and the very
-large matrix (5 x 3, lambda = 1), whose item-major copy is a hot layout and
-whose user-major copy is tiled, so that its combine covers every row.  Each
+large matrix (5 x 3, lambda = 1), whose item-major copy is split (its leading
+items tiled, the others a hot layout) and whose user-major copy is tiled, so
+that its combine covers every row.  Each
 test prints what it runs before it starts, and keeps to about two minutes: the
 very large workload is split into drawing the matrix, the first outer
 iteration and the rest of the schedule.
@@ -45,9 +46,12 @@ def _say(msg):
 # The automatic cache policy of the two copies (1 streaming, 2 write-back residual
 # stores, 3 cached): medium's residual streams fit in the memory-side cache; large
 # takes write-back stores on its one-tile user-major copy; the very large matrix has
-# no one-tile copy.  The gather mode of each copy (2 tiled, 3 hot).
+# no one-tile copy.  The gather mode of each copy (2 tiled, 3 hot), and whether the
+# item-major copy is split into tiled leading items and a hot rest: the very large
+# matrix's is (its hot part streams too).
 EXPECT_CACHE = {"medium": (3, 3), "large": (2, 1), "vlarge": (1, 1)}
-EXPECT_GATHER = {"medium": (2, 2), "large": (2, 2), "vlarge": (2, 3)}
+EXPECT_GATHER = {"medium": (2, 2), "large": (2, 2), "vlarge": (2, 2)}
+EXPECT_SPLIT = {"medium": False, "large": False, "vlarge": True}
 
 
 class Side:
@@ -63,6 +67,9 @@ class Side:
         if w.name in EXPECT_CACHE:
             assert (info["u_cache"], info["v_cache"]) == EXPECT_CACHE[w.name]
             assert (info["u_gather"], info["v_gather"]) == EXPECT_GATHER[w.name]
+            assert (info["v_split_rows"] > 0) == EXPECT_SPLIT[w.name]
+            if EXPECT_SPLIT[w.name]:
+                assert info["v2_gather"] == 3 and info["v2_cache"] == 1
         h0 = ds.h0(k)
         self.g.set_factors(np.zeros((w.m, k), np.float32), h0)
         t0 = time.perf_counter()
