@@ -48,12 +48,18 @@ LAYOUT_NAMES = {0: "rows", 1: "cols"}
 
 def kernel_symbol(kind: int, info: dict, layout: int, wb_stores: bool = True) -> str:
     """The kernel's name as a trace shows it (the sweep kernels are templated on
-    LDS staging, 16-bit indices, P == 1 and the value type)."""
+    LDS staging, 16-bit indices, P == 1 and the value type).  A split item-major
+    copy runs two kernels per pass, its tiled part's and its hot part's: "A + B"."""
     v = "double" if info.get("value_bytes", 4) == 8 else "float"
     if kind == 2:  # (4 lanes per row instead of 16 on layouts whose rows have few partials)
         return f"void ccdk::ccd_combine<16, {v}>(ccdk::CombineArgs<{v}>)"
     if kind == 3:
         return f"void ccdk::ccd_copy<{v}>({v} const*, {v}*, long)"
+    if layout == 1 and info.get("v_split_rows", 0) > 0:
+        hot = dict(info, v_gather=info["v2_gather"], v_tiles=1,
+                   v_tile_width=info["v2_tile_width"], v_cache=info["v2_cache"], v_split_rows=0)
+        return (kernel_symbol(kind, dict(info, v_split_rows=0), 1, wb_stores) + " + " +
+                kernel_symbol(kind, hot, 1, wb_stores))
     pre = "u" if layout == 0 else "v"
     gather = info[f"{pre}_gather"]
     staged = gather in (2, 3)  # tiled, or hot (leading columns staged)
@@ -324,7 +330,7 @@ def main():
             d = per_layout[dom]
             n, tot, b = g.profile_read(d["kind"], d["layout"])
             live = {"launches": n, "mean_us": round(tot / n * 1e3, 3), "total_ms": round(tot, 4),
-                    "algo_bytes_per_launch": b / n}
+                    "stored_bytes_per_launch": b / n}
         else:
             kinds, per_layout = read_kernels()
             kinds_steps = args.steps
@@ -349,7 +355,7 @@ def main():
         sec = live["mean_us"] * 1e-6
         mb = d["model_bytes_per_launch"]
         achieved = mb / sec / 1e9
-        stored = live["algo_bytes_per_launch"] / sec / 1e9
+        stored = live["stored_bytes_per_launch"] / sec / 1e9
         traffic = stored_traffic(dom, w.name, args.precision)
         roofline = {"kernel": d["kernel"], "layout": dom.split("/")[1], "bound": "hbm",
                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -360,7 +366,7 @@ def main():
                     "frac_stored": round(stored / HBM_PEAK_GBS, 4),
                     "mean_us": live["mean_us"], "launches": live["launches"],
                     "algo_bytes_per_launch": mb,
-                    "stored_bytes_per_launch": live["algo_bytes_per_launch"]}
+                    "stored_bytes_per_launch": live["stored_bytes_per_launch"]}
     train_rmse = g.train_rmse()
     test_rmse = g.rmse(ds.test_row, ds.test_col, ds.test_val) if ds.test_row.size else None
     # The open outer loop with monitoring: three more outer iterations, each followed by

@@ -308,7 +308,10 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   that are tiled (0: not split; fields 10..14, 19..22 and 25..26 then describe
  *   that tiled part), [28..34] the hot part of a split copy: gather mode, hot
  *   width, workgroups, segments, rows finished in the pass, rows combined,
- *   cache policy (zeros when not split).
+ *   cache policy (zeros when not split), [35..40] the device build's phases in
+ *   microseconds: inputs copied and degrees counted; relabelling; the
+ *   user-major copy; the item-major copy and the map between the copies;
+ *   cache policies, index coding and scratch; the factors.
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

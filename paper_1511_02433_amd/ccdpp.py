@@ -272,7 +272,9 @@ INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_
                "u_rows_combined", "v_rows_finished_in_pass", "v_rows_combined", "u_cache",
                "v_cache", "u_delta_windows", "u_windows", "v_delta_windows", "v_windows",
                "v_split_rows", "v2_gather", "v2_tile_width", "v2_workgroups", "v2_segments",
-               "v2_rows_finished_in_pass", "v2_rows_combined", "v2_cache")
+               "v2_rows_finished_in_pass", "v2_rows_combined", "v2_cache", "build_inputs_us",
+               "build_relabel_us", "build_user_major_us", "build_item_major_us", "build_setup_us",
+               "build_factors_us")
 
 
 def ccdpp_info(h):

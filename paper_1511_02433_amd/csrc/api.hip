@@ -135,6 +135,10 @@ struct ccdpp {
     std::string err;
     bool poisoned = false;
     int64_t build_us = 0;
+    // Device build phases, microseconds: inputs and degrees; relabelling; user-major copy;
+    // item-major copy and the map between the copies; cache policy, index coding and
+    // scratch; factors.
+    int64_t build_phase_us[6] = {};
     int64_t bytes_held = 0;
     std::vector<std::pair<void*, int64_t>> allocs;  // device allocations and their sizes
     // kernel timing
@@ -937,6 +941,12 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
                   uint64_t seed, const ccdpp_options_t* opt) {
     using namespace ccdk;
     const auto t0 = std::chrono::steady_clock::now();
+    auto tprev = t0;
+    auto phase = [&](int i) {
+        const auto t = std::chrono::steady_clock::now();
+        h->build_phase_us[i] = std::chrono::duration_cast<std::chrono::microseconds>(t - tprev).count();
+        tprev = t;
+    };
     const int64_t m = h->m, n = h->n, N = h->nnz;
     HIPCK(h, hipGetDevice(&h->device));
     hipDeviceProp_t prop;
@@ -989,6 +999,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, hipMemcpyAsync(cnt_r.data(), d_cnt_r, m * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipMemcpyAsync(cnt_c.data(), d_cnt_c, n * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
+    phase(0);
 
     // Relabel users and items by decreasing degree.
     std::vector<int32_t> rn2o, ro2n, cn2o, co2n;
@@ -1004,11 +1015,14 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, talloc(t_ci, &d_ci, N));
     HIPCK(h, launch_map(d_row, h->rold2new, N, d_ru, s));
     HIPCK(h, launch_map(d_col, h->cold2new, N, d_ci, s));
+    HIPCK(h, hipStreamSynchronize(s));
+    phase(1);
 
     // The two copies, the ratings in user-major order and the map between copies.
     HIPCK(h, dalloc(h, &h->perm0, N));
     HIPCK(h, dalloc(h, &h->pos0, N));
     RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s, N));
+    phase(2);
     {
         int32_t *perm1, *pos1, *inv1, *e01;
         Tmp tp1, tq1, tinv, te;
@@ -1023,6 +1037,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         HIPCK(h, launch_compose(pos1, e01, N, h->map01, s));
         HIPCK(h, hipStreamSynchronize(s));
     }
+    phase(3);
     RCK(choose_cache(h, opt));
     for (int part = 0; part < 3; ++part) RCK(code_windows(h, part, opt));
     h->sse_nparts = std::max<int32_t>((h->L[0].grid + h->L[1].grid + h->L[2].grid) * kWaves,
@@ -1030,6 +1045,8 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, dalloc(h, &h->sse_part, h->sse_nparts));
     HIPCK(h, dalloc(h, &h->d_scalar, 1));
     HIPCK(h, dalloc(h, &h->d_count, 1));
+    HIPCK(h, hipStreamSynchronize(s));
+    phase(4);
     for (int part = 0; part < 3; ++part)  // partials are written before they are read: start them as NaN
         if (h->L[part].part)
             HIPCK(h, launch_fill<float>(static_cast<float*>(h->L[part].part), __builtin_nanf(""),
@@ -1070,6 +1087,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         return CCDPP_OK;
     }));
     h->pending = -1;
+    phase(5);
     h->build_us = std::chrono::duration_cast<std::chrono::microseconds>(
                       std::chrono::steady_clock::now() - t0)
                       .count();
@@ -1823,7 +1841,7 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     };
     const ccdk::Layout& L2 = h->L[2];
     const bool sp = h->split > 0;
-    const int64_t v[35] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[41] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
@@ -1833,8 +1851,10 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
                            h->L[1].npad / ccdk::kWin, h->split,
                            sp ? L2.gather : 0, sp ? width(L2) : 0, sp ? L2.grid : 0,
                            sp ? L2.nseg : 0, sp ? L2.ncut : 0, sp ? L2.ncomb : 0,
-                           sp ? L2.cache + 1 : 0};
-    int32_t w = std::min<int32_t>(len, 35);
+                           sp ? L2.cache + 1 : 0, h->build_phase_us[0], h->build_phase_us[1],
+                           h->build_phase_us[2], h->build_phase_us[3], h->build_phase_us[4],
+                           h->build_phase_us[5]};
+    int32_t w = std::min<int32_t>(len, 41);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }
