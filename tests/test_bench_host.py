@@ -28,21 +28,27 @@ def test_kernel_symbols_follow_the_layout_and_cache_policy():
     hot = dict(INFO, v_gather=3, v_tiles=1, v_tile_width=40768, value_bytes=8)
     assert k(1, hot, 1) == "void ccdk::ccd_pass<true, false, true, 0, double>(ccdk::PassArgs<double>)"
     assert k(2, INFO, 1) == "void ccdk::ccd_combine<16, float>(ccdk::CombineArgs<float>)"
+    # A split item-major copy: its tiled part's kernel, then its hot part's.
+    split = dict(INFO, v_tiles=75, v_tile_width=13504, v_cache=1, v_split_rows=36620,
+                 v2_gather=3, v2_tile_width=40768, v2_cache=1)
+    assert k(1, split, 1) == ("void ccdk::ccd_pass<true, true, false, 0, float>(ccdk::PassArgs<float>)"
+                              " + void ccdk::ccd_pass<true, false, true, 0, float>(ccdk::PassArgs<float>)")
 
 
 def test_stored_traffic_only_for_the_sources_it_was_taken_on():
     # The committed counters carry the digest of the kernel sources they were taken on;
     # bench.py reports them only while the sources are unchanged.
-    with open(os.path.join(ROOT, "profiles", "traffic_large.json")) as f:
-        t = json.load(f)
-    assert len(t["source_digest"]) == 16
-    for key, v in t["kernels"].items():
-        assert v["bytes_per_launch"] > 0 and v["algo_bytes_per_launch"] > 0
-        got = bench.stored_traffic(key, "large")
-        if t["source_digest"] == bench.source_digest():
-            assert got == v["bytes_per_launch"]
-        else:
-            assert got is None
+    for wl in ("large", "vlarge"):
+        with open(os.path.join(ROOT, "profiles", f"traffic_{wl}.json")) as f:
+            t = json.load(f)
+        assert len(t["source_digest"]) == 16
+        for key, v in t["kernels"].items():
+            assert v["bytes_per_launch"] > 0 and v["stored_bytes_per_launch"] > 0
+            got = bench.stored_traffic(key, wl)
+            if t["source_digest"] == bench.source_digest():
+                assert got == v["bytes_per_launch"]
+            else:
+                assert got is None
     assert bench.stored_traffic("ccd_pass/rows", "no_such_workload") is None
 
 
