@@ -248,39 +248,30 @@ hipError_t talloc(Tmp& t, T** p, int64_t count) {
 
 bool usable(const ccdpp* h) { return h && !h->poisoned; }
 
-// splitmix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
-// generators", OOPSLA 2014): a counter-based 64-bit generator.
-uint64_t splitmix64(uint64_t x) {
-    x += 0x9E3779B97F4A7C15ull;
-    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
-    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
-    return x ^ (x >> 31);
-}
-
-// H0 entry e (row-major n x k): N(0, 0.01) by Box-Muller on two counter draws.
-float initial_h(uint64_t seed, uint64_t e) {
-    const uint64_t s = splitmix64(seed);
-    const double u1 = (double)(splitmix64(s + 2 * e) >> 11) * 0x1.0p-53;
-    const double u2 = (double)(splitmix64(s + 2 * e + 1) >> 11) * 0x1.0p-53;
-    const double z = std::sqrt(-2.0 * std::log1p(-u1)) * std::cos(6.283185307179586 * u2);
-    return (float)(0.1 * z);
-}
-
 int bits_for(uint64_t maxval) {
     int b = 1;
     while (b < 64 && (maxval >> b) != 0) ++b;
     return b;
 }
 
-// Order ids by decreasing count, ties by increasing id.
+// Order ids by decreasing count, ties by increasing id: a counting sort over the
+// counts (a comparison sort when the largest count dwarfs the number of ids).
 void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
              std::vector<int32_t>& old2new) {
     const int64_t N = (int64_t)count.size();
     new2old.resize(N);
-    std::iota(new2old.begin(), new2old.end(), 0);
-    std::stable_sort(new2old.begin(), new2old.end(),
-                     [&](int32_t a, int32_t b) { return count[a] > count[b]; });
     old2new.resize(N);
+    const int32_t maxc = N ? *std::max_element(count.begin(), count.end()) : 0;
+    if ((int64_t)maxc <= 4 * N + 1024) {
+        std::vector<int64_t> start((size_t)maxc + 2, 0);  // bucket b = maxc - count
+        for (int32_t c : count) ++start[(size_t)(maxc - c) + 1];
+        for (size_t b = 1; b < start.size(); ++b) start[b] += start[b - 1];
+        for (int64_t i = 0; i < N; ++i) new2old[(size_t)start[(size_t)(maxc - count[i])]++] = (int32_t)i;
+    } else {
+        std::iota(new2old.begin(), new2old.end(), 0);
+        std::stable_sort(new2old.begin(), new2old.end(),
+                         [&](int32_t a, int32_t b) { return count[a] > count[b]; });
+    }
     for (int64_t i = 0; i < N; ++i) old2new[new2old[i]] = (int32_t)i;
 }
 
@@ -322,7 +313,7 @@ int64_t choose_split(const std::vector<int32_t>& cnt, int64_t P, int64_t rows, i
 int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, const int32_t* lrow,
                  const int32_t* lcol, const float* val_in, const ccdpp_options_t* opt,
                  int32_t* perm, int32_t* epos, hipStream_t s, int64_t nnz,
-                 int64_t* split_out = nullptr) {
+                 int64_t* split_out = nullptr, const int32_t* row_deg = nullptr) {
     using namespace ccdk;
     const int64_t N = nnz;
     L.rows = rows;
@@ -365,15 +356,19 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // Entries per (tile, row).
     std::vector<int32_t> cnt;
     for (int attempt = 0; attempt < 2; ++attempt) {
-        int32_t* d_cnt;
-        Tmp tc;
-        HIPCK(h, talloc(tc, &d_cnt, P * rows));
-        HIPCK(h, hipMemsetAsync(d_cnt, 0, (size_t)(P * rows) * 4, s));
-        HIPCK(h, launch_seg_histogram(lrow, lcol, N, (int32_t)rows, (int32_t)T, d_cnt, s));
-        cnt.assign((size_t)(P * rows), 0);
-        HIPCK(h, hipMemcpyAsync(cnt.data(), d_cnt, (size_t)(P * rows) * 4, hipMemcpyDeviceToHost,
-                                s));
-        HIPCK(h, hipStreamSynchronize(s));
+        if (P == 1 && row_deg) {  // one tile: the entries per row are the row lengths
+            cnt.assign(row_deg, row_deg + rows);
+        } else {
+            int32_t* d_cnt;
+            Tmp tc;
+            HIPCK(h, talloc(tc, &d_cnt, P * rows));
+            HIPCK(h, hipMemsetAsync(d_cnt, 0, (size_t)(P * rows) * 4, s));
+            HIPCK(h, launch_seg_histogram(lrow, lcol, N, (int32_t)rows, (int32_t)T, d_cnt, s));
+            cnt.assign((size_t)(P * rows), 0);
+            HIPCK(h, hipMemcpyAsync(cnt.data(), d_cnt, (size_t)(P * rows) * 4,
+                                    hipMemcpyDeviceToHost, s));
+            HIPCK(h, hipStreamSynchronize(s));
+        }
         if (P == 1 || forced == kGatherLds) break;
         // Tiling pays only when segments are long enough; otherwise stage the leading
         // columns and gather the others through L2.
@@ -507,14 +502,23 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
                            seg_start.begin();  // segments starting at or before e
         return e + wseg * sg;
     };
-    auto pos_at = [&](int64_t t) -> int64_t {
-        int64_t lo = 0, hi = NP;  // work_at is increasing: largest e with work_at(e) <= t
-        while (lo < hi) {
-            const int64_t mid = (lo + hi + 1) / 2;
-            if (work_at(mid) <= t) lo = mid; else hi = mid - 1;
-        }
-        return lo;
+    // The largest position e <= NP with work_at(e) <= t (0 if there is none).  Segment
+    // starts are strictly increasing, and inside segment s the work grows by one per
+    // position from ws[s], the work at its start, so one search over the segment
+    // starts finds it.
+    std::vector<int64_t> ws;
+    auto index_work = [&]() {
+        ws.resize((size_t)S_work);
+        for (int64_t sg = 0; sg < S_work; ++sg) ws[sg] = seg_start[sg] + wseg * (sg + 1);
     };
+    auto pos_at = [&](int64_t t) -> int64_t {
+        if (S_work == 0) return std::max<int64_t>(0, std::min(t, NP));
+        const int64_t sg = std::upper_bound(ws.begin(), ws.end(), t) - ws.begin() - 1;
+        if (sg < 0) return std::max<int64_t>(0, std::min(t, seg_start[0] - 1));
+        const int64_t end = sg + 1 < S_work ? seg_start[sg + 1] - 1 : NP;
+        return std::min(seg_start[sg] + (t - ws[sg]), std::min(end, NP));
+    };
+    index_work();
     auto target = [&](int64_t wt, int64_t g) { return wt / G * g + wt % G * g / G; };
     // With P == 1 (float) every share boundary moves to the start of the nearest row,
     // when none of them changes its shares by more than an eighth: rows are then
@@ -538,6 +542,7 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         if (snapped) {
             for (int64_t g = 1; g < G; ++g) align_first[snap[g]] = 1;
             RCK(pad_layout());
+            index_work();
         } else {
             std::fill(snap.begin(), snap.end(), -1);
         }
@@ -853,16 +858,18 @@ int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
 // pos1 as for build_layout, over the two parts in turn (heavy entries first), with
 // the light part's slots offset by off2 into the one value array of the copy.
 int build_item_major(ccdpp* h, const int32_t* lrow, const int32_t* lcol, const float* val,
-                     const ccdpp_options_t* opt, int32_t* perm1, int32_t* pos1, hipStream_t s) {
+                     const ccdpp_options_t* opt, int32_t* perm1, int32_t* pos1, hipStream_t s,
+                     const int32_t* deg) {
     using namespace ccdk;
     const int64_t m = h->m, n = h->n, N = h->nnz;
     const int32_t forced = opt ? opt->split_rows : 0;
     int64_t H = forced > 0 ? forced : 0;
     if (forced == 0) {
-        RCK(build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N, &H));
+        RCK(build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N, &H, deg));
         if (H == 0) return CCDPP_OK;  // built whole
     } else if (forced < 0) {
-        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N);
+        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, opt, perm1, pos1, s, N, nullptr,
+                            deg);
     }
     // The entries of the leading H items and of the others, each in input order.
     int32_t *ih, *il;
@@ -883,7 +890,8 @@ int build_item_major(ccdpp* h, const int32_t* lrow, const int32_t* lcol, const f
         ccdpp_options_t o1{};
         if (opt) o1 = *opt;
         o1.split_rows = -1;
-        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, &o1, perm1, pos1, s, N);
+        return build_layout(h, 1, h->L[1], n, m, lrow, lcol, val, &o1, perm1, pos1, s, N, nullptr,
+                            deg);
     }
     int32_t *rh, *ch, *rl, *cl, *ph, *qh, *pl, *ql;
     float *vh, *vl;
@@ -910,8 +918,8 @@ int build_item_major(ccdpp* h, const int32_t* lrow, const int32_t* lcol, const f
     oh.gather_mode[1] = kGatherLds;
     ol.gather_mode[1] = kGatherHot;
     ol.tile_width[1] = 0;
-    RCK(build_layout(h, 1, h->L[1], H, m, rh, ch, vh, &oh, ph, qh, s, nh));
-    RCK(build_layout(h, 1, h->L[2], n - H, m, rl, cl, vl, &ol, pl, ql, s, nl));
+    RCK(build_layout(h, 1, h->L[1], H, m, rh, ch, vh, &oh, ph, qh, s, nh, nullptr, deg));
+    RCK(build_layout(h, 1, h->L[2], n - H, m, rl, cl, vl, &ol, pl, ql, s, nl, nullptr, deg + H));
     const int64_t off2 = h->L[1].npad + kEntryPad;
     if (off2 + h->L[2].npad + kEntryPad > (int64_t)INT32_MAX)
         return fail(h, CCDPP_EINVAL, "the split item-major copy exceeds 2^31 value slots");
@@ -1021,14 +1029,19 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     // The two copies, the ratings in user-major order and the map between copies.
     HIPCK(h, dalloc(h, &h->perm0, N));
     HIPCK(h, dalloc(h, &h->pos0, N));
-    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s, N));
+    // Row lengths in relabelled order (rows are relabelled by decreasing length).
+    std::vector<int32_t> deg_u((size_t)m), deg_i((size_t)n);
+    for (int64_t r = 0; r < m; ++r) deg_u[r] = cnt_r[rn2o[r]];
+    for (int64_t r = 0; r < n; ++r) deg_i[r] = cnt_c[cn2o[r]];
+    RCK(build_layout(h, 0, h->L[0], m, n, d_ru, d_ci, d_val, opt, h->perm0, h->pos0, s, N, nullptr,
+                     deg_u.data()));
     phase(2);
     {
         int32_t *perm1, *pos1, *inv1, *e01;
         Tmp tp1, tq1, tinv, te;
         HIPCK(h, talloc(tp1, &perm1, N));
         HIPCK(h, talloc(tq1, &pos1, N));
-        RCK(build_item_major(h, d_ci, d_ru, d_val, opt, perm1, pos1, s));
+        RCK(build_item_major(h, d_ci, d_ru, d_val, opt, perm1, pos1, s, deg_i.data()));
         HIPCK(h, talloc(tinv, &inv1, N));
         HIPCK(h, launch_invert(perm1, N, inv1, s));
         HIPCK(h, talloc(te, &e01, N));
@@ -1075,13 +1088,7 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
                 HIPCK(h, dalloc(h, &f, (int64_t)h->k * h->L[part].nseg));
                 h->fseg[part] = f;
             }
-        std::vector<float> h0((size_t)n * h->k);
-        for (int64_t e = 0; e < n * h->k; ++e) h0[e] = initial_h(seed, (uint64_t)e);
-        float* d_h0;
-        Tmp th0;
-        HIPCK(h, talloc(th0, &d_h0, n * h->k));
-        HIPCK(h, hipMemcpyAsync(d_h0, h0.data(), h0.size() * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, (launch_scatter_factor_in<float, V>(d_h0, h->cnew2old, n, h->k, H, s)));
+        HIPCK(h, (launch_initial_h<V>(seed, h->cnew2old, n, h->k, H, s)));
         RCK(spread_factors(h));
         HIPCK(h, hipStreamSynchronize(s));
         return CCDPP_OK;

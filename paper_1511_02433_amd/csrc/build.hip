@@ -277,6 +277,36 @@ __global__ void k_consistency(const V* __restrict__ a, const int32_t* __restrict
             atomicAdd(count, 1ull);
 }
 
+// splitmix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+// generators", OOPSLA 2014): a counter-based 64-bit generator.
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+
+// The initial H: entry (j, t) of the row-major n x k matrix over input ids, e = j k + t,
+// is 0.1 z, z ~ N(0, 1) by the Box-Muller transform of the counter draws 2e and 2e + 1
+// of a stream keyed by the seed, rounded to float; written column-major over
+// relabelled ids (H[t n + j'] for j' = old2new[j]).
+template <class V>
+__global__ void k_initial_h(uint64_t seed, const int32_t* __restrict__ new2old, int64_t n,
+                            int32_t k, V* __restrict__ H) {
+    const uint64_t key = splitmix64(seed);
+    const int64_t total = n * k;
+    for (int64_t q = (int64_t)blockIdx.x * kT + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * kT) {
+        const int64_t t = q / n;
+        const int64_t jn = q - t * n;
+        const uint64_t e = (uint64_t)new2old[jn] * (uint64_t)k + (uint64_t)t;
+        const double u1 = (double)(splitmix64(key + 2 * e) >> 11) * 0x1.0p-53;
+        const double u2 = (double)(splitmix64(key + 2 * e + 1) >> 11) * 0x1.0p-53;
+        const double z = __builtin_sqrt(-2.0 * log1p(-u1)) * cos(6.283185307179586 * u2);
+        H[q] = (V)(float)(0.1 * z);
+    }
+}
+
 template <class V>
 __global__ void k_seg_spread(const V* __restrict__ F, int64_t rows,
                              const int32_t* __restrict__ seg_row, int64_t S, int32_t k,
@@ -511,6 +541,14 @@ hipError_t launch_consistency(const V* a, const int32_t* amap, const V* b, const
 }
 
 template <class V>
+hipError_t launch_initial_h(uint64_t seed, const int32_t* new2old, int64_t n, int32_t k, V* H,
+                            hipStream_t s) {
+    if (n * k == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_initial_h<V>, grid_for(n * k), dim3(kT), 0, s, seed, new2old, n, k, H);
+    return hipGetLastError();
+}
+
+template <class V>
 hipError_t launch_seg_spread(const V* F, int64_t rows, const int32_t* seg_row, int64_t S,
                              int32_t k, V* out, hipStream_t s) {
     if (S == 0 || k == 0) return hipSuccess;
@@ -563,6 +601,8 @@ hipError_t launch_test_err(const int32_t* row, const int32_t* col, const float* 
                                               hipStream_t);                                     \
     template hipError_t launch_seg_spread<V>(const V*, int64_t, const int32_t*, int64_t,        \
                                              int32_t, V*, hipStream_t);                         \
+    template hipError_t launch_initial_h<V>(uint64_t, const int32_t*, int64_t, int32_t, V*,     \
+                                            hipStream_t);                                       \
     template hipError_t launch_sq_sum<V>(const V*, int64_t, double*, int32_t, hipStream_t);     \
     template hipError_t launch_test_err<V>(const int32_t*, const int32_t*, const float*,        \
                                            int64_t, const int32_t*, const int32_t*, const V*,   \

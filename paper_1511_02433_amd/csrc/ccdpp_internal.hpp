@@ -361,6 +361,10 @@ hipError_t launch_copy_mapped(const S* src, const int32_t* smap, V* dst, const i
 template <class V>
 hipError_t launch_consistency(const V* a, const int32_t* amap, const V* b, const int32_t* bmap,
                               int64_t n, unsigned long long* count, hipStream_t s);
+// The initial H from a seed (column-major over relabelled ids, k x n); see build.hip.
+template <class V>
+hipError_t launch_initial_h(uint64_t seed, const int32_t* new2old, int64_t n, int32_t k, V* H,
+                            hipStream_t s);
 // out[t * S + s] = F[t * rows + seg_row[s]] for t < k
 template <class V>
 hipError_t launch_seg_spread(const V* F, int64_t rows, const int32_t* seg_row, int64_t S,

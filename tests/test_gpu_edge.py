@@ -121,3 +121,44 @@ def test_index_width_boundary_of_global_layouts(n):
     g = _compare(len(lens), n, 2, 0.1, row, col, val, H0, outer=2, inner=2,
                  opts=make_options(gather_mode=(1, 1)))
     assert g.info()["u_tile_width"] == n
+
+
+def _splitmix64(x):
+    """splitmix64 (Steele, Lea and Flood, OOPSLA 2014) on uint64 arrays."""
+    with np.errstate(over="ignore"):
+        x = x + np.uint64(0x9E3779B97F4A7C15)
+        x = (x ^ (x >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        x = (x ^ (x >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return x ^ (x >> np.uint64(31))
+
+
+def test_seeded_initial_state():
+    """ccdpp_create's initial state: W = 0 (Algorithm 3), and H entry (j, t) is 0.1 z
+    with z from the Box-Muller transform of counter draws 2e and 2e + 1 (e = j k + t)
+    of splitmix64 keyed by the seed, rounded to float: checked against that
+    definition evaluated here, to within one float rounding, and for the spread of
+    N(0, 0.01)."""
+    m, n, k = 700, 5000, 6
+    row, col, val, _ = synth.small_random(m, n, 20_000, k, seed=71)
+    g = CCDPP(m, n, k, 0.1, row, col, val, seed=12345)
+    W, H = g.factors()
+    assert np.all(W == 0)
+    e = np.arange(n * k, dtype=np.uint64)
+    key = _splitmix64(np.array([12345], dtype=np.uint64))[0]
+    with np.errstate(over="ignore"):
+        u1 = (_splitmix64(key + np.uint64(2) * e) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+        u2 = (_splitmix64(key + np.uint64(2) * e + np.uint64(1)) >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+    z = np.sqrt(-2.0 * np.log1p(-u1)) * np.cos(6.283185307179586 * u2)
+    ref = (0.1 * z).astype(np.float32).reshape(n, k)
+    ulp = np.spacing(np.abs(ref))
+    assert np.all(np.abs(H - ref) <= ulp)
+    assert abs(float(H.std()) - 0.1) < 0.003 and abs(float(H.mean())) < 0.003
+    # the same seed gives the same H, another seed another one; float64 handles start
+    # from the same float values
+    W2, H2 = CCDPP(m, n, k, 0.1, row, col, val, seed=12345).factors()
+    assert np.array_equal(H, H2)
+    _, H3 = CCDPP(m, n, k, 0.1, row, col, val, seed=54321).factors()
+    assert not np.array_equal(H, H3)
+    from paper_1511_02433_amd.ccdpp import make_options
+    _, H4 = CCDPP(m, n, k, 0.1, row, col, val, seed=12345, opts=make_options(precision=1)).factors_f64()
+    assert np.array_equal(H4, H.astype(np.float64))
