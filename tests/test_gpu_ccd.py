@@ -93,18 +93,19 @@ def test_layout_strategies(name):
 
 
 @pytest.mark.timeout(600)
-def test_medium_full_size():
-    ds = synth.load("medium")
+@pytest.mark.parametrize("name", ["medium", "large"])
+def test_full_size(name):
+    ds = synth.load(name)
     w = ds.workload
-    print(f"case: element-wise CCD medium {w.m} x {w.n}, nnz {w.nnz}", flush=True)
+    print(f"case: element-wise CCD {name} {w.m} x {w.n}, nnz {w.nnz}", flush=True)
     g, o = _pair(w.m, w.n, w.k, w.lam, ds.row, ds.col, ds.val, ds.h0(w.k))
     g.ccd_run(1)
     o.ccd_run(1)
     ew, eh = _errs(g, o)
-    print(f"medium after 1 outer: W err {ew:.3e}  H err {eh:.3e}")
+    print(f"{name} after 1 outer: W err {ew:.3e}  H err {eh:.3e}")
     assert ew <= 1e-3 and eh <= 1e-3
     g.ccd_run(2)
     o.ccd_run(2)
-    print(f"medium after 3 outer: train RMSE {g.train_rmse():.7f} vs {o.train_rmse():.7f}")
+    print(f"{name} after 3 outer: train RMSE {g.train_rmse():.7f} vs {o.train_rmse():.7f}")
     assert abs(g.train_rmse() - o.train_rmse()) <= 1e-4
     assert g.check_consistency() == 0
