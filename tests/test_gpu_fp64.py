@@ -156,3 +156,10 @@ def test_full_size_one_outer(name):
     assert ew <= W_TOL and eh <= W_TOL
     assert abs(g.train_rmse() - o.train_rmse()) <= RMSE_TOL
     assert g.check_consistency() == 0
+    if name == "medium":  # on to the full schedule
+        g.run(w.outer - 1, w.inner)
+        o.run(w.outer - 1, w.inner)
+        print(f"fp64 {name} after {w.outer} x {w.inner}: train RMSE {g.train_rmse():.12f} vs "
+              f"{o.train_rmse():.12f}")
+        assert abs(g.train_rmse() - o.train_rmse()) <= RMSE_TOL
+        assert g.check_consistency() == 0
