@@ -30,7 +30,9 @@ namespace ccdk {
 // (numerator, denominator) and a combine kernel adds a row's partials in tile
 // order.  A layout whose tiles would hold too few entries per segment keeps
 // P == 1 and becomes a hot layout (below); a forced "global" layout gathers
-// everything from global memory.
+// everything from global memory.  The item-major copy may instead be split in
+// two layouts over its rows: the longest rows tiled, the others hot, their
+// values in one array (api.hip).
 //
 // Persistent workgroups of kWG threads each own an equal, contiguous share of
 // the layout's (tile-major) entries (two shares per CU when every wave still

@@ -143,3 +143,29 @@ def test_split_rows_arguments():
         with pytest.raises(CCDPPError) as ei:
             CCDPP(M, N, K, 0.1, row, col, val, opts=make_options(**kw))
         assert ei.value.code == CCDPP_EINVAL and "split_rows" in str(ei.value)
+
+
+def test_split_copy_cache_policies_and_index_coding_are_bitwise_neutral():
+    """On a split copy, the tiled part takes the write-back policies and delta-coded
+    indices, the hot part streams; none of them changes a bit of the results."""
+    row, col, val, H0 = _prob()
+    print("case: split copy, cache policies and index coding", flush=True)
+    ref = None
+    for kw in (dict(cache=(1, 1), index_coding=(1, 1)), dict(cache=(1, 1)), dict(cache=(1, 2)),
+               dict(cache=(1, 3)), dict(cache=(2, 2), index_coding=(0, 1))):
+        g = CCDPP(M, N, K, 0.1, row, col, val, opts=make_options(split_rows=40, **kw))
+        info = g.info()
+        assert info["v_split_rows"] == 40 and info["v2_cache"] == 1
+        assert info["v_cache"] == kw["cache"][1]
+        g.set_factors(np.zeros((M, K), np.float32), H0)
+        g.run(1, 2)
+        g.run(1, 1)
+        g.ccd_run(1)
+        out = g.factors() + (g.residual(),)
+        assert g.check_consistency() == 0
+        g.close()
+        if ref is None:
+            ref = out
+        else:
+            for a, b in zip(ref, out):
+                assert np.array_equal(a, b), f"{kw} differs"
