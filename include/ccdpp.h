@@ -260,8 +260,10 @@ int ccdpp_get_residual_f64(ccdpp_t *h, double *R);
 int ccdpp_check_consistency(ccdpp_t *h, int64_t *mismatches);
 
 /* Use this HIP stream (a hipStream_t, e.g. PyTorch's current stream) for all
- * later work; NULL selects the handle's own stream.  The stream must belong
- * to the handle's device and outlive its use. */
+ * later work; NULL selects the device's null stream, which a handle uses from
+ * its creation on (the device build included).  The stream must belong to the
+ * handle's device and outlive its use.  Waits for the work already enqueued on
+ * the previous stream. */
 int ccdpp_set_stream(ccdpp_t *h, void *hip_stream);
 
 /* Kernel timing.  When enabled, every kernel launch of ccdpp_run is bracketed
@@ -311,7 +313,8 @@ int ccdpp_profile_read(ccdpp_t *h, int32_t kind, int32_t layout, int64_t *launch
  *   cache policy (zeros when not split), [35..40] the device build's phases in
  *   microseconds: inputs copied and degrees counted; relabelling; the
  *   user-major copy; the item-major copy and the map between the copies;
- *   cache policies, index coding and scratch; the factors.
+ *   cache policies, index coding and scratch; the factors; [41] the device
+ *   set-up before them (device checks, kernel attributes, scratch address).
  * Returns the number of values written. */
 int ccdpp_info(ccdpp_t *h, int64_t *out, int32_t len);
 

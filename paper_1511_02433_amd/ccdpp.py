@@ -274,7 +274,7 @@ INFO_FIELDS = ("m", "n", "nnz", "k", "build_us", "u_gather", "u_tiles", "u_tile_
                "v_split_rows", "v2_gather", "v2_tile_width", "v2_workgroups", "v2_segments",
                "v2_rows_finished_in_pass", "v2_rows_combined", "v2_cache", "build_inputs_us",
                "build_relabel_us", "build_user_major_us", "build_item_major_us", "build_setup_us",
-               "build_factors_us")
+               "build_factors_us", "build_device_setup_us")
 
 
 def ccdpp_info(h):

@@ -21,6 +21,7 @@
 #include "ccdpp_internal.hpp"
 
 using ccdk::Layout;
+using ccdk::Stager;
 
 namespace {
 
@@ -96,8 +97,7 @@ struct ccdpp {
     double lambda = 0.0;
     int device = 0;
     int cus = 0;
-    hipStream_t own_stream = nullptr;
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr;  // the device's null stream unless the caller sets one
     // 0: rows are users (eq. 15); 1: rows are items (eq. 16).  When the item-major copy
     // is split, L[1] holds its rows 0 .. split - 1 (the items with the most ratings),
     // tiled, and L[2] the others as a hot layout, its row r being item split + r; the
@@ -137,8 +137,9 @@ struct ccdpp {
     int64_t build_us = 0;
     // Device build phases, microseconds: inputs and degrees; relabelling; user-major copy;
     // item-major copy and the map between the copies; cache policy, index coding and
-    // scratch; factors.
-    int64_t build_phase_us[6] = {};
+    // scratch; factors; the device set-up before the inputs (device checks, kernel
+    // attributes, scratch address).
+    int64_t build_phase_us[7] = {};
     int64_t bytes_held = 0;
     std::vector<std::pair<void*, int64_t>> allocs;  // device allocations and their sizes
     // kernel timing
@@ -368,6 +369,8 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             HIPCK(h, hipMemcpyAsync(cnt.data(), d_cnt, (size_t)(P * rows) * 4,
                                     hipMemcpyDeviceToHost, s));
             HIPCK(h, hipStreamSynchronize(s));
+            if (std::accumulate(cnt.begin(), cnt.end(), int64_t(0)) != N)
+                return fail(h, CCDPP_EDEVICE, "segment counts do not add up to nnz");
         }
         if (P == 1 || forced == kGatherLds) break;
         // Tiling pays only when segments are long enough; otherwise stage the leading
@@ -981,9 +984,8 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
         }
         h->scratch = g_scratch_dev[h->device];
     }
-    HIPCK(h, hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
-    h->stream = h->own_stream;
     hipStream_t s = h->stream;
+    phase(6);
 
     // Inputs and degrees.
     int32_t *d_row, *d_col, *d_cnt_r, *d_cnt_c;
@@ -994,19 +996,22 @@ int create_device(ccdpp* h, const int32_t* row, const int32_t* col, const float*
     HIPCK(h, talloc(t_val, &d_val, N));
     HIPCK(h, talloc(t_cr, &d_cnt_r, m));
     HIPCK(h, talloc(t_cc, &d_cnt_c, n));
-    if (N) {
-        HIPCK(h, hipMemcpyAsync(d_row, row, N * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, hipMemcpyAsync(d_col, col, N * 4, hipMemcpyHostToDevice, s));
-        HIPCK(h, hipMemcpyAsync(d_val, val, N * 4, hipMemcpyHostToDevice, s));
-    }
+    Stager stage(s);
+    HIPCK(h, stage.copy(d_row, row, (size_t)N * 4));
+    HIPCK(h, stage.copy(d_col, col, (size_t)N * 4));
+    HIPCK(h, stage.copy(d_val, val, (size_t)N * 4));
     HIPCK(h, hipMemsetAsync(d_cnt_r, 0, m * 4, s));
     HIPCK(h, hipMemsetAsync(d_cnt_c, 0, n * 4, s));
-    HIPCK(h, launch_histogram(d_row, N, d_cnt_r, s));
-    HIPCK(h, launch_histogram(d_col, N, d_cnt_c, s));
+    HIPCK(h, launch_histogram(d_row, N, (int32_t)m, d_cnt_r, h->cus, s));
+    HIPCK(h, launch_histogram(d_col, N, (int32_t)n, d_cnt_c, h->cus, s));
     std::vector<int32_t> cnt_r(m), cnt_c(n);
     HIPCK(h, hipMemcpyAsync(cnt_r.data(), d_cnt_r, m * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipMemcpyAsync(cnt_c.data(), d_cnt_c, n * 4, hipMemcpyDeviceToHost, s));
     HIPCK(h, hipStreamSynchronize(s));
+    // The layout places entries by these counts; they must cover every entry once.
+    if (std::accumulate(cnt_r.begin(), cnt_r.end(), int64_t(0)) != N ||
+        std::accumulate(cnt_c.begin(), cnt_c.end(), int64_t(0)) != N)
+        return fail(h, CCDPP_EDEVICE, "degree counts do not add up to nnz");
     phase(0);
 
     // Relabel users and items by decreasing degree.
@@ -1109,7 +1114,6 @@ void destroy_all(ccdpp* h) {
         h->event_pool.push_back(pe.b);
     }
     for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
-    if (h->own_stream) (void)hipStreamDestroy(h->own_stream);
 }
 
 // ---- kernel timing ---------------------------------------------------------------
@@ -1296,13 +1300,24 @@ int create_impl(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, con
         if (opts->split_rows > 0 && opts->gather_mode[1] != 0)
             return fail(nullptr, CCDPP_EINVAL, "split_rows needs gather_mode[1] = 0");
     }
-    for (int64_t e = 0; e < nnz; ++e) {
+    // The first bad triplet, searched by a few host threads over contiguous ranges.
+    const int workers = ccdk::host_workers();
+    std::vector<int64_t> first_bad(workers, nnz);
+    ccdk::parallel_ranges(nnz, workers, [&](int w, int64_t lo, int64_t hi) {
+        for (int64_t e = lo; e < hi; ++e) {
+            if (row[e] < 0 || row[e] >= m || col[e] < 0 || col[e] >= n || !std::isfinite(val[e])) {
+                first_bad[w] = e;
+                return;
+            }
+        }
+    });
+    const int64_t e = *std::min_element(first_bad.begin(), first_bad.end());
+    if (e < nnz) {
         if (row[e] < 0 || row[e] >= m)
             return fail(nullptr, CCDPP_EINVAL, "row[%lld] = %d out of range", (long long)e, row[e]);
         if (col[e] < 0 || col[e] >= n)
             return fail(nullptr, CCDPP_EINVAL, "col[%lld] = %d out of range", (long long)e, col[e]);
-        if (!std::isfinite(val[e]))
-            return fail(nullptr, CCDPP_EINVAL, "val[%lld] is not finite", (long long)e);
+        return fail(nullptr, CCDPP_EINVAL, "val[%lld] is not finite", (long long)e);
     }
     ccdpp* h = new (std::nothrow) ccdpp();
     if (!h) return fail(nullptr, CCDPP_ENOMEM, "host allocation failed");
@@ -1785,7 +1800,7 @@ int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
 int ccdpp_set_stream(ccdpp_t* h, void* hip_stream) {
     if (!usable(h)) return CCDPP_ESTATE;
     HIPCK(h, hipStreamSynchronize(h->stream));
-    h->stream = hip_stream ? static_cast<hipStream_t>(hip_stream) : h->own_stream;
+    h->stream = static_cast<hipStream_t>(hip_stream);
     return CCDPP_OK;
 }
 
@@ -1848,7 +1863,7 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
     };
     const ccdk::Layout& L2 = h->L[2];
     const bool sp = h->split > 0;
-    const int64_t v[41] = {h->m,         h->n,         h->nnz,       h->k,
+    const int64_t v[42] = {h->m,         h->n,         h->nnz,       h->k,
                            h->build_us,  h->L[0].gather, h->L[0].P,  width(h->L[0]),
                            h->L[0].grid, h->L[0].nseg, h->L[1].gather, h->L[1].P,
                            width(h->L[1]), h->L[1].grid, h->L[1].nseg, h->bytes_held,
@@ -1860,8 +1875,8 @@ int ccdpp_info(ccdpp_t* h, int64_t* out, int32_t len) {
                            sp ? L2.nseg : 0, sp ? L2.ncut : 0, sp ? L2.ncomb : 0,
                            sp ? L2.cache + 1 : 0, h->build_phase_us[0], h->build_phase_us[1],
                            h->build_phase_us[2], h->build_phase_us[3], h->build_phase_us[4],
-                           h->build_phase_us[5]};
-    int32_t w = std::min<int32_t>(len, 41);
+                           h->build_phase_us[5], h->build_phase_us[6]};
+    int32_t w = std::min<int32_t>(len, 42);
     for (int32_t i = 0; i < w; ++i) out[i] = v[i];
     return w;
 }

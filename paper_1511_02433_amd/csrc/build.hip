@@ -11,6 +11,7 @@
 #include <rocprim/device/device_select.hpp>
 #include <rocprim/iterator/counting_iterator.hpp>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "ccdpp_internal.hpp"
@@ -19,6 +20,8 @@ namespace ccdk {
 namespace {
 
 constexpr int kT = 256;
+// Histograms with at most this many bins count in LDS (128 KB per workgroup).
+constexpr int32_t kHistLdsBins = 32768;
 
 inline dim3 grid_for(int64_t n, int64_t cap = 1 << 20) {
     int64_t g = (n + kT - 1) / kT;
@@ -27,9 +30,55 @@ inline dim3 grid_for(int64_t n, int64_t cap = 1 << 20) {
     return dim3((unsigned)g);
 }
 
-__global__ void k_histogram(const int32_t* __restrict__ key, int64_t n, int32_t* count) {
-    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < n; e += (int64_t)gridDim.x * kT)
-        atomicAdd(&count[key[e]], 1);
+// Adds one to count[key] for every valid lane of the wave.  A lane whose key equals
+// the previous lane's (a run, as in triplets grouped by row) adds through the run's
+// first lane, so a run costs one atomic.  The valid lanes are a prefix of the wave,
+// and every lane of the wave calls this.
+__device__ inline void count_runs(int32_t key, bool valid, int32_t* count) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int32_t prev = __shfl_up(key, 1);
+    const bool head = valid && (lane == 0 || prev != key);
+    const uint64_t heads = __ballot(head);
+    const int nvalid = __popcll(__ballot(valid));
+    if (head) {
+        const uint64_t later = lane == 63 ? 0 : heads >> (lane + 1);
+        const int next = later ? lane + __ffsll((unsigned long long)later) : nvalid;
+        atomicAdd(&count[key], next - lane);
+    }
+}
+
+// Range [lo, hi) of entries of workgroup blockIdx.x: contiguous, so that runs stay in
+// one wave.
+__device__ inline void block_range(int64_t n, int64_t* lo, int64_t* hi) {
+    const int64_t per = ((n + gridDim.x - 1) / gridDim.x + 63) / 64 * 64;
+    *lo = min(n, (int64_t)blockIdx.x * per);
+    *hi = min(n, *lo + per);
+}
+
+// count[key[e]] += 1 for every e < n.  bins <= kHistLdsBins: the workgroup counts in
+// LDS and adds its non-zero counts at the end; else straight into global memory.
+template <bool kLds>
+__global__ void __launch_bounds__(1024) k_histogram(const int32_t* __restrict__ key, int64_t n,
+                                                    int32_t bins, int32_t* count) {
+    extern __shared__ int32_t lds_count[];
+    int32_t* c = count;
+    if constexpr (kLds) {
+        for (int32_t b = threadIdx.x; b < bins; b += blockDim.x) lds_count[b] = 0;
+        __syncthreads();
+        c = lds_count;
+    }
+    int64_t lo, hi;
+    block_range(n, &lo, &hi);
+    for (int64_t base = lo + (threadIdx.x & ~63); base < hi; base += blockDim.x) {
+        const int64_t e = base + (threadIdx.x & 63);
+        const bool valid = e < hi;
+        count_runs(valid ? key[e] : 0, valid, c);
+    }
+    if constexpr (kLds) {
+        __syncthreads();
+        for (int32_t b = threadIdx.x; b < bins; b += blockDim.x)
+            if (lds_count[b]) atomicAdd(&count[b], lds_count[b]);
+    }
 }
 
 __global__ void k_add(int32_t* __restrict__ a, int64_t n, int32_t delta) {
@@ -51,12 +100,16 @@ __global__ void k_map(const int32_t* __restrict__ in, const int32_t* __restrict_
 }
 
 // Entries per (tile, row) segment: count[(col / T) * rows + row].
-__global__ void k_seg_histogram(const int32_t* __restrict__ lrow, const int32_t* __restrict__ lcol,
-                                int64_t nnz, int32_t rows, int32_t T, int32_t* count) {
-    for (int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x; e < nnz;
-         e += (int64_t)gridDim.x * kT) {
-        const int64_t p = lcol[e] / T;
-        atomicAdd(&count[p * rows + lrow[e]], 1);
+__global__ void __launch_bounds__(kT) k_seg_histogram(const int32_t* __restrict__ lrow,
+                                                      const int32_t* __restrict__ lcol, int64_t nnz,
+                                                      int32_t rows, int32_t T, int32_t* count) {
+    int64_t lo, hi;
+    block_range(nnz, &lo, &hi);
+    for (int64_t base = lo + (threadIdx.x & ~63); base < hi; base += blockDim.x) {
+        const int64_t e = base + (threadIdx.x & 63);
+        const bool valid = e < hi;
+        const int32_t key = valid ? (lcol[e] / T) * rows + lrow[e] : 0;
+        count_runs(key, valid, count);
     }
 }
 
@@ -384,9 +437,21 @@ __global__ void k_test_err(const int32_t* __restrict__ row, const int32_t* __res
 
 }  // namespace
 
-hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t* count, hipStream_t s) {
+hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t bins, int32_t* count,
+                           int32_t workgroups, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_histogram, grid_for(n, 8192), dim3(kT), 0, s, key, n, count);
+    if (bins <= kHistLdsBins) {
+        const size_t lds = (size_t)bins * 4;
+        hipError_t e = hipFuncSetAttribute((const void*)k_histogram<true>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        const int64_t g = std::min<int64_t>(workgroups, (n + 1023) / 1024);
+        hipLaunchKernelGGL(k_histogram<true>, dim3((unsigned)g), dim3(1024), lds, s, key, n, bins,
+                           count);
+    } else {
+        hipLaunchKernelGGL(k_histogram<false>, grid_for(n, 8192), dim3(kT), 0, s, key, n, bins,
+                           count);
+    }
     return hipGetLastError();
 }
 

@@ -3,6 +3,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <functional>
+
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -302,6 +304,37 @@ struct Layout {
     int32_t grid = 0;                // persistent workgroups per pass
 };
 
+// Host helpers (host_copy.hip).  host_workers(): the host threads a set-up loop uses
+// (at most 8).  parallel_ranges(n, w, f): f(worker, lo, hi) over w contiguous ranges of
+// [0, n), the last on the calling thread; returns when all have finished.
+int host_workers();
+void parallel_ranges(int64_t n, int workers, const std::function<void(int, int64_t, int64_t)>& f);
+
+// Host-to-device copies of caller memory on one stream through two pinned 32 MiB
+// staging buffers (copies under 4 MiB, or without pinned memory, go straight).  The
+// source may be reused once copy() returns; finish() waits until the staging
+// buffers are read, and the destructor does so too before freeing them.
+class Stager {
+public:
+    explicit Stager(hipStream_t s);
+    ~Stager();
+    Stager(const Stager&) = delete;
+    Stager& operator=(const Stager&) = delete;
+    hipError_t copy(void* dst, const void* src, size_t bytes);
+    hipError_t finish();
+
+private:
+    bool ready();
+    void release();
+    hipStream_t s_;
+    int workers_;
+    void* slot_[2] = {nullptr, nullptr};
+    hipEvent_t ev_[2] = {nullptr, nullptr};
+    bool busy_[2] = {false, false};
+    int next_ = 0;
+    bool tried_ = false;
+};
+
 // Every device allocation of the library (api.hip); a host-forced failure for tests
 // of the error paths returns hipErrorOutOfMemory.
 hipError_t dev_malloc(void** p, size_t bytes);
@@ -320,7 +353,10 @@ hipError_t launch_reduce_sum(const double* part, int32_t n, double* out, hipStre
 int staged_vectors(PassMode mode, bool x_is_q);
 
 // Device build and utilities (build.hip); V as above, S a host-side element type.
-hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t* count, hipStream_t s);
+// count[key[e]] += 1 over e < n, key[e] < bins (count zeroed by the caller); at most
+// `workgroups` workgroups when the bins fit LDS.
+hipError_t launch_histogram(const int32_t* key, int64_t n, int32_t bins, int32_t* count,
+                           int32_t workgroups, hipStream_t s);
 hipError_t launch_map(const int32_t* in, const int32_t* table, int64_t n, int32_t* out,
                       hipStream_t s);
 hipError_t launch_seg_histogram(const int32_t* lrow, const int32_t* lcol, int64_t nnz,

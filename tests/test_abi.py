@@ -120,3 +120,28 @@ def test_without_a_device_create_reports_edevice():
     with pytest.raises(C.CCDPPError) as ei:
         _create()
     assert ei.value.code == C.CCDPP_EDEVICE
+
+
+def test_create_reports_the_first_bad_triplet():
+    """Triplets are checked by several host threads over contiguous ranges; the error
+    still names the first bad one in input order."""
+    _lib_or_skip()
+    nnz = 200_003
+    row = np.arange(nnz, dtype=np.int32) % 97
+    col = np.arange(nnz, dtype=np.int32) % 89
+    val = np.ones(nnz, np.float32)
+    val[190_000] = np.nan
+    col[150_001] = 89
+    row[120_000] = -3
+    with pytest.raises(C.CCDPPError) as ei:
+        C.ccdpp_create_ex(97, 89, 2, 0.1, row, col, val, 0, None)
+    assert ei.value.code == C.CCDPP_EINVAL
+    assert "row[120000] = -3 out of range" in str(ei.value)
+    row[120_000] = 0
+    with pytest.raises(C.CCDPPError) as ei:
+        C.ccdpp_create_ex(97, 89, 2, 0.1, row, col, val, 0, None)
+    assert "col[150001] = 89 out of range" in str(ei.value)
+    col[150_001] = 0
+    with pytest.raises(C.CCDPPError) as ei:
+        C.ccdpp_create_ex(97, 89, 2, 0.1, row, col, val, 0, None)
+    assert "val[190000] is not finite" in str(ei.value)

@@ -1,0 +1,66 @@
+"""The stream a handle works on: the device's null stream by default (the device
+build included), a caller's stream after ccdpp_set_stream, and back.  The results
+do not depend on it, bit for bit, and each call still returns with its work done."""
+import numpy as np
+import pytest
+
+from oracle import Oracle
+from paper_1511_02433_amd import synth
+from paper_1511_02433_amd.ccdpp import CCDPP
+from gpu_util import colscaled_max_rel_err
+
+pytestmark = pytest.mark.gpu
+
+M, N, K, LAM = 2000, 700, 5, 0.05
+
+
+def _problem():
+    return synth.small_random(M, N, 60_000, K, seed=77)
+
+
+def _run(row, col, val, H0, streams):
+    """One outer iteration per entry of `streams` (None: the null stream)."""
+    g = CCDPP(M, N, K, LAM, row, col, val)
+    g.set_factors(np.zeros((M, K), np.float32), H0)
+    for s in streams:
+        g.set_stream(s)
+        g.run(1, 3)
+    W, H = g.factors()
+    rmse = g.train_rmse()
+    assert g.check_consistency() == 0
+    g.close()
+    return W, H, rmse
+
+
+def test_results_do_not_depend_on_the_stream():
+    import torch
+
+    row, col, val, H0 = _problem()
+    side = torch.cuda.Stream()
+    other = torch.cuda.Stream()
+    ref = _run(row, col, val, H0, [None, None, None])
+    for streams in ([side.cuda_stream] * 3, [side.cuda_stream, None, other.cuda_stream]):
+        W, H, rmse = _run(row, col, val, H0, streams)
+        assert np.array_equal(W, ref[0]) and np.array_equal(H, ref[1])
+        assert rmse == ref[2]
+    o = Oracle(M, N, K, LAM, row, col, val, H0)
+    o.run(3, 3)
+    Wo, Ho = o.factors()
+    assert colscaled_max_rel_err(ref[0], Wo) <= 1e-3 and colscaled_max_rel_err(ref[1], Ho) <= 1e-3
+
+
+def test_torch_current_stream():
+    """use_torch_stream() inside a PyTorch stream context runs on that stream."""
+    import torch
+
+    row, col, val, H0 = _problem()
+    side = torch.cuda.Stream()
+    g = CCDPP(M, N, K, LAM, row, col, val)
+    with torch.cuda.stream(side):
+        g.use_torch_stream()
+        g.set_factors(np.zeros((M, K), np.float32), H0)
+        g.run(2, 3)
+    W, H = g.factors()
+    g.close()
+    Wr, Hr, _ = _run(row, col, val, H0, [None, None])
+    assert np.array_equal(W, Wr) and np.array_equal(H, Hr)
