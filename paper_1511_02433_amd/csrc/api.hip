@@ -285,16 +285,21 @@ void relabel(const std::vector<int32_t>& count, std::vector<int32_t>& new2old,
 // takes.
 int64_t choose_split(const std::vector<int32_t>& cnt, int64_t P, int64_t rows, int64_t T,
                      int64_t hot, int64_t seg_cost) {
+    // Segments and cold entries per row, gathered tile by tile (cnt is tile-major).
+    std::vector<int32_t> segs((size_t)rows, 0);
+    std::vector<int64_t> cold((size_t)rows, 0);
+    for (int64_t p = 0; p < P; ++p) {
+        const int32_t* cp = cnt.data() + p * rows;
+        const bool is_cold = p * T >= hot;
+        for (int64_t r = 0; r < rows; ++r) {
+            segs[r] += cp[r] > 0;
+            if (is_cold) cold[r] += cp[r];
+        }
+    }
     int64_t best = 0, H = 0, gain = 0;
     for (int64_t r = 0; r < rows; ++r) {
-        int64_t segs = 0, cold = 0;
-        for (int64_t p = 0; p < P; ++p) {
-            const int32_t c = cnt[(size_t)(p * rows + r)];
-            segs += c > 0;
-            if (p * T >= hot) cold += c;
-        }
-        if (segs == 0) break;  // the empty rows come last
-        gain += cold - seg_cost * segs;
+        if (segs[r] == 0) break;  // the empty rows come last
+        gain += cold[r] - seg_cost * segs[r];
         if (gain > best) {
             best = gain;
             H = r + 1;
@@ -665,16 +670,19 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
             L.ncomb = (int32_t)ids.size();
             if (!ids.empty()) RCK(upload(h, &L.comb_rows, ids));
         } else {
-            gptr.assign(1, 0);
+            // The segments of each row in tile order: segment ids grow with the tile, so
+            // bucketing them by row in id order lists each row's in tile order.
+            gptr.assign((size_t)rows + 1, 0);
+            for (int64_t sg = 0; sg < S; ++sg) ++gptr[seg_row[sg] + 1];
+            for (int64_t r = 0; r < rows; ++r) gptr[r + 1] += gptr[r];
+            gsegs.resize((size_t)S);
+            {
+                std::vector<int32_t> next(gptr.begin(), gptr.end() - 1);
+                for (int64_t sg = 0; sg < S; ++sg) gsegs[next[seg_row[sg]]++] = (int32_t)sg;
+            }
             for (int64_t r = 0; r < rows; ++r) {
-                for (int64_t p = 0; p < P; ++p) {
-                    const int32_t sg = segid[p * rows + r];
-                    if (sg < 0) continue;
-                    add_seg(sg);
-                    gsegs.push_back(sg);
-                }
+                for (int32_t i = gptr[r]; i < gptr[r + 1]; ++i) add_seg(gsegs[i]);
                 sptr.push_back((int32_t)srcs.size());
-                gptr.push_back((int32_t)gsegs.size());
             }
             L.ncomb = (int32_t)rows;
             RCK(upload(h, &L.row_seg_ptr, gptr));
