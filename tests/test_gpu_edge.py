@@ -123,6 +123,20 @@ def test_index_width_boundary_of_global_layouts(n):
     assert g.info()["u_tile_width"] == n
 
 
+@pytest.mark.parametrize("m, n", [(32_768, 32_769), (32_769, 32_768)])
+@pytest.mark.parametrize("shuffle", [False, True])
+def test_degree_counts_at_the_lds_bin_limit(m, n, shuffle):
+    # Degrees are counted in LDS for up to 32,768 rows or columns and in global memory
+    # above; triplets grouped by row (runs of one key) or shuffled (no runs).
+    lens = list(np.random.default_rng(68).integers(1, 16, m))
+    row, col, val, H0 = synth.lengths_problem(lens, n, 2, seed=69)
+    if shuffle:
+        p = np.random.default_rng(70).permutation(row.size)
+        row, col, val = row[p], col[p], val[p]
+    print(f"case: degree counts m={m} n={n} shuffle={shuffle} nnz={row.size}", flush=True)
+    _compare(m, n, 2, 0.1, row, col, val, H0, outer=2, inner=2)
+
+
 def _splitmix64(x):
     """splitmix64 (Steele, Lea and Flood, OOPSLA 2014) on uint64 arrays."""
     with np.errstate(over="ignore"):
