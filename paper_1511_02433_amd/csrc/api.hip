@@ -559,7 +559,8 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     const int64_t work_total = work_at(NP);
     std::vector<int32_t> wg_piece(1, 0), piece_tile, piece_seg, chunk_flags;
     std::vector<int64_t> piece_chunk;
-    std::vector<std::vector<int32_t>> src_of((size_t)S);  // partial slots of each cut segment
+    // Partial slots of the cut segments, as (segment, slot) in the order the chunks are cut.
+    std::vector<std::pair<int32_t, int32_t>> cuts;
     std::vector<int64_t> gb((size_t)G + 1);
     for (int64_t g = 0; g <= G; ++g) {
         gb[g] = g == 0 ? 0 : g == G ? NP
@@ -592,12 +593,28 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
                 const bool cont = seg_start[s1 + 1] > c1;  // last segment goes on
                 piece_seg.push_back((int32_t)s0);
                 chunk_flags.push_back((mid ? kChunkMid : 0) | (cont ? kChunkCont : 0));
-                if (mid) src_of[s0].push_back((int32_t)(S + 2 * gc));
-                if (cont && !(mid && s1 == s0)) src_of[s1].push_back((int32_t)(S + 2 * gc + 1));
+                if (mid) cuts.emplace_back((int32_t)s0, (int32_t)(S + 2 * gc));
+                if (cont && !(mid && s1 == s0)) cuts.emplace_back((int32_t)s1, (int32_t)(S + 2 * gc + 1));
             }
         }
         wg_piece.push_back((int32_t)piece_tile.size());
     }
+    // Grouped by segment (a stable sort keeps each segment's slots in entry order):
+    // cut_seg[c] is the c-th cut segment, its slots cut_slot[cut_off[c] .. cut_off[c + 1]).
+    std::stable_sort(cuts.begin(), cuts.end(),
+                     [](const std::pair<int32_t, int32_t>& a, const std::pair<int32_t, int32_t>& b) {
+                         return a.first < b.first;
+                     });
+    std::vector<int32_t> cut_seg, cut_slot, cut_off(1, 0);
+    for (const auto& c : cuts) {
+        if (cut_seg.empty() || cut_seg.back() != c.first) {
+            if (!cut_seg.empty()) cut_off.push_back((int32_t)cut_slot.size());
+            cut_seg.push_back(c.first);
+        }
+        cut_slot.push_back(c.second);
+    }
+    if (!cut_seg.empty()) cut_off.push_back((int32_t)cut_slot.size());
+    std::vector<char> cut_fin(cut_seg.size(), 0);  // finished by its workgroup in the pass
     L.grid = (int32_t)G;
     L.npieces = (int32_t)piece_tile.size();
     const int64_t nslots = S + 2 * (int64_t)L.npieces * kWaves;
@@ -617,21 +634,22 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
         std::vector<int32_t> wcut(1, 0), crow;
         std::vector<uint64_t> cdesc;
         std::vector<std::vector<int64_t>> local((size_t)G);
-        for (int64_t sg = 0; snapped && sg < S; ++sg) {
-            const auto& sl = src_of[sg];
-            if (sl.empty() || (int)sl.size() > kCutMaxSlots) continue;
+        for (size_t c = 0; snapped && c < cut_seg.size(); ++c) {
+            const int32_t* sl = cut_slot.data() + cut_off[c];
+            const int32_t ns = cut_off[c + 1] - cut_off[c];
+            if (ns > kCutMaxSlots) continue;
             const int32_t g0 = slot_wg(sl[0]);
             bool one = true;
-            for (int32_t x : sl) one = one && slot_wg(x) == g0;
+            for (int32_t i = 0; i < ns; ++i) one = one && slot_wg(sl[i]) == g0;
             if (!one) continue;
             // Local slot 2w (head) or 2w + 1 (tail) of wave w: the workgroup has one piece.
-            uint64_t d = (uint64_t)(sl.size() - 1);
-            for (size_t i = 0; i < sl.size(); ++i)
+            uint64_t d = (uint64_t)(ns - 1);
+            for (int32_t i = 0; i < ns; ++i)
                 d |= (uint64_t)((sl[i] - S) % (2 * kWaves)) << (4 + 5 * i);
             if (local[g0].size() >= 64) return fail(h, CCDPP_EDEVICE, "internal: too many cut rows");
-            local[g0].push_back(sg);
+            local[g0].push_back(cut_seg[c]);
             cdesc.push_back(d);
-            src_of[sg].insert(src_of[sg].begin(), -1);  // finished in the pass
+            cut_fin[c] = 1;
         }
         std::vector<uint64_t> cdesc_sorted;
         {
@@ -654,17 +672,14 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     }
     {
         std::vector<int32_t> ids, sptr(1, 0), srcs, gptr, gsegs;
-        auto add_seg = [&](int64_t sg) {
-            if (src_of[sg].empty())
-                srcs.push_back((int32_t)sg);
-            else
-                srcs.insert(srcs.end(), src_of[sg].begin(), src_of[sg].end());
+        auto add_cut = [&](size_t c) {
+            srcs.insert(srcs.end(), cut_slot.begin() + cut_off[c], cut_slot.begin() + cut_off[c + 1]);
         };
         if (P == 1) {
-            for (int64_t sg = 0; sg < S; ++sg)
-                if (!src_of[sg].empty() && src_of[sg][0] >= 0) {
-                    ids.push_back((int32_t)sg);
-                    add_seg(sg);
+            for (size_t c = 0; c < cut_seg.size(); ++c)
+                if (!cut_fin[c]) {
+                    ids.push_back(cut_seg[c]);
+                    add_cut(c);
                     sptr.push_back((int32_t)srcs.size());
                 }
             L.ncomb = (int32_t)ids.size();
@@ -680,8 +695,16 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
                 std::vector<int32_t> next(gptr.begin(), gptr.end() - 1);
                 for (int64_t sg = 0; sg < S; ++sg) gsegs[next[seg_row[sg]]++] = (int32_t)sg;
             }
+            std::vector<int32_t> cut_of((size_t)S, -1);  // index into cut_seg, or -1
+            for (size_t c = 0; c < cut_seg.size(); ++c) cut_of[cut_seg[c]] = (int32_t)c;
             for (int64_t r = 0; r < rows; ++r) {
-                for (int32_t i = gptr[r]; i < gptr[r + 1]; ++i) add_seg(gsegs[i]);
+                for (int32_t i = gptr[r]; i < gptr[r + 1]; ++i) {
+                    const int32_t sg = gsegs[i];
+                    if (cut_of[sg] < 0)
+                        srcs.push_back(sg);
+                    else
+                        add_cut((size_t)cut_of[sg]);
+                }
                 sptr.push_back((int32_t)srcs.size());
             }
             L.ncomb = (int32_t)rows;
