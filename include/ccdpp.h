@@ -27,7 +27,8 @@
  *  - Factor matrices at the boundary are row-major float32: W is m x k
  *    (row i = w_i), H is n x k (row j = h_j).
  *  - The handle owns all device memory (on the device that was current at
- *    ccdpp_create) and is not thread-safe.
+ *    ccdpp_create) and is not thread-safe.  Every call on a handle makes
+ *    that device current while it runs and restores the caller's afterwards.
  *  - Calls return CCDPP_OK (0) or a negative status.  Out-parameters are left
  *    untouched on error.  After a device error the handle answers every
  *    later call with CCDPP_ESTATE until it is destroyed.  A failed device

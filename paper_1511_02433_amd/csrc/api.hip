@@ -1623,6 +1623,22 @@ int get_residual_impl(ccdpp* h, S* R) {
 }
 }  // namespace
 
+// Makes the handle's device current for one call and restores the caller's after it:
+// the handle's memory, kernels and null stream all belong to that device.
+struct DeviceScope {
+    int prev = -1;
+    bool changed = false;
+    explicit DeviceScope(const ccdpp* h) {
+        if (h && hipGetDevice(&prev) == hipSuccess && prev != h->device)
+            changed = hipSetDevice(h->device) == hipSuccess;
+    }
+    ~DeviceScope() {
+        if (changed) (void)hipSetDevice(prev);
+    }
+    DeviceScope(const DeviceScope&) = delete;
+    DeviceScope& operator=(const DeviceScope&) = delete;
+};
+
 extern "C" {
 
 int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz, const int32_t* row,
@@ -1638,6 +1654,7 @@ int ccdpp_create_ex(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
 
 
 int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (outer < 0 || inner < 1)
         return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0 and inner_iters >= 1");
@@ -1645,6 +1662,7 @@ int ccdpp_run(ccdpp_t* h, int32_t outer, int32_t inner) {
 }
 
 int ccdpp_ccd_run(ccdpp_t* h, int32_t outer) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (outer < 0) return fail(h, CCDPP_EINVAL, "outer_iters must be >= 0");
     RCK(flush_pending(h));
@@ -1654,6 +1672,7 @@ int ccdpp_ccd_run(ccdpp_t* h, int32_t outer) {
 int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol,
                     int64_t test_nnz, const int32_t* test_row, const int32_t* test_col,
                     const float* test_val, double* history, int32_t* outer_done) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (!outer_done) return fail(h, CCDPP_EINVAL, "outer_done is NULL");
     if (max_outer < 0 || inner < 1)
@@ -1721,19 +1740,26 @@ int ccdpp_run_until(ccdpp_t* h, int32_t max_outer, int32_t inner, double rel_tol
 }
 
 
-int ccdpp_get_factors(ccdpp_t* h, float* W, float* H) { return get_factors_impl<float>(h, W, H); }
+int ccdpp_get_factors(ccdpp_t* h, float* W, float* H) {
+    DeviceScope dev(h);
+    return get_factors_impl<float>(h, W, H);
+}
 int ccdpp_get_factors_f64(ccdpp_t* h, double* W, double* H) {
+    DeviceScope dev(h);
     return get_factors_impl<double>(h, W, H);
 }
 int ccdpp_set_factors(ccdpp_t* h, const float* W, const float* H) {
+    DeviceScope dev(h);
     return set_factors_impl<float>(h, W, H);
 }
 int ccdpp_set_factors_f64(ccdpp_t* h, const double* W, const double* H) {
+    DeviceScope dev(h);
     return set_factors_impl<double>(h, W, H);
 }
 
 int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, const float* val,
                double* rmse_out) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (!rmse_out) return fail(h, CCDPP_EINVAL, "rmse_out is NULL");
     if (nnz < 1 || nnz > kMaxNnz) return fail(h, CCDPP_EINVAL, "nnz must be in [1, 2^31-1]");
@@ -1765,6 +1791,7 @@ int ccdpp_rmse(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col, 
 
 int ccdpp_rmse_noalloc(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_t* col,
                        const float* val, double* rmse_out) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (!rmse_out) return fail(h, CCDPP_EINVAL, "rmse_out is NULL");
     if (nnz < 1 || nnz > kMaxNnz) return fail(h, CCDPP_EINVAL, "nnz must be in [1, 2^31-1]");
@@ -1787,6 +1814,7 @@ int ccdpp_rmse_noalloc(ccdpp_t* h, int64_t nnz, const int32_t* row, const int32_
 }
 
 int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (!rmse_out) return fail(h, CCDPP_EINVAL, "rmse_out is NULL");
     if (h->nnz < 1) return fail(h, CCDPP_EINVAL, "no observed entries");
@@ -1806,10 +1834,17 @@ int ccdpp_train_rmse(ccdpp_t* h, double* rmse_out) {
 }
 
 
-int ccdpp_get_residual(ccdpp_t* h, float* R) { return get_residual_impl<float>(h, R); }
-int ccdpp_get_residual_f64(ccdpp_t* h, double* R) { return get_residual_impl<double>(h, R); }
+int ccdpp_get_residual(ccdpp_t* h, float* R) {
+    DeviceScope dev(h);
+    return get_residual_impl<float>(h, R);
+}
+int ccdpp_get_residual_f64(ccdpp_t* h, double* R) {
+    DeviceScope dev(h);
+    return get_residual_impl<double>(h, R);
+}
 
 int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (!mismatches) return fail(h, CCDPP_EINVAL, "mismatches is NULL");
     RCK(flush_pending(h));
@@ -1829,6 +1864,7 @@ int ccdpp_check_consistency(ccdpp_t* h, int64_t* mismatches) {
 }
 
 int ccdpp_set_stream(ccdpp_t* h, void* hip_stream) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     HIPCK(h, hipStreamSynchronize(h->stream));
     h->stream = static_cast<hipStream_t>(hip_stream);
@@ -1836,6 +1872,7 @@ int ccdpp_set_stream(ccdpp_t* h, void* hip_stream) {
 }
 
 int ccdpp_profile(ccdpp_t* h, int32_t enable) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     HIPCK(h, hipStreamSynchronize(h->stream));
     collect_profile(h);
@@ -1850,6 +1887,7 @@ int ccdpp_profile(ccdpp_t* h, int32_t enable) {
 }
 
 int ccdpp_profile_only(ccdpp_t* h, int32_t kind, int32_t layout) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (kind < -1 || kind >= CCDPP_K_COUNT) return fail(h, CCDPP_EINVAL, "bad kernel kind");
     if (layout < -1 || layout > 1) return fail(h, CCDPP_EINVAL, "bad layout");
@@ -1860,6 +1898,7 @@ int ccdpp_profile_only(ccdpp_t* h, int32_t kind, int32_t layout) {
 }
 
 int ccdpp_profile_every(ccdpp_t* h, int32_t every) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (every < 1) return fail(h, CCDPP_EINVAL, "every must be >= 1");
     h->prof_every = every;
@@ -1869,6 +1908,7 @@ int ccdpp_profile_every(ccdpp_t* h, int32_t every) {
 
 int ccdpp_profile_read(ccdpp_t* h, int32_t kind, int32_t layout, int64_t* launches,
                        double* total_ms, double* algo_bytes) {
+    DeviceScope dev(h);
     if (!usable(h)) return CCDPP_ESTATE;
     if (kind < 0 || kind >= CCDPP_K_COUNT) return fail(h, CCDPP_EINVAL, "bad kernel kind");
     if (layout < -1 || layout > 1) return fail(h, CCDPP_EINVAL, "bad layout");
@@ -1928,8 +1968,9 @@ const char* ccdpp_last_error(const ccdpp_t* h) {
 }
 
 void ccdpp_destroy(ccdpp_t* h) {
+    DeviceScope dev(h);
     if (!h) return;
-    if (h->stream) (void)hipStreamSynchronize(h->stream);
+    (void)hipStreamSynchronize(h->stream);
     destroy_all(h);
     delete h;
 }
