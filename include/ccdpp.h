@@ -118,10 +118,12 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 create fails with EINVAL.  Automatic: 3 on both copies
  *                 when their residual streams (values and indices) total at
  *                 most 160 MB, so that they stay in the memory-side cache;
- *                 otherwise 2 on the first copy staged with one tile, 1 on
- *                 the other, where an automatic 2 applies to ccdpp_run and
- *                 ccdpp_run_until with inner_iters >= 2 only (elsewhere the
- *                 copy streams).
+ *                 otherwise 2 on one copy and 1 on the other: the item-major
+ *                 copy takes the 2 when it is staged in LDS and not split,
+ *                 else a user-major copy staged with one tile does (neither
+ *                 does when the other copy's policy is given as 2 or 3); an
+ *                 automatic 2 applies to ccdpp_run and ccdpp_run_until with
+ *                 inner_iters >= 2 only (elsewhere the copy streams).
  *   index_coding: 0 automatic: in a copy staged in LDS with 16-bit indices
  *                 (gather_mode 2 and fewer than 32,768 tile columns) whose
  *                 cache policy is not 3, every window of 512 entries whose

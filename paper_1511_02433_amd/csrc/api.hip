@@ -850,37 +850,44 @@ int spread_factors(ccdpp* h) {
 // - when both streams fit in the memory-side cache (10M ratings: 123 MB), cached
 //   loads and stores keep them there between passes: 7% less time per outer
 //   iteration than streaming;
-// - when they do not (100M ratings: 1.23 GB), cached accesses are 13% slower,
-//   but write-back R-hat stores on one tiled copy with P == 1 make its first pass
-//   of each feature 13% faster for a 6% slower next pass over that copy (1.2% per
-//   outer iteration); on both copies together the gains cancel.
+// - when they do not (100M ratings: 1.23 GB), cached accesses are 13% slower, but
+//   write-back R-hat stores on one copy make its first pass of each feature about
+//   13% faster for a slower next pass over that copy (1.7% less time per outer
+//   iteration on the user-major copy of large, 1.6% on its item-major one); on both copies
+//   together the gains cancel, and on a split copy they are a loss.  So the item-major
+//   copy takes them when it is tiled in LDS and not split, else a user-major copy
+//   tiled with P == 1.
 int choose_cache(ccdpp* h, const ccdpp_options_t* opt) {
     using namespace ccdk;
     const int64_t vb = h->dbl ? 8 : 4;
     int64_t stream = 0;
     for (const Layout& L : h->L) stream += L.npad * (vb + (L.idx16 ? 2 : 4));
-    bool stores_given = false;
+    auto forced_of = [&](int li) { return opt ? opt->cache[li] : 0; };
+    auto eligible = [&](int part) { return !h->dbl && h->L[part].gather == kGatherLds; };
+    int wb = -1;  // the part that takes automatic write-back stores
+    if (stream > kCachedStreamBytes && forced_of(0) < 2 && forced_of(1) < 2) {
+        if (forced_of(1) == 0 && eligible(1) && h->split == 0)
+            wb = 1;
+        else if (forced_of(0) == 0 && eligible(0) && h->L[0].P == 1)
+            wb = 0;
+    }
     for (int part = 0; part < 3; ++part) {
         Layout& L = h->L[part];
         const int li = part == 0 ? 0 : 1;
         if (L.npad == 0 && part == 2) break;  // the item-major copy is not split
-        const bool eligible = !h->dbl && L.gather == kGatherLds;
-        int forced = opt ? opt->cache[li] : 0;
+        int forced = forced_of(li);
         if (part == 2 && forced > 1) forced = 1;  // a split copy's hot part always streams
         h->cache_auto[li] = forced == 0;
-        if (forced > 1 && !eligible)
+        if (forced > 1 && !eligible(part))
             return fail(h, CCDPP_EINVAL, "cache policy %d needs a tiled float copy", forced);
         if (forced > 0) {
             L.cache = forced - 1;
-        } else if (!eligible) {
+        } else if (!eligible(part)) {
             L.cache = kCacheStream;
         } else if (stream <= kCachedStreamBytes) {
             L.cache = kCacheAll;
-        } else if (L.P == 1 && !stores_given) {
-            L.cache = kCacheStores;
-            stores_given = true;
         } else {
-            L.cache = kCacheStream;
+            L.cache = part == wb ? kCacheStores : kCacheStream;
         }
     }
     return CCDPP_OK;

@@ -9,22 +9,26 @@ import bench
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
-# ccdpp_info fields of the large layouts: user-major tiled with one tile (write-back
-# stores), item-major tiled with 36 tiles (streaming).
-INFO = {"value_bytes": 4, "u_gather": 2, "u_tiles": 1, "u_tile_width": 17770, "u_cache": 2,
-        "v_gather": 2, "v_tiles": 36, "v_tile_width": 13376, "v_cache": 1}
+# ccdpp_info fields of the large layouts: user-major tiled with one tile (streaming),
+# item-major tiled with 36 tiles (write-back stores).
+INFO = {"value_bytes": 4, "u_gather": 2, "u_tiles": 1, "u_tile_width": 17770, "u_cache": 1,
+        "v_gather": 2, "v_tiles": 36, "v_tile_width": 13376, "v_cache": 2}
 
 
 def test_kernel_symbols_follow_the_layout_and_cache_policy():
     k = bench.kernel_symbol
-    assert k(0, INFO, 0) == "void ccdk::ccd_pass_fused<true, true, true, 1, float>(ccdk::PassArgs<float>)"
+    assert k(0, INFO, 0) == "void ccdk::ccd_pass_fused<true, true, true, 0, float>(ccdk::PassArgs<float>)"
+    assert k(0, INFO, 1) == "void ccdk::ccd_pass_fused<true, true, false, 1, float>(ccdk::PassArgs<float>)"
     # the plain pass stores no residual: the streaming kernel
     assert k(1, INFO, 0) == "void ccdk::ccd_pass<true, true, true, 0, float>(ccdk::PassArgs<float>)"
     assert k(1, INFO, 1) == "void ccdk::ccd_pass<true, true, false, 0, float>(ccdk::PassArgs<float>)"
-    assert k(4, INFO, 1) == "void ccdk::ccd_flush<true, true, false, 0, float>(ccdk::PassArgs<float>)"
+    assert k(4, INFO, 1) == "void ccdk::ccd_flush<true, true, false, 1, float>(ccdk::PassArgs<float>)"
     # automatic write-back stores apply to CCD++ with two or more inner iterations only
-    assert k(0, INFO, 0, wb_stores=False) == \
-        "void ccdk::ccd_pass_fused<true, true, true, 0, float>(ccdk::PassArgs<float>)"
+    assert k(0, INFO, 1, wb_stores=False) == \
+        "void ccdk::ccd_pass_fused<true, true, false, 0, float>(ccdk::PassArgs<float>)"
+    wb_user = dict(INFO, u_cache=2, v_cache=1)
+    assert k(0, wb_user, 0) == "void ccdk::ccd_pass_fused<true, true, true, 1, float>(ccdk::PassArgs<float>)"
+    assert k(4, wb_user, 1) == "void ccdk::ccd_flush<true, true, false, 0, float>(ccdk::PassArgs<float>)"
     hot = dict(INFO, v_gather=3, v_tiles=1, v_tile_width=40768, value_bytes=8)
     assert k(1, hot, 1) == "void ccdk::ccd_pass<true, false, true, 0, double>(ccdk::PassArgs<double>)"
     assert k(2, INFO, 1) == "void ccdk::ccd_combine<16, float>(ccdk::CombineArgs<float>)"

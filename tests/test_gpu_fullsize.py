@@ -49,7 +49,7 @@ def _say(msg):
 # no one-tile copy.  The gather mode of each copy (2 tiled, 3 hot), and whether the
 # item-major copy is split into tiled leading items and a hot rest: the very large
 # matrix's is (its hot part streams too).
-EXPECT_CACHE = {"medium": (3, 3), "large": (2, 1), "vlarge": (1, 1)}
+EXPECT_CACHE = {"medium": (3, 3), "large": (1, 2), "vlarge": (1, 1)}
 EXPECT_GATHER = {"medium": (2, 2), "large": (2, 2), "vlarge": (2, 2)}
 EXPECT_SPLIT = {"medium": False, "large": False, "vlarge": True}
 
