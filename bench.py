@@ -11,7 +11,7 @@ before timing.
 
   value    = 2 * inner * k * nnz / (seconds per step) / 1e9   [G nonzero visits / s]
   roofline = algorithmic bytes of the dominant kernel per launch / its mean
-             duration (HIP events on the library's stream, inside the timed
+             duration (HIP events on the handle's stream, inside the timed
              region), against 8 TB/s HBM peak.  The algorithmic bytes follow
              the byte model of the sweep with 4-byte indices and row pointers:
              a plain pass reads index and value of every entry (8 B per entry
@@ -323,7 +323,7 @@ def main():
     torch.cuda.synchronize()
     dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"]) if per_layout else None
 
-    # The timed region: exactly `steps` steps.  HIP events on the library's stream
+    # The timed region: exactly `steps` steps.  HIP events on the handle's stream
     # bracket every launch of the dominant kernel (of every kernel without warmup).
     prof = not args.no_prof
     if prof:
