@@ -324,7 +324,8 @@ def main():
     dom = max(per_layout, key=lambda kk: per_layout[kk]["total_ms"]) if per_layout else None
 
     # The timed region: exactly `steps` steps.  HIP events on the handle's stream
-    # bracket every launch of the dominant kernel (of every kernel without warmup).
+    # bracket every `event_every`-th launch of the dominant kernel (every launch of
+    # every kernel without warmup).
     prof = not args.no_prof
     if prof:
         g.profile(True)
