@@ -18,8 +18,8 @@ ARCH = "gfx950"
 # row and column copies of the residual evaluate bit-identical expressions.
 # The packed-fp32 feature is disabled for all device code.
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=off",
-          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
-          "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
+          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall", "-Werror=align-mismatch",
+          f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _compile(src: str, obj: str) -> str:

@@ -191,13 +191,6 @@ __device__ __forceinline__ double wave_sum(double x) {
     return xor32_sum(x);
 }
 
-__device__ __forceinline__ int64_t lane_i64(int64_t v, int src) {
-    const int2 p = __builtin_bit_cast(int2, v);
-    int2 r;
-    r.x = __builtin_amdgcn_readlane(p.x, src);
-    r.y = __builtin_amdgcn_readlane(p.y, src);
-    return __builtin_bit_cast(int64_t, r);
-}
 __device__ __forceinline__ double lane_f64(double v, int src) {
     const int2 p = __builtin_bit_cast(int2, v);
     int2 r;
@@ -363,6 +356,16 @@ struct DMask {
     int32_t i;  // word index, -1 before the first load
 };
 typedef uint32_t u32x3a __attribute__((ext_vector_type(3), aligned(4)));
+// The 12-byte index record of a lane in a delta-coded window, aligned to 4 bytes
+// only: loaded through its own type, since deducing load_res's parameter type would
+// drop that alignment.
+template <int CA>
+__device__ __forceinline__ u32x3a load_rec12(const u32x3a* p) {
+    if constexpr (CA == kCacheAll)
+        return *p;
+    else
+        return __builtin_nontemporal_load(p);
+}
 
 // Data loads of the window block at b (a multiple of kWin): lane l's values from
 // the two halves of the block (val_slot order), its indices in entry order (or,
@@ -395,7 +398,7 @@ __device__ __forceinline__ void load_data(const PassArgs<V>& a, int32_t b, bool 
             // 12 bytes per lane: the window's indices take its first 768 bytes.
             const u32x3a* rp = reinterpret_cast<const u32x3a*>(static_cast<const uint32_t*>(a.idx) +
                                                               b / 2 + 3 * (int)(lo / kE));
-            const u32x3a r = load_res<CA>(rp);
+            const u32x3a r = load_rec12<CA>(rp);
             w.c0.x = r.x;
             w.c0.y = r.y;
             w.c0.z = r.z;
