@@ -3,8 +3,9 @@ oracle: row lengths from one to the column count, empty rows and columns, every
 gather mode with forced tile and hot widths, workgroup counts from 1 to 64, segment
 weights, both index codings, the cache policies a copy allows, forced splits of the
 item-major copy, float and double, lambda from 0.01 to 1.  Each case: W and H
-after one outer iteration, the training RMSE after a second, bitwise agreement of
-the two residual copies."""
+after one outer iteration, the training RMSE after a second, then, from the oracle's
+factors, W and H after an outer iteration of element-wise CCD on the same handle,
+and bitwise agreement of the two residual copies throughout."""
 import numpy as np
 import pytest
 
@@ -87,6 +88,24 @@ def test_random_layout(seed):
     o.run(1, inner)
     if row.size:
         assert abs(g.train_rmse() - o.train_rmse()) <= (1e-9 if prec else 1e-4)
+    assert g.check_consistency() == 0
+    # Then one outer iteration of element-wise CCD (Algorithm 2) on the same copies,
+    # both sides starting from the oracle's factors (in the handle's precision).
+    Ws, Hs = o.factors()
+    o.close()
+    if not prec:
+        Ws, Hs = Ws.astype(np.float32), Hs.astype(np.float32)
+        g.set_factors(Ws, Hs)
+    else:
+        g.set_factors_f64(Ws, Hs)
+    o = Oracle(m, n, k, lam, row, col, val, Hs, W0=Ws)
+    g.ccd_run(1)
+    o.ccd_run(1)
+    W, H = g.factors_f64() if prec else g.factors()
+    Wo, Ho = o.factors()
+    ew, eh = colscaled_max_rel_err(W, Wo), colscaled_max_rel_err(H, Ho)
+    print(f"  element-wise CCD: W err {ew:.2e}  H err {eh:.2e}", flush=True)
+    assert ew <= tol and eh <= tol
     assert g.check_consistency() == 0
     g.close()
     o.close()
