@@ -145,3 +145,23 @@ def test_create_reports_the_first_bad_triplet():
     with pytest.raises(C.CCDPPError) as ei:
         C.ccdpp_create_ex(97, 89, 2, 0.1, row, col, val, 0, None)
     assert "val[190000] is not finite" in str(ei.value)
+
+
+def test_every_handle_call_answers_estate_on_a_null_handle():
+    """Every exported call that takes a handle refuses a NULL one with ESTATE before
+    touching any other argument (destroy accepts NULL)."""
+    L = _lib_or_skip()
+    skip = {"ccdpp_create", "ccdpp_create_ex", "ccdpp_destroy", "ccdpp_last_error",
+            "ccdpp_debug_inject"}
+    checked = 0
+    for name in C.declared_symbols():
+        if name in skip:
+            continue
+        fn = getattr(L, name)
+        args = []
+        for t in fn.argtypes:
+            args.append(None if t in (ctypes.c_void_p,) or hasattr(t, "contents") or
+                        t is ctypes.c_char_p else t(0))
+        assert fn(*args) == C.CCDPP_ESTATE, name
+        checked += 1
+    assert checked >= 18
