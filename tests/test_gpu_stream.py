@@ -1,6 +1,7 @@
 """The stream a handle works on: the device's null stream by default (the device
 build included), a caller's stream after ccdpp_set_stream, and back.  The results
-do not depend on it, bit for bit, and each call still returns with its work done."""
+do not depend on it, bit for bit, and each call still returns with its work done;
+two handles driven by two host threads at once give what each gives alone."""
 import numpy as np
 import pytest
 
@@ -64,3 +65,40 @@ def test_torch_current_stream():
     g.close()
     Wr, Hr, _ = _run(row, col, val, H0, [None, None])
     assert np.array_equal(W, Wr) and np.array_equal(H, Hr)
+
+
+def test_two_handles_in_two_threads():
+    """Two handles, each created and run by its own host thread on its own stream, at
+    the same time: each gives bitwise what it gives alone."""
+    import threading
+
+    import torch
+
+    probs = [_problem(), synth.small_random(1500, 900, 40_000, K, seed=78)]
+    shapes = [(M, N), (1500, 900)]
+
+    def job(i, out):
+        row, col, val, H0 = probs[i]
+        m, n = shapes[i]
+        s = torch.cuda.Stream()
+        g = CCDPP(m, n, K, LAM, row, col, val)
+        g.set_stream(s.cuda_stream)
+        g.set_factors(np.zeros((m, K), np.float32), H0)
+        g.run(3, 3)
+        out[i] = g.factors() + (g.train_rmse(),)
+        g.close()
+
+    alone = {}
+    for i in range(2):
+        job(i, alone)
+    together = {}
+    threads = [threading.Thread(target=job, args=(i, together)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert set(together) == {0, 1}
+    for i in range(2):
+        assert np.array_equal(alone[i][0], together[i][0])
+        assert np.array_equal(alone[i][1], together[i][1])
+        assert alone[i][2] == together[i][2]
