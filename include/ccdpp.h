@@ -102,7 +102,8 @@ int ccdpp_create(int64_t m, int64_t n, int32_t k, double lambda, int64_t nnz,
  *                 rounded down to a multiple of 64 (0: that maximum); each
  *                 pass stages as much of it as its vectors leave room for
  *   workgroups  : persistent workgroups per pass (0: two per compute unit,
- *                 one for copies of fewer than about 33.5M entries)
+ *                 one for copies of fewer than about 33.5M entries, four for
+ *                 copies of more than about 252M, padding included)
  *   seg_weight  : work of one row segment, in entries, when the entries are
  *                 shared out among workgroups and waves (0: the default, 4;
  *                 -1: shares by entries alone)

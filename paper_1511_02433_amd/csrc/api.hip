@@ -486,13 +486,17 @@ int build_layout(ccdpp* h, int side, Layout& L, int64_t rows, int64_t cols, cons
     // workgroup holds a whole CU's LDS, so the second round of workgroups goes to
     // whichever CUs finish first, which evens out the remaining differences in speed
     // between shares.  Smaller layouts take one share per compute unit, which halves
-    // the per-workgroup staging and start-up.
+    // the per-workgroup staging and start-up; very long ones four, whose shorter last
+    // round leaves less of the pass's end to the slowest shares (measured on MI355X:
+    // 252.8M ratings, user-major passes 2-3% faster; with 100M ratings four rounds were
+    // slower, the staging then weighing more).
     int64_t G;
     if (opt && opt->workgroups > 0) {
         G = opt->workgroups;
     } else {
-        const int64_t two = 2 * (int64_t)h->cus;
-        G = NP >= two * kWaves * kWin * 8 ? two : (int64_t)h->cus;
+        const int64_t cus = h->cus;
+        const int64_t per_wave = NP / (cus * kWaves * kWin);  // windows per wave, one round
+        G = per_wave >= 120 ? 4 * cus : per_wave >= 16 ? 2 * cus : cus;
         G = std::max<int64_t>(1, std::min<int64_t>(G, (NP + kWaves * kWin - 1) / (kWaves * kWin)));
     }
     const int64_t wseg = !opt || opt->seg_weight == 0 ? kSegWeight
