@@ -93,7 +93,7 @@ def test_layout_strategies(name):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("name", ["medium", "large"])
+@pytest.mark.parametrize("name", ["medium", "large", "vlarge"])
 def test_full_size(name):
     ds = synth.load(name)
     w = ds.workload
