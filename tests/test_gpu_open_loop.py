@@ -88,6 +88,27 @@ def test_medium_until_converged():
     _compare(hg, ho)
 
 
+@pytest.mark.timeout(600)
+def test_large_until_converged():
+    """The full-size workload with its held-out set: the oracle runs the whole schedule
+    once (its first iterations are those of any stopping run); the GPU stops where that
+    history says a rule well inside a gap of the decreases stops."""
+    ds = synth.load("large")
+    w = ds.workload
+    test = (ds.test_row, ds.test_col, ds.test_val)
+    print(f"case: large open loop {w.m} x {w.n}, nnz {w.nnz}", flush=True)
+    g, o = _pair(ds, w.k)
+    do, ho = o.run_until(w.outer, w.inner, -1.0, test)
+    assert do == w.outer
+    tol, expect = _robust_tol(ho[:, 0])
+    assert tol is not None
+    dg, hg = g.run_until(w.outer, w.inner, tol, test)
+    print(f"tol {tol:.3e}: gpu stops after {dg}, expected {expect}; "
+          f"test RMSE {hg[-1, 2]:.6f} vs {ho[dg - 1, 2]:.6f}")
+    assert dg == expect
+    _compare(hg, ho[:dg])
+
+
 def test_argument_checks():
     ds = synth.load("tiny")
     w = ds.workload
